@@ -1,0 +1,98 @@
+"""Workload descriptions: UNet topologies, the noise schedule and the selector table.
+
+Everything here is an *input* to the cache-hit path: the network shape a
+deployment chooses, the diffusion schedule constants handed to the sampler,
+and the similarity -> K table the cache selector is configured with.
+
+Topology rule (shared by all three shapes, latent-diffusion UNet of Sec. 2.1):
+  conv_in -> for each level l: n_res ResBlocks (each followed by a transformer
+  of depth[l] when depth[l] > 0), then a stride-2 conv except at the last level
+  -> middle Res / Transformer(mid_depth) / Res -> for each level from the last:
+  n_res+1 ResBlocks on [h, skip] concatenations (+ transformer), nearest x2
+  upsample + conv except at level 0 -> GroupNorm, SiLU, conv_out.
+"""
+
+# Tiny shape: 4x16x16 latent, two levels of 32/64 channels, one ResBlock per
+# level, GroupNorm with 8 groups, 4-head transformers at level 1 with an
+# 8-token x 64 context.
+UNET_TINY = dict(
+    name="tiny", in_ch=4, out_ch=4, H=16, W=16,
+    ch=(32, 64), depth=(0, 1), mid_depth=1, n_res=1,
+    n_heads=4, head_dim=0, gn_groups=8,
+    ctx_len=8, ctx_dim=64, pooled_dim=0,
+    gn_eps=1e-5, ln_eps=1e-5,
+)
+
+# Stable-Diffusion-1.5-shaped: 4x64x64 latent, 320/640/1280/1280 channels,
+# two ResBlocks per level, 8 heads (head_dim = C/8), 77x768 context.
+UNET_SD15 = dict(
+    name="sd15", in_ch=4, out_ch=4, H=64, W=64,
+    ch=(320, 640, 1280, 1280), depth=(1, 1, 1, 0), mid_depth=1, n_res=2,
+    n_heads=8, head_dim=0, gn_groups=32,
+    ctx_len=77, ctx_dim=768, pooled_dim=0,
+    gn_eps=1e-5, ln_eps=1e-5,
+)
+
+# SDXL-shaped: 4x128x128 latent, 320/640/1280 channels, transformer depth
+# 0/2/10, head_dim 64, 77x2048 context and a 1280-d pooled vector added to the
+# time embedding.
+UNET_SDXL = dict(
+    name="sdxl", in_ch=4, out_ch=4, H=128, W=128,
+    ch=(320, 640, 1280), depth=(0, 2, 10), mid_depth=10, n_res=2,
+    n_heads=0, head_dim=64, gn_groups=32,
+    ctx_len=77, ctx_dim=2048, pooled_dim=1280,
+    gn_eps=1e-5, ln_eps=1e-5,
+)
+
+_UNETS = {"tiny": UNET_TINY, "sd15": UNET_SD15, "sdxl": UNET_SDXL}
+
+
+def unet_config(name, **overrides):
+    """Return a copy of a named topology with optional field overrides."""
+    cfg = dict(_UNETS[name])
+    cfg.update(overrides)
+    return cfg
+
+
+# Diffusion schedule handed to the sampler: T training steps and the scaled-
+# linear beta range of latent diffusion models (Sec. 2.1, DDIM sampler of Sec. 6).
+SCHEDULE_SD = dict(T=1000, beta_start=0.00085, beta_end=0.012)
+
+# Similarity -> K table of the cache selector (Sec. 5.3.1): strictly
+# descending thresholds, each paired with the number of skipped steps.
+THRESHOLDS_PAPER = ((0.95, 25), (0.90, 20), (0.85, 15), (0.75, 10), (0.65, 5))
+
+# Tiny workload (N = 20, K in {0, 5, 10}): two thresholds at about the same
+# K/N fractions as the paper's table.
+THRESHOLDS_TINY = ((0.90, 10), (0.75, 5))
+
+
+# Workload recipes.  Sizes follow the paper's shapes: 768-d prompt embeddings,
+# N = 50 DDIM steps, K in {5, 10, 15, 20, 25}.
+WORKLOADS = {
+    "tiny": dict(
+        unet="tiny", n_cache=1024, d=64, cache_dtype="f32", clusters=16, sigma=0.1,
+        cache_seed=1, query_seed=2, query_sims=(0.99, 0.93, 0.85, 0.78, 0.70, 0.60),
+        n_cluster_queries=2, N=20, guidance=7.5, thresholds=THRESHOLDS_TINY,
+        weight_seed=0, batch=1,
+    ),
+    "sd15_b1": dict(
+        unet="sd15", n_cache=100_000, d=768, cache_dtype="bf16", clusters=1000, sigma=0.05,
+        cache_seed=11, query_seed=12, query_sims=(0.97,), n_cluster_queries=0,
+        N=50, guidance=7.5, thresholds=THRESHOLDS_PAPER, weight_seed=0, batch=1,
+        cond_seed=3, uncond_seed=4, k_sweep=(5, 10, 15, 20, 25),
+    ),
+    "sd15_b8_mixed": dict(
+        unet="sd15", n_cache=1_000_000, d=768, cache_dtype="bf16", clusters=1000, sigma=0.05,
+        cache_seed=21, query_seed=22, N=50, guidance=7.5, thresholds=THRESHOLDS_PAPER,
+        weight_seed=0, batch=8, k_seed=5, cond_seed=3, uncond_seed=4,
+    ),
+    "sdxl_b2": dict(
+        unet="sdxl", N=50, guidance=7.5, weight_seed=0, batch=2, k_sweep=(10, 20),
+        cond_seed=3, uncond_seed=4, pooled_seed=6,
+    ),
+    "retrieval_heavy": dict(
+        n_cache=10_000_000, d=768, cache_dtype="bf16", clusters=10_000, sigma=0.05,
+        cache_seed=31, query_seed=32, n_queries=256, thresholds=THRESHOLDS_PAPER,
+    ),
+}

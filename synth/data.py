@@ -1,0 +1,108 @@
+"""Seeded synthetic data: cache embeddings, queries, contexts and latents.
+
+Stand-ins for CLIP prompt embeddings (768-d unit vectors, cosine similarity)
+and for the prompt stream: no dataset item is reproduced.
+
+Cluster recipe: centres mu_c uniform on the unit sphere; a member is
+normalize(mu_c + sigma * g) with g ~ N(0, I_d) (sigma per coordinate).
+Rows are generated in fixed chunks of CHUNK rows, each from its own PCG64
+stream, so a row's value depends only on (seed, row index).
+"""
+import numpy as np
+
+CHUNK = 65536
+
+
+def to_bf16_bits(x):
+    """float32 -> uint16 bfloat16 bit patterns, round to nearest even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def from_bf16_bits(b):
+    """uint16 bfloat16 bit patterns -> float32 (exact)."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+def cluster_centres(clusters, d, seed):
+    rng = np.random.default_rng([seed, 0])
+    mu = rng.standard_normal((clusters, d))
+    mu /= np.linalg.norm(mu, axis=1, keepdims=True)
+    return mu.astype(np.float32)
+
+
+def _chunk_rows(mu, sigma, seed, chunk_index, rows):
+    rng = np.random.default_rng([seed, 1, chunk_index])
+    cid = rng.integers(0, mu.shape[0], size=rows)
+    x = mu[cid] + np.float32(sigma) * rng.standard_normal((rows, mu.shape[1]), dtype=np.float32)
+    nrm = np.sqrt(np.einsum("ij,ij->i", x.astype(np.float64), x.astype(np.float64)))
+    return (x / nrm[:, None]).astype(np.float32)
+
+
+def make_cache(n, d, clusters, sigma, seed, dtype="bf16", dup_pairs=()):
+    """Cache of n unit-norm embeddings.
+
+    dtype "f32" -> float32 [n][d]; "bf16" -> uint16 bit patterns [n][d].
+    dup_pairs: (i, j) pairs; row j is overwritten with an exact copy of row i.
+    """
+    mu = cluster_centres(clusters, d, seed)
+    out = np.empty((n, d), dtype=np.float32 if dtype == "f32" else np.uint16)
+    for c, start in enumerate(range(0, n, CHUNK)):
+        rows = min(CHUNK, n - start)
+        x = _chunk_rows(mu, sigma, seed, c, rows)
+        out[start:start + rows] = x if dtype == "f32" else to_bf16_bits(x)
+    for i, j in dup_pairs:
+        out[j] = out[i]
+    return out
+
+
+def cache_rows_f32(cache, rows):
+    rows = np.asarray(rows)
+    sel = cache[rows]
+    return sel.astype(np.float32) if sel.dtype == np.float32 else from_bf16_bits(sel)
+
+
+def make_queries_at_sims(targets, sims, seed):
+    """q = s * t_hat + sqrt(1 - s^2) * u, u a random unit vector orthogonal to t_hat.
+
+    targets: float32 [m][d]; sims: length m.  Returns float32 [m][d] unit vectors whose
+    cosine with the matching target is s (up to float32 rounding).
+    """
+    rng = np.random.default_rng([seed, 2])
+    t = np.asarray(targets, dtype=np.float64)
+    t = t / np.linalg.norm(t, axis=1, keepdims=True)
+    g = rng.standard_normal(t.shape)
+    g -= np.einsum("ij,ij->i", g, t)[:, None] * t
+    g /= np.linalg.norm(g, axis=1, keepdims=True)
+    s = np.asarray(sims, dtype=np.float64)[:, None]
+    return (s * t + np.sqrt(1.0 - s * s) * g).astype(np.float32)
+
+
+def make_cluster_queries(m, d, clusters, sigma, cache_seed, seed):
+    """Fresh draws from the cache's cluster process (new prompts of a popular theme)."""
+    mu = cluster_centres(clusters, d, cache_seed)
+    rng = np.random.default_rng([seed, 3])
+    cid = rng.integers(0, clusters, size=m)
+    x = mu[cid].astype(np.float64) + sigma * rng.standard_normal((m, d))
+    return (x / np.linalg.norm(x, axis=1, keepdims=True)).astype(np.float32)
+
+
+def make_contexts(b, length, dim, seed):
+    """Text-encoder output stand-in: N(0, 1), rounded to bfloat16 values (float32 array)."""
+    rng = np.random.default_rng([seed, 4])
+    x = rng.standard_normal((b, length, dim), dtype=np.float32)
+    return from_bf16_bits(to_bf16_bits(x)).reshape(b, length, dim)
+
+
+def make_latents(b, c, h, w, seed):
+    """x_N ~ N(0, I) in float32 [b][c][h][w]."""
+    rng = np.random.default_rng([seed, 5])
+    return rng.standard_normal((b, c, h, w), dtype=np.float32)
+
+
+def make_k_values(b, choices, seed):
+    rng = np.random.default_rng([seed, 6])
+    return rng.choice(np.asarray(choices, dtype=np.int32), size=b)
