@@ -1,0 +1,201 @@
+/*
+ * nv.h -- C ABI of the approximate-caching cache-hit generation path on MI355X.
+ *
+ * Method (Agarwal et al., "Approximate Caching for Efficiently Serving
+ * Diffusion Models"): a request's prompt embedding is matched against the
+ * cached prompt embeddings (Sec. 4.3, Alg. 1); the best cosine similarity is
+ * mapped to a skip count K by the cache selector (Sec. 5.3.1); the matched
+ * entry's intermediate latent after K denoising steps is fetched
+ * (Sec. 5.3, storage) and the remaining N - K guided DDIM steps of the
+ * latent-diffusion UNet are run for the new prompt (Sec. 4.1, Sec. 2.1, Sec. 6).
+ *
+ * Conventions shared by every entry point:
+ *   - Every tensor pointer is a DEVICE pointer unless its comment says "host".
+ *     The caller owns all buffers; the library never frees caller memory.
+ *     Only nv_unet_create allocates (weights), released by nv_unet_destroy.
+ *   - Work is enqueued on `stream` (a hipStream_t, NULL = default stream) and
+ *     is asynchronous unless stated.  Host arrays are read before return.
+ *   - Validation failures return synchronously before any launch and leave
+ *     outputs untouched.  nv_last_error() gives a message for the last
+ *     failing call on the calling thread.
+ *   - Handles are not thread-safe: concurrent calls on one nv_unet, or calls
+ *     sharing a workspace, race.
+ */
+#ifndef NV_H
+#define NV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NV_OK = 0,
+  NV_ERR_INVALID_ARG = -1,   /* null pointer, bad size, bad table, K out of range */
+  NV_ERR_UNSUPPORTED = -2,   /* legal but not implemented (e.g. d % 8 != 0) */
+  NV_ERR_OUT_OF_MEMORY = -3, /* device allocation failed (nv_unet_create only) */
+  NV_ERR_HIP = -4,           /* a HIP runtime call or kernel launch failed */
+  NV_ERR_WORKSPACE = -5      /* workspace pointer null or smaller than required */
+} nv_status;
+
+typedef enum { NV_F32 = 0, NV_BF16 = 1 } nv_dtype;
+
+/* Text for a status code.  Never NULL. */
+const char* nv_status_string(int32_t status);
+/* Detail of the last error on this thread ("" if none).  Never NULL. */
+const char* nv_last_error(void);
+/* Library version string. */
+const char* nv_version(void);
+
+/* ------------------------------------------------------------------------ *
+ * Cache lookup + cache selector (Sec. 4.3 Alg. 1 search and K choice;
+ * Sec. 5.3.1 selector table).
+ *
+ * For each query q_j (float32 [m][d], row-major) and cache row c_i
+ * ([n][d] row-major, float32 or bfloat16), the canonical similarity is the
+ * float64 sum of (double)q_jk * (double)c_ik over k = 0..d-1 taken strictly
+ * left to right (every product is exact in float64).  The result is
+ *   idx_out[j] = lowest i with the maximal canonical similarity,
+ *   sim_out[j] = that similarity rounded to float32 (nearest even),
+ *   k_out[j]   = k_values[t] for the first t with sim_out[j] > thresholds[t]
+ *                (float32 compare, strict), or 0 when none does.
+ * These outputs are exact, not approximate: a reduced-precision scan (bf16
+ * matrix cores) keeps every row within a proven error margin of the best
+ * and only those rows are rescored canonically.
+ * n == 0 is legal: idx = -1, sim = -inf, K = 0 (the "no suitable cache" branch).
+ *
+ * Arguments: queries device f32 [m][d]; cache device [n][d] of c_dtype;
+ * thresholds/k_values HOST arrays of length J (1..16), thresholds finite and
+ * strictly descending, k_values >= 0; idx_out device int64 [m], sim_out
+ * device f32 [m], k_out device int32 [m].  Limits: 1 <= m <= 4096,
+ * 0 <= n < 2^31, 1 <= d <= 4096; d % 8 != 0 or d > 2048 gives NV_ERR_UNSUPPORTED.
+ * workspace: device, >= nv_cache_lookup_workspace(m, n, d) bytes, 256-byte
+ * aligned, contents need not be initialised.
+ * ------------------------------------------------------------------------ */
+size_t nv_cache_lookup_workspace(int32_t m, int64_t n, int32_t d);
+int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache, int32_t c_dtype,
+                        int64_t n, int32_t d, const float* thresholds, const int32_t* k_values,
+                        int32_t J, int64_t* idx_out, float* sim_out, int32_t* k_out,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ *
+ * State fetch (Sec. 5.3 storage; Alg. 1 retrieval of the state after step K).
+ *
+ * store: device f32 [n_store][n_slots][latent_elems]; slot s holds the
+ * state after slot_k[s] steps (slot_k HOST int32 [n_slots], each > 0).
+ * payload: device int32 [n_rows] mapping a cache row to its store entry
+ * (NULL = identity, n_store >= n_rows).  idx, k: device [B] (lookup outputs).
+ * noise: device f32 [B][latent_elems], used for samples with K = 0.
+ * out[b] = store[payload[idx[b]]][slot of k[b]] when k[b] > 0, else noise[b].
+ * A sample whose K has no slot, or whose idx/payload is out of range, gets
+ * noise[b] and its k is rewritten to 0 in k (device, in place), so the
+ * caller's later nv_denoise runs it from scratch.
+ * ------------------------------------------------------------------------ */
+int32_t nv_gather_states(const float* store, int64_t n_store, int32_t n_slots,
+                         const int32_t* slot_k, const int32_t* payload, int64_t n_rows,
+                         const int64_t* idx, int32_t* k, const float* noise, int32_t B,
+                         int64_t latent_elems, float* out, void* stream);
+
+/* ------------------------------------------------------------------------ *
+ * Latent-diffusion UNet (Sec. 2.1: UNet backbone, text conditioning through
+ * cross-attention, operating on latents).  Topology rule:
+ *   conv_in; per level l: n_res ResBlocks (+ transformer of depth[l] if > 0),
+ *   stride-2 conv except at the last level; middle Res / Transformer
+ *   (mid_depth, skipped if 0) / Res; per level from the last: n_res + 1
+ *   ResBlocks on [h, skip] channel concatenations (+ transformer), nearest x2
+ *   upsample + conv except at level 0; GroupNorm, SiLU, conv_out.
+ *   Time embedding: [cos(t f_k), sin(t f_k)], f_k = exp(-ln(1e4) k / (ch0/2)),
+ *   Linear(ch0, 4 ch0), SiLU, Linear(4 ch0, 4 ch0), + pooled (pooled_dim
+ *   must then equal 4 ch0).  Heads: n_heads if > 0, else C / head_dim.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t in_ch, out_ch;  /* latent channels (4, 4) */
+  int32_t H, W;           /* latent size, divisible by 2^(n_levels-1) */
+  int32_t n_levels;       /* 1..4 */
+  int32_t ch[4];          /* channels per level, multiples of 32 and of gn_groups */
+  int32_t depth[4];       /* transformer depth per level (0 = none) */
+  int32_t mid_depth;      /* transformer depth of the middle block */
+  int32_t n_res;          /* ResBlocks per down level (n_res + 1 per up level) */
+  int32_t n_heads;        /* > 0: fixed head count */
+  int32_t head_dim;       /* used when n_heads == 0 */
+  int32_t gn_groups;      /* GroupNorm groups */
+  int32_t ctx_len, ctx_dim; /* conditioning tokens and their width */
+  int32_t pooled_dim;     /* 0, or 4*ch[0]: pooled vector added to the time embedding */
+  float gn_eps, ln_eps;
+} nv_unet_config;
+
+typedef struct nv_unet nv_unet;
+
+/* Number of float weights of a topology (-1 if the config is invalid). */
+int64_t nv_unet_param_count(const nv_unet_config* cfg);
+
+/* Name and element count of parameter i (0-based) in canonical order;
+ * name is NUL-terminated and truncated to name_len bytes. */
+int32_t nv_unet_param_info(const nv_unet_config* cfg, int64_t i, char* name, int32_t name_len,
+                           int64_t* numel);
+
+/* weights_host: HOST float32 array of nv_unet_param_count(cfg) values, the
+ * tensors concatenated in canonical order (conv weights [Cout][Cin][3][3],
+ * linear [out][in], row-major):
+ *   time.l1.{w,b} time.l2.{w,b} conv_in.{w,b}
+ *   per down level, per ResBlock: res, then transformer if depth > 0;
+ *     then ds.{w,b} unless last level
+ *   mid.res0, mid.attn (if mid_depth > 0), mid.res1
+ *   per up level from the last, per ResBlock (n_res + 1): res, transformer;
+ *     then us.{w,b} unless level 0
+ *   out.gn.{g,b} conv_out.{w,b}
+ * res(cin, cout) = gn1.{g,b} conv1.{w,b} temb.{w,b} gn2.{g,b} conv2.{w,b}
+ *   [skip.{w,b} (linear [cout][cin]) when cin != cout]
+ * transformer(c, depth) = gn.{g,b} proj_in.{w,b}, per block:
+ *   ln1.{g,b} attn1.q.w attn1.k.w attn1.v.w attn1.o.{w,b} ln2.{g,b}
+ *   attn2.q.w attn2.k.w ([c][ctx_dim]) attn2.v.w attn2.o.{w,b} ln3.{g,b}
+ *   ff1.{w,b} ([8c][c], output [a | g]) ff2.{w,b} ([c][4c]); then proj_out.{w,b}.
+ * Matrices are converted to float16 on the device (exact for bfloat16-valued
+ * weights of magnitude in [2^-17, 65504]); norms and biases stay float32.
+ * The model computes with float16 matrix-core operands, float32 accumulation
+ * and float32 statistics.  *out receives the handle. */
+int32_t nv_unet_create(const nv_unet_config* cfg, const float* weights_host, int64_t n_weights,
+                       nv_unet** out);
+void nv_unet_destroy(nv_unet* net);
+
+/* DDIM schedule: T training steps (T % N == 0), scaled-linear betas
+ * beta_t = (sqrt(beta_start) + (sqrt(beta_end) - sqrt(beta_start)) t/(T-1))^2,
+ * abar_t = prod_{s<=t}(1 - beta_s); grid t_i = (N-1-i) T/N + 1; step i goes
+ * t_i -> t_{i+1}, the last step to abar_0.  Deterministic (eta = 0). */
+typedef struct {
+  int32_t T, N;
+  float beta_start, beta_end;
+} nv_schedule;
+
+/* Device workspace needed by nv_denoise / nv_unet_eps for B samples (2B rows). */
+size_t nv_denoise_workspace(const nv_unet* net, int32_t B);
+
+/* Resume B samples from their cached states (Sec. 4.1): sample b holds, in
+ * latent (device f32 [B][in_ch][H][W]), the state after k[b] steps, and
+ * runs steps k[b] .. N-1; on return latent holds x_0 for every sample.
+ * k: HOST int32 [B], 0 <= k[b] <= N (k[b] == N: returned unchanged; k[b] == 0:
+ * full generation from x_N).  cond, uncond: device f32 [B][ctx_len][ctx_dim]
+ * (the prompt's and the empty prompt's encodings).  pooled: device f32
+ * [B][pooled_dim], or NULL when pooled_dim == 0 (applied to both rows).
+ * Each step evaluates the UNet on 2 rows per sample (uncond, cond), combines
+ * eps = eps_u + guidance (eps_c - eps_u) and applies the DDIM update.
+ * Samples with different k run together: at iteration j sample b is at
+ * step k[b] + j and leaves the batch after step N-1.  1 <= B <= 64. */
+int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent, const int32_t* k,
+                   int32_t B, const float* cond, const float* uncond, const float* pooled,
+                   float guidance, void* workspace, size_t workspace_bytes, void* stream);
+
+/* One UNet evaluation per row for teacher-forced checks: sample b at step
+ * index step_idx[b] (HOST int32 [B], 0 <= step_idx < N, timestep t_i of the
+ * grid) gives eps_uncond[b], eps_cond[b] (device f32 [B][out_ch][H][W]). */
+int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const float* x,
+                    const int32_t* step_idx, int32_t B, const float* cond, const float* uncond,
+                    const float* pooled, float* eps_uncond, float* eps_cond, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NV_H */

@@ -1,0 +1,15 @@
+"""MI355X-native cache-hit generation path of approximate caching for diffusion serving.
+
+Entry points (same names as the C ABI in include/nv.h):
+  nv_cache_lookup   exact cosine top-1 over the cached prompt embeddings + cache selector
+  nv_gather_states  fetch the matched entry's intermediate latent at the chosen K
+  NvUNet            device-resident latent-diffusion UNet; .nv_denoise runs the
+                    remaining N - K guided DDIM steps, .nv_unet_eps one evaluation
+
+Importing the package loads libnv.so and fails if it has not been built.
+"""
+from .api import (NvUNet, nv_cache_lookup, nv_cache_lookup_workspace, nv_gather_states,
+                  nv_unet_param_count, nv_unet_param_info, workspace)
+
+__all__ = ["NvUNet", "nv_cache_lookup", "nv_cache_lookup_workspace", "nv_gather_states",
+           "nv_unet_param_count", "nv_unet_param_info", "workspace"]

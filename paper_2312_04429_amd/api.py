@@ -1,0 +1,169 @@
+"""Python entry points with the C ABI's names (argument marshalling only).
+
+Tensors are torch device tensors; outputs and workspaces are allocated with
+torch; every computation happens in libnv.so on the current HIP stream.
+"""
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import _native as N
+
+BF16_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _p(t):
+    return C.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("device tensor expected")
+
+
+def workspace(nbytes, device):
+    """A 256-byte aligned device byte buffer: (owner tensor, aligned address)."""
+    t = torch.empty(int(nbytes) + 256, dtype=torch.uint8, device=device)
+    addr = t.data_ptr()
+    return t, addr + (-addr) % 256
+
+
+def nv_cache_lookup_workspace(m, n, d):
+    return int(N.lib.nv_cache_lookup_workspace(m, n, d))
+
+
+def nv_cache_lookup(queries, cache, thresholds, k_values, ws=None):
+    """Exact cosine top-1 + cache selector.  Returns (idx int64, sim f32, K int32) on device."""
+    _need_cuda(queries, cache)
+    assert queries.dtype == torch.float32 and queries.is_contiguous()
+    assert cache.is_contiguous()
+    m, d = queries.shape
+    n = cache.shape[0]
+    if cache.dtype == torch.float32:
+        cdt = N.NV_F32
+    elif cache.dtype in BF16_DTYPES:
+        cdt = N.NV_BF16
+    else:
+        raise ValueError("cache must be float32 or bfloat16 (bits)")
+    thr = (C.c_float * len(thresholds))(*thresholds)
+    kv = (C.c_int32 * len(k_values))(*k_values)
+    dev = queries.device
+    idx = torch.empty(m, dtype=torch.int64, device=dev)
+    sim = torch.empty(m, dtype=torch.float32, device=dev)
+    kk = torch.empty(m, dtype=torch.int32, device=dev)
+    need = nv_cache_lookup_workspace(m, n, d)
+    if ws is None:
+        _own, addr = workspace(need, dev)
+        wbytes = need
+    else:
+        _own, addr, wbytes = ws
+    st = N.lib.nv_cache_lookup(_p(queries), m, _p(cache) if n > 0 else None, cdt, n, d, thr, kv,
+                               len(thresholds), _p(idx), _p(sim), _p(kk), C.c_void_p(addr),
+                               wbytes, _stream())
+    N.check(st, "nv_cache_lookup")
+    return idx, sim, kk
+
+
+def nv_gather_states(store, slot_k, payload, n_rows, idx, k, noise, out=None):
+    """store [n_store][n_slots][*latent] f32; returns out [B][*latent]; k rewritten in place."""
+    _need_cuda(store, idx, k, noise)
+    B = idx.shape[0]
+    lat = int(np.prod(noise.shape[1:]))
+    if out is None:
+        out = torch.empty_like(noise)
+    sk = (C.c_int32 * len(slot_k))(*slot_k)
+    st = N.lib.nv_gather_states(_p(store), store.shape[0], len(slot_k), sk, _p(payload), n_rows,
+                                _p(idx), _p(k), _p(noise), B, lat, _p(out), _stream())
+    N.check(st, "nv_gather_states")
+    return out
+
+
+def nv_unet_param_count(cfg):
+    c = N.make_config(cfg)
+    return int(N.lib.nv_unet_param_count(C.byref(c)))
+
+
+def nv_unet_param_info(cfg, i):
+    c = N.make_config(cfg)
+    buf = C.create_string_buffer(256)
+    n = C.c_int64()
+    N.check(N.lib.nv_unet_param_info(C.byref(c), i, buf, 256, C.byref(n)), "nv_unet_param_info")
+    return buf.value.decode(), int(n.value)
+
+
+class NvUNet:
+    """Handle of a device-resident UNet (nv_unet_create / nv_unet_destroy)."""
+
+    def __init__(self, cfg, weights):
+        self.cfg = dict(cfg)
+        self._c = N.make_config(cfg)
+        if isinstance(weights, dict):
+            flat = np.concatenate([np.ascontiguousarray(v, dtype=np.float32).ravel()
+                                   for v in weights.values()])
+        else:
+            flat = np.ascontiguousarray(weights, dtype=np.float32).ravel()
+        h = C.c_void_p()
+        st = N.lib.nv_unet_create(C.byref(self._c), flat.ctypes.data_as(C.c_void_p), flat.size,
+                                  C.byref(h))
+        N.check(st, "nv_unet_create")
+        self._h = h
+        self._ws = {}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            N.lib.nv_unet_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_bytes(self, B):
+        n = int(N.lib.nv_denoise_workspace(self._h, B))
+        if n == 0:
+            raise N.NvError(N.NV_ERR_INVALID_ARG, "nv_denoise_workspace")
+        return n
+
+    def _workspace(self, B, device):
+        if B not in self._ws:
+            need = self.workspace_bytes(B)
+            own, addr = workspace(need, device)
+            self._ws[B] = (own, addr, need)
+        return self._ws[B]
+
+    def nv_denoise(self, latent, k, cond, uncond, pooled=None, guidance=7.5,
+                   sched=(1000, 50, 0.00085, 0.012)):
+        """In place: latent [B][C][H][W] f32 holds x_K per sample, returns x_0."""
+        _need_cuda(latent, cond, uncond, pooled)
+        B = latent.shape[0]
+        kk = (C.c_int32 * B)(*[int(v) for v in k])
+        s = N.make_schedule(*sched)
+        _own, addr, need = self._workspace(B, latent.device)
+        st = N.lib.nv_denoise(self._h, C.byref(s), _p(latent), kk, B, _p(cond), _p(uncond),
+                              _p(pooled), float(guidance), C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_denoise")
+        return latent
+
+    def nv_unet_eps(self, x, step_idx, cond, uncond, pooled=None,
+                    sched=(1000, 50, 0.00085, 0.012)):
+        """Per-row epsilon of one evaluation: (eps_uncond, eps_cond) [B][C][H][W] f32."""
+        _need_cuda(x, cond, uncond, pooled)
+        B = x.shape[0]
+        si = (C.c_int32 * B)(*[int(v) for v in step_idx])
+        s = N.make_schedule(*sched)
+        eu = torch.empty((B, self.cfg["out_ch"], self.cfg["H"], self.cfg["W"]),
+                         dtype=torch.float32, device=x.device)
+        ec = torch.empty_like(eu)
+        _own, addr, need = self._workspace(B, x.device)
+        st = N.lib.nv_unet_eps(self._h, C.byref(s), _p(x), si, B, _p(cond), _p(uncond),
+                               _p(pooled), _p(eu), _p(ec), C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_unet_eps")
+        return eu, ec

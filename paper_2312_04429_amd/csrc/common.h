@@ -1,0 +1,55 @@
+// Internal helpers shared by the library's HIP sources (not part of the ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+
+#include <cstdint>
+#include <string>
+
+#include "../../include/nv.h"
+
+namespace nv {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// Last-error message for the calling thread.
+void set_error(const std::string& msg);
+void clear_error();
+
+#define NV_CHECK_ARG(cond, msg)                 \
+  do {                                          \
+    if (!(cond)) {                              \
+      ::nv::set_error(msg);                     \
+      return NV_ERR_INVALID_ARG;                \
+    }                                           \
+  } while (0)
+
+#define NV_HIP_TRY(expr)                                                          \
+  do {                                                                            \
+    hipError_t e_ = (expr);                                                       \
+    if (e_ != hipSuccess) {                                                       \
+      ::nv::set_error(std::string(#expr) + ": " + hipGetErrorString(e_));         \
+      return NV_ERR_HIP;                                                          \
+    }                                                                             \
+  } while (0)
+
+// Check for launch errors after a kernel launch.
+#define NV_LAUNCH_CHECK(name)                                                     \
+  do {                                                                            \
+    hipError_t e_ = hipGetLastError();                                            \
+    if (e_ != hipSuccess) {                                                       \
+      ::nv::set_error(std::string("launch ") + name + ": " + hipGetErrorString(e_)); \
+      return NV_ERR_HIP;                                                          \
+    }                                                                             \
+  } while (0)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace nv

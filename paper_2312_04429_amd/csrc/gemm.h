@@ -1,0 +1,38 @@
+// Launch interface of the matrix-core GEMM / implicit-GEMM convolution.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace nv {
+
+struct GemmArgs {
+  int64_t M;                // output rows (tokens or output pixels)
+  int N, K;                 // output columns, reduction length
+  // A operand
+  const _Float16* src1;     // dense: [M][lda1]; conv: NHWC [rows][Hin][Win][C1]
+  const _Float16* src2;     // second concatenated source (C2 channels) or null
+  int C1, C2;               // dense: K split (C1 = K when no src2); conv: channels
+  int lda1, lda2;           // dense row strides (halfs)
+  int conv;                 // 0 dense, 1 conv 3x3
+  int Hin, Win, Ho, Wo, stride, upsample;
+  // B operand: weights [N][ldw], K contiguous
+  const _Float16* w;
+  int ldw;
+  // epilogue
+  const float* bias;        // [N] or null
+  const float* rowvec;      // [M / rows_div][ld_rowvec] or null
+  int64_t rows_div;
+  int ld_rowvec;
+  const _Float16* residual; // [M][ld_res] or null
+  int ld_res;
+  int silu;
+  int geglu;                // output N/2 columns
+  void* out;
+  int ldo;
+  int out_f32;
+};
+
+hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
+
+}  // namespace nv

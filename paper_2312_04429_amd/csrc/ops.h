@@ -1,0 +1,51 @@
+// Launch interface of the element-wise / normalisation / sampler kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace nv {
+
+constexpr int MAX_SAMPLES = 64;
+
+// Per-iteration sampler state passed by value: sample b (in the batch's
+// K-ascending order) is at grid step kstep[b] + j; perm maps that order back
+// to the caller's sample index.
+struct StepArgs {
+  int32_t kstep[MAX_SAMPLES];
+  int32_t perm[MAX_SAMPLES];
+  int32_t j;
+};
+
+struct GnArgs {
+  const _Float16* src1;  // [rows][HW][C1]
+  const _Float16* src2;  // [rows][HW][C2] (channel concat) or null
+  int C1, C2, HW, G;
+  float eps;
+  const float* gamma;
+  const float* beta;
+  int silu;
+  float* stats;          // [rows][G][2] (mean, rstd) scratch
+  _Float16* out;         // [rows][HW][C1 + C2]
+};
+
+hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s);
+hipError_t layernorm_launch(const _Float16* x, const float* g, const float* b, _Float16* out,
+                            int64_t tokens, int C, float eps, hipStream_t s);
+hipError_t schedule_launch(int T, int N, double b0, double b1, int32_t* ts, float* a_t,
+                           float* a_prev, hipStream_t s);
+hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int rows, _Float16* out,
+                           hipStream_t s);
+hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Cin, int H, int W,
+                          int C0, int rows, _Float16* out, hipStream_t s);
+hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C, int HW,
+                           int samples, float guidance, const float* a_t, const float* a_prev,
+                           hipStream_t s);
+hipError_t eps_split_launch(const float* eps, int C, int HW, int samples, float* eu, float* ec,
+                            hipStream_t s);
+hipError_t ctx_rows_launch(const StepArgs& st, const float* cond, const float* uncond,
+                           int64_t per_sample, int rows, _Float16* out, hipStream_t s);
+hipError_t permute_launch(const StepArgs& st, const float* src, float* dst, int64_t per_sample,
+                          int samples, int to_sorted, hipStream_t s);
+
+}  // namespace nv

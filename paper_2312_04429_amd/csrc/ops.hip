@@ -1,0 +1,335 @@
+// Element-wise, normalisation and sampler kernels of the UNet step:
+// GroupNorm (+SiLU), LayerNorm, the sinusoidal time embedding, conv_in on the
+// float32 latent, classifier-free guidance + DDIM update, the DDIM schedule
+// tables, and layout/permutation helpers.
+#include <cmath>
+
+#include "common.h"
+#include "ops.h"
+
+namespace nv {
+namespace {
+
+__device__ inline float silu(float x) { return x / (1.0f + __expf(-x)); }
+
+__device__ inline float block_sum_256(float v, float* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+__device__ inline float load_cat(const _Float16* s1, int C1, const _Float16* s2, int C2,
+                                 int64_t pix, int c) {
+  return c < C1 ? (float)s1[pix * C1 + c] : (float)s2[pix * C2 + (c - C1)];
+}
+
+// One workgroup per (row, group): two-pass mean / variance in float32.
+__global__ void __launch_bounds__(256) gn_stats_k(GnArgs a) {
+  __shared__ float red[4];
+  const int row = blockIdx.x / a.G, g = blockIdx.x % a.G;
+  const int C = a.C1 + a.C2, cg = C / a.G;
+  const int64_t cnt = (int64_t)a.HW * cg;
+  const int64_t pix0 = (int64_t)row * a.HW;
+  float s = 0.f;
+  for (int64_t e = threadIdx.x; e < cnt; e += 256) {
+    const int p = (int)(e / cg), c = g * cg + (int)(e % cg);
+    s += load_cat(a.src1, a.C1, a.src2, a.C2, pix0 + p, c);
+  }
+  const float mean = block_sum_256(s, red) / (float)cnt;
+  float v = 0.f;
+  for (int64_t e = threadIdx.x; e < cnt; e += 256) {
+    const int p = (int)(e / cg), c = g * cg + (int)(e % cg);
+    const float d = load_cat(a.src1, a.C1, a.src2, a.C2, pix0 + p, c) - mean;
+    v += d * d;
+  }
+  const float var = block_sum_256(v, red) / (float)cnt;
+  if (threadIdx.x == 0) {
+    a.stats[2 * blockIdx.x] = mean;
+    a.stats[2 * blockIdx.x + 1] = rsqrtf(var + a.eps);
+  }
+}
+
+// Normalise, affine, optional SiLU; 8 channels per thread; output [rows][HW][C].
+__global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int64_t total8) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total8) return;
+  const int C = a.C1 + a.C2, cg = C / a.G;
+  const int64_t e = i * 8;
+  const int64_t pix = e / C;
+  const int c0 = (int)(e - pix * C);
+  const int row = (int)(pix / a.HW);
+  half8 x = c0 < a.C1 ? *(const half8*)(a.src1 + pix * a.C1 + c0)
+                      : *(const half8*)(a.src2 + pix * a.C2 + (c0 - a.C1));
+  half8 y;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int c = c0 + j, g = c / cg;
+    const float mean = a.stats[2 * (row * a.G + g)], rstd = a.stats[2 * (row * a.G + g) + 1];
+    float v = ((float)x[j] - mean) * rstd * a.gamma[c] + a.beta[c];
+    if (a.silu) v = silu(v);
+    y[j] = (_Float16)v;
+  }
+  *(half8*)(a.out + e) = y;
+}
+
+// One wave per token; C <= 2048, C % 8 == 0.
+__global__ void __launch_bounds__(256) layernorm_k(const _Float16* __restrict__ x,
+                                                   const float* __restrict__ gamma,
+                                                   const float* __restrict__ beta,
+                                                   _Float16* __restrict__ out, int64_t tokens,
+                                                   int C, float eps) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= tokens) return;
+  const _Float16* xr = x + t * C;
+  const int nch = C / 8;
+  float v[4][8];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = lane + i * 64;
+    if (ch < nch) {
+      const half8 h = *(const half8*)(xr + ch * 8);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[i][j] = (float)h[j];
+        s += v[i][j];
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  const float mean = s / (float)C;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = lane + i * 64;
+    if (ch < nch) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float d = v[i][j] - mean;
+        q += d * d;
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  const float rstd = rsqrtf(q / (float)C + eps);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = lane + i * 64;
+    if (ch < nch) {
+      half8 y;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = ch * 8 + j;
+        y[j] = (_Float16)((v[i][j] - mean) * rstd * gamma[c] + beta[c]);
+      }
+      *(half8*)(out + t * C + ch * 8) = y;
+    }
+  }
+}
+
+// DDIM tables: abar_t accumulated in float64 and rounded to float32; for grid
+// step i: ts[i] = t_i = (N-1-i) T/N + 1, a_t[i] = abar(t_i), a_prev[i] =
+// abar(t_{i+1}) (abar_0 after the last step).  Requires T/N >= 2.
+__global__ void schedule_k(int T, int N, double b0, double b1, int32_t* ts, float* a_t,
+                           float* a_prev) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int stride = T / N;
+  const double r0 = sqrt(b0), r1 = sqrt(b1);
+  double acc = 1.0, abar0 = 1.0;
+  for (int t = 0; t < T; ++t) {
+    const double rb = r0 + (r1 - r0) * (double)t / (double)(T - 1);
+    acc *= 1.0 - rb * rb;
+    if (t == 0) abar0 = acc;
+    if (t >= 1 && (t - 1) % stride == 0) {
+      const int i = N - 1 - (t - 1) / stride;
+      if (i >= 0 && i < N) {
+        ts[i] = t;
+        a_t[i] = (float)acc;
+      }
+    }
+  }
+  for (int i = 0; i + 1 < N; ++i) a_prev[i] = a_t[i + 1];
+  a_prev[N - 1] = (float)abar0;
+}
+
+// Sinusoidal embedding [cos(t f_k), sin(t f_k)] of the timestep of each row.
+// Rows 2b, 2b+1 belong to sample b at grid step kstep[b] + j.
+__global__ void temb_sin_k(StepArgs st, const int32_t* __restrict__ ts, int C0, int rows,
+                           _Float16* __restrict__ out) {
+  const int r = blockIdx.x;
+  if (r >= rows) return;
+  const int b = r >> 1;
+  const float t = (float)ts[st.kstep[b] + st.j];
+  const int half = C0 / 2;
+  for (int k = threadIdx.x; k < half; k += blockDim.x) {
+    const float f = expf(-logf(10000.0f) * (float)k / (float)half);
+    const float arg = t * f;
+    out[(int64_t)r * C0 + k] = (_Float16)cosf(arg);
+    out[(int64_t)r * C0 + half + k] = (_Float16)sinf(arg);
+  }
+}
+
+// conv_in in float32 from the float32 latent x [samples][Cin][H][W]; output
+// [rows][H*W][C0] float16, rows 2b and 2b+1 read sample b.
+__global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
+                                                 const float* __restrict__ w,
+                                                 const float* __restrict__ bias, int Cin, int H,
+                                                 int W, int C0, int rows,
+                                                 _Float16* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)rows * H * W * C0;
+  if (i >= total) return;
+  const int co = (int)(i % C0);
+  const int64_t pix = i / C0;
+  const int r = (int)(pix / (H * W));
+  const int p = (int)(pix % (H * W));
+  const int y = p / W, xx = p % W;
+  const float* xs = x + (int64_t)(r >> 1) * Cin * H * W;
+  float acc = bias[co];
+  for (int ci = 0; ci < Cin; ++ci)
+    for (int ky = 0; ky < 3; ++ky) {
+      const int iy = y + ky - 1;
+      if (iy < 0 || iy >= H) continue;
+      for (int kx = 0; kx < 3; ++kx) {
+        const int ix = xx + kx - 1;
+        if (ix < 0 || ix >= W) continue;
+        acc = fmaf(w[((co * Cin + ci) * 3 + ky) * 3 + kx], xs[((int64_t)ci * H + iy) * W + ix], acc);
+      }
+    }
+  out[i] = (_Float16)acc;
+}
+
+// eps = eps_u + s (eps_c - eps_u); x <- sqrt(a_p) (x - sqrt(1-a_t) eps)/sqrt(a_t) + sqrt(1-a_p) eps
+__global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __restrict__ eps,
+                                                  float* __restrict__ x, int C, int HW,
+                                                  int samples, float guidance,
+                                                  const float* __restrict__ a_t,
+                                                  const float* __restrict__ a_prev) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)samples * C * HW;
+  if (i >= total) return;
+  const int b = (int)(i / ((int64_t)C * HW));
+  const int rem = (int)(i % ((int64_t)C * HW));
+  const int c = rem / HW, p = rem % HW;
+  const int step = st.kstep[b] + st.j;
+  const float at = a_t[step], ap = a_prev[step];
+  const float eu = eps[((int64_t)(2 * b) * HW + p) * C + c];
+  const float ec = eps[((int64_t)(2 * b + 1) * HW + p) * C + c];
+  const float e = eu + guidance * (ec - eu);
+  const float xv = x[i];
+  const float x0 = (xv - sqrtf(1.0f - at) * e) / sqrtf(at);
+  x[i] = sqrtf(ap) * x0 + sqrtf(1.0f - ap) * e;
+}
+
+// eps rows [rows][HW][C] float32 -> eps_u / eps_c [samples][C][HW].
+__global__ void eps_split_k(const float* __restrict__ eps, int C, int HW, int samples,
+                            float* __restrict__ eu, float* __restrict__ ec) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)samples * C * HW;
+  if (i >= total) return;
+  const int b = (int)(i / ((int64_t)C * HW));
+  const int rem = (int)(i % ((int64_t)C * HW));
+  const int c = rem / HW, p = rem % HW;
+  eu[i] = eps[((int64_t)(2 * b) * HW + p) * C + c];
+  ec[i] = eps[((int64_t)(2 * b + 1) * HW + p) * C + c];
+}
+
+// Context rows: row 2b = uncond[perm[b]], row 2b+1 = cond[perm[b]] as float16.
+__global__ void ctx_rows_k(StepArgs st, const float* __restrict__ cond,
+                           const float* __restrict__ uncond, int64_t per_sample, int rows,
+                           _Float16* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * per_sample) return;
+  const int r = (int)(i / per_sample);
+  const int64_t e = i % per_sample;
+  const int src = st.perm[r >> 1];
+  const float v = (r & 1) ? cond[(int64_t)src * per_sample + e] : uncond[(int64_t)src * per_sample + e];
+  out[i] = (_Float16)v;
+}
+
+// dst[b] = src[perm[b]] (to_sorted) or dst[perm[b]] = src[b] (from sorted), float32.
+__global__ void permute_k(StepArgs st, const float* __restrict__ src, float* __restrict__ dst,
+                          int64_t per_sample, int samples, int to_sorted) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= samples * per_sample) return;
+  const int b = (int)(i / per_sample);
+  const int64_t e = i % per_sample;
+  if (to_sorted)
+    dst[i] = src[(int64_t)st.perm[b] * per_sample + e];
+  else
+    dst[(int64_t)st.perm[b] * per_sample + e] = src[i];
+}
+
+inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
+
+}  // namespace
+
+hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
+  hipLaunchKernelGGL(gn_stats_k, dim3(rows * a.G), dim3(256), 0, s, a);
+  const int64_t total8 = (int64_t)rows * a.HW * (a.C1 + a.C2) / 8;
+  hipLaunchKernelGGL(gn_apply_k, dim3(blocks_for(total8)), dim3(256), 0, s, a, total8);
+  return hipGetLastError();
+}
+
+hipError_t layernorm_launch(const _Float16* x, const float* g, const float* b, _Float16* out,
+                            int64_t tokens, int C, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(layernorm_k, dim3((unsigned)ceil_div(tokens, 4)), dim3(256), 0, s, x, g, b,
+                     out, tokens, C, eps);
+  return hipGetLastError();
+}
+
+hipError_t schedule_launch(int T, int N, double b0, double b1, int32_t* ts, float* a_t,
+                           float* a_prev, hipStream_t s) {
+  hipLaunchKernelGGL(schedule_k, dim3(1), dim3(64), 0, s, T, N, b0, b1, ts, a_t, a_prev);
+  return hipGetLastError();
+}
+
+hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int rows, _Float16* out,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(temb_sin_k, dim3(rows), dim3(128), 0, s, st, ts, C0, rows, out);
+  return hipGetLastError();
+}
+
+hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Cin, int H, int W,
+                          int C0, int rows, _Float16* out, hipStream_t s) {
+  const int64_t total = (int64_t)rows * H * W * C0;
+  hipLaunchKernelGGL(conv_in_k, dim3(blocks_for(total)), dim3(256), 0, s, x, w, b, Cin, H, W, C0,
+                     rows, out);
+  return hipGetLastError();
+}
+
+hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C, int HW,
+                           int samples, float guidance, const float* a_t, const float* a_prev,
+                           hipStream_t s) {
+  const int64_t total = (int64_t)samples * C * HW;
+  hipLaunchKernelGGL(cfg_ddim_k, dim3(blocks_for(total)), dim3(256), 0, s, st, eps, x, C, HW,
+                     samples, guidance, a_t, a_prev);
+  return hipGetLastError();
+}
+
+hipError_t eps_split_launch(const float* eps, int C, int HW, int samples, float* eu, float* ec,
+                            hipStream_t s) {
+  const int64_t total = (int64_t)samples * C * HW;
+  hipLaunchKernelGGL(eps_split_k, dim3(blocks_for(total)), dim3(256), 0, s, eps, C, HW, samples,
+                     eu, ec);
+  return hipGetLastError();
+}
+
+hipError_t ctx_rows_launch(const StepArgs& st, const float* cond, const float* uncond,
+                           int64_t per_sample, int rows, _Float16* out, hipStream_t s) {
+  hipLaunchKernelGGL(ctx_rows_k, dim3(blocks_for(rows * per_sample)), dim3(256), 0, s, st, cond,
+                     uncond, per_sample, rows, out);
+  return hipGetLastError();
+}
+
+hipError_t permute_launch(const StepArgs& st, const float* src, float* dst, int64_t per_sample,
+                          int samples, int to_sorted, hipStream_t s) {
+  hipLaunchKernelGGL(permute_k, dim3(blocks_for(samples * per_sample)), dim3(256), 0, s, st, src,
+                     dst, per_sample, samples, to_sorted);
+  return hipGetLastError();
+}
+
+}  // namespace nv

@@ -1,0 +1,1173 @@
+// UNet handle, execution plan and the K-skipped DDIM loop (host side).
+//
+// nv_unet_create packs the canonical float32 weight blob into device layouts
+// (3x3 conv weights [Cout][ky][kx][Cin] float16, linear [out][in] float16,
+// self-attention q|k|v and cross-attention k|v concatenated, GEGLU rows
+// interleaved in groups of 16, every ResBlock's time projection stacked into
+// one matrix; norms and biases float32).
+//
+// A plan is the ordered list of kernel launches of one UNet evaluation for up
+// to R rows (2 per sample: unconditional, conditional), with every
+// activation placed in the caller's workspace by a first-fit arena over
+// buffer lifetimes.  The same plan runs with fewer active rows: all
+// activations are row-major with rows outermost.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <functional>
+#include <map>
+#include <memory>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "attention.h"
+#include "common.h"
+#include "gemm.h"
+#include "ops.h"
+
+namespace nv {
+
+static thread_local std::string g_err;
+void set_error(const std::string& m) { g_err = m; }
+void clear_error() { g_err.clear(); }
+
+namespace {
+
+struct ParamInfo {
+  std::string name;
+  std::vector<int64_t> shape;
+  int64_t offset = 0;
+  int64_t numel() const {
+    int64_t n = 1;
+    for (auto s : shape) n *= s;
+    return n;
+  }
+};
+
+int heads_for(const nv_unet_config& c, int ch) {
+  return c.n_heads > 0 ? c.n_heads : ch / c.head_dim;
+}
+
+// Canonical parameter order (documented in nv.h).
+void enumerate_params(const nv_unet_config& c, std::vector<ParamInfo>& out) {
+  out.clear();
+  const int c0 = c.ch[0], td = 4 * c0, L = c.n_levels;
+  auto add = [&](const std::string& n, std::vector<int64_t> s) { out.push_back({n, s, 0}); };
+  auto lin = [&](const std::string& n, int o, int i, bool bias = true) {
+    add(n + ".w", {o, i});
+    if (bias) add(n + ".b", {o});
+  };
+  auto conv = [&](const std::string& n, int o, int i) {
+    add(n + ".w", {o, i, 3, 3});
+    add(n + ".b", {o});
+  };
+  auto norm = [&](const std::string& n, int ch) {
+    add(n + ".g", {ch});
+    add(n + ".b", {ch});
+  };
+  auto res = [&](const std::string& n, int cin, int cout) {
+    norm(n + ".gn1", cin);
+    conv(n + ".conv1", cout, cin);
+    lin(n + ".temb", cout, td);
+    norm(n + ".gn2", cout);
+    conv(n + ".conv2", cout, cout);
+    if (cin != cout) lin(n + ".skip", cout, cin);
+  };
+  auto tr = [&](const std::string& n, int ch, int depth) {
+    norm(n + ".gn", ch);
+    lin(n + ".proj_in", ch, ch);
+    for (int j = 0; j < depth; ++j) {
+      const std::string b = n + ".blk" + std::to_string(j);
+      norm(b + ".ln1", ch);
+      lin(b + ".attn1.q", ch, ch, false);
+      lin(b + ".attn1.k", ch, ch, false);
+      lin(b + ".attn1.v", ch, ch, false);
+      lin(b + ".attn1.o", ch, ch);
+      norm(b + ".ln2", ch);
+      lin(b + ".attn2.q", ch, ch, false);
+      lin(b + ".attn2.k", ch, c.ctx_dim, false);
+      lin(b + ".attn2.v", ch, c.ctx_dim, false);
+      lin(b + ".attn2.o", ch, ch);
+      norm(b + ".ln3", ch);
+      lin(b + ".ff1", 8 * ch, ch);
+      lin(b + ".ff2", ch, 4 * ch);
+    }
+    lin(n + ".proj_out", ch, ch);
+  };
+  lin("time.l1", td, c0);
+  lin("time.l2", td, td);
+  conv("conv_in", c0, c.in_ch);
+  std::vector<int> skips{c0};
+  int cur = c0;
+  for (int lv = 0; lv < L; ++lv) {
+    const int co = c.ch[lv];
+    for (int r = 0; r < c.n_res; ++r) {
+      res("down" + std::to_string(lv) + ".res" + std::to_string(r), cur, co);
+      cur = co;
+      if (c.depth[lv] > 0)
+        tr("down" + std::to_string(lv) + ".attn" + std::to_string(r), cur, c.depth[lv]);
+      skips.push_back(cur);
+    }
+    if (lv < L - 1) {
+      conv("down" + std::to_string(lv) + ".ds", cur, cur);
+      skips.push_back(cur);
+    }
+  }
+  res("mid.res0", cur, cur);
+  if (c.mid_depth > 0) tr("mid.attn", cur, c.mid_depth);
+  res("mid.res1", cur, cur);
+  for (int lv = L - 1; lv >= 0; --lv) {
+    const int co = c.ch[lv];
+    for (int r = 0; r < c.n_res + 1; ++r) {
+      const int sk = skips.back();
+      skips.pop_back();
+      res("up" + std::to_string(lv) + ".res" + std::to_string(r), cur + sk, co);
+      cur = co;
+      if (c.depth[lv] > 0)
+        tr("up" + std::to_string(lv) + ".attn" + std::to_string(r), cur, c.depth[lv]);
+    }
+    if (lv > 0) conv("up" + std::to_string(lv) + ".us", cur, cur);
+  }
+  norm("out.gn", cur);
+  conv("conv_out", c.out_ch, cur);
+  int64_t off = 0;
+  for (auto& p : out) {
+    p.offset = off;
+    off += p.numel();
+  }
+}
+
+bool validate_cfg(const nv_unet_config* c, std::string* why) {
+  auto fail = [&](const std::string& m) {
+    *why = m;
+    return false;
+  };
+  if (!c) return fail("null config");
+  if (c->in_ch < 1 || c->in_ch > 16 || c->out_ch < 1 || c->out_ch > 16)
+    return fail("in_ch/out_ch must be in [1, 16]");
+  if (c->n_levels < 1 || c->n_levels > 4) return fail("n_levels must be in [1, 4]");
+  if (c->n_res < 1 || c->n_res > 8) return fail("n_res must be in [1, 8]");
+  if (c->gn_groups < 1) return fail("gn_groups must be >= 1");
+  const int f = 1 << (c->n_levels - 1);
+  if (c->H < f || c->W < f || c->H % f || c->W % f)
+    return fail("H and W must be divisible by 2^(n_levels-1)");
+  if (c->ctx_len < 1 || c->ctx_dim < 8 || c->ctx_dim % 8) return fail("bad context shape");
+  if (!(c->gn_eps > 0) || !(c->ln_eps > 0)) return fail("eps must be > 0");
+  if (c->pooled_dim != 0 && c->pooled_dim != 4 * c->ch[0])
+    return fail("pooled_dim must be 0 or 4*ch[0]");
+  for (int l = 0; l < c->n_levels; ++l) {
+    const int ch = c->ch[l];
+    if (ch < 32 || ch % 32 || ch % c->gn_groups || ch > 2048)
+      return fail("channels must be multiples of 32 and of gn_groups, at most 2048");
+    if (c->depth[l] < 0) return fail("depth must be >= 0");
+  }
+  if (c->mid_depth < 0) return fail("mid_depth must be >= 0");
+  // attention head dims and concatenated channel counts
+  std::vector<int> skips{c->ch[0]};
+  int cur = c->ch[0];
+  auto check_tr = [&](int ch) -> bool {
+    if (c->n_heads <= 0 && c->head_dim <= 0) return false;
+    const int h = heads_for(*c, ch);
+    if (h < 1 || ch % h) return false;
+    return attn_supported(ch / h);
+  };
+  for (int l = 0; l < c->n_levels; ++l) {
+    for (int r = 0; r < c->n_res; ++r) {
+      cur = c->ch[l];
+      skips.push_back(cur);
+    }
+    if (c->depth[l] > 0 && !check_tr(c->ch[l])) return fail("unsupported head dim");
+    if (l < c->n_levels - 1) skips.push_back(cur);
+  }
+  if (c->mid_depth > 0 && !check_tr(cur)) return fail("unsupported head dim (mid)");
+  for (int l = c->n_levels - 1; l >= 0; --l)
+    for (int r = 0; r < c->n_res + 1; ++r) {
+      const int sk = skips.back();
+      skips.pop_back();
+      const int cin = cur + sk;
+      if (cin % c->gn_groups) return fail("concatenated channels must be divisible by gn_groups");
+      if (cin == c->ch[l]) return fail("concatenated input equal to output width is unsupported");
+      cur = c->ch[l];
+    }
+  return true;
+}
+
+// ---------------------------------------------------------------- weights
+struct Lin {
+  const _Float16* w = nullptr;
+  const float* b = nullptr;
+  int out = 0, in = 0;
+};
+struct Norm {
+  const float* g = nullptr;
+  const float* b = nullptr;
+};
+
+// Execution-time context of one UNet evaluation.
+struct RunCtx {
+  char* ws;
+  int R;             // active rows
+  hipStream_t s;
+  const float* x;    // float32 latent [samples][Cin][H][W]
+  StepArgs st;
+};
+using Op = std::function<hipError_t(const RunCtx&)>;
+
+struct Arena {
+  std::vector<std::pair<size_t, size_t>> free_;  // (off, size)
+  size_t top = 0;
+  size_t alloc(size_t bytes) {
+    bytes = align_up(std::max<size_t>(bytes, 1), 256);
+    for (size_t i = 0; i < free_.size(); ++i) {
+      if (free_[i].second >= bytes) {
+        const size_t off = free_[i].first;
+        free_[i].first += bytes;
+        free_[i].second -= bytes;
+        if (free_[i].second == 0) free_.erase(free_.begin() + i);
+        return off;
+      }
+    }
+    const size_t off = top;
+    top += bytes;
+    return off;
+  }
+  void release(size_t off, size_t bytes) {
+    bytes = align_up(std::max<size_t>(bytes, 1), 256);
+    free_.push_back({off, bytes});
+    std::sort(free_.begin(), free_.end());
+    std::vector<std::pair<size_t, size_t>> m;
+    for (auto& f : free_) {
+      if (!m.empty() && m.back().first + m.back().second == f.first)
+        m.back().second += f.second;
+      else
+        m.push_back(f);
+    }
+    if (!m.empty() && m.back().first + m.back().second == top) {
+      top = m.back().first;
+      m.pop_back();
+    }
+    free_ = m;
+  }
+};
+
+struct Ten {
+  int id = -1;
+  size_t off = 0;
+  int HW = 0, C = 0;
+};
+
+struct Plan {
+  int Rmax = 0;
+  std::vector<Op> pre;   // once per call (context projections)
+  std::vector<Op> step;  // one UNet evaluation
+  size_t bytes = 0;
+  // fixed regions
+  size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0, stats = 0;
+};
+
+}  // namespace
+}  // namespace nv
+
+struct nv_unet {
+  nv_unet_config cfg;
+  std::vector<nv::ParamInfo> params;
+  std::map<std::string, const _Float16*> w16;
+  std::map<std::string, const float*> w32;
+  _Float16* d16 = nullptr;
+  float* d32 = nullptr;
+  int temb_total = 0;                       // sum of ResBlock widths
+  std::map<std::string, int> temb_off;      // ResBlock name -> column offset
+  std::map<int, std::unique_ptr<nv::Plan>> plans;
+};
+
+namespace nv {
+namespace {
+
+class Builder {
+ public:
+  Builder(nv_unet* net, Plan* p, int Rmax) : net_(net), P(p), Rmax_(Rmax) {}
+
+  Ten alloc(int HW, int C, int esize = 2) {
+    Ten t;
+    t.id = (int)sizes_.size();
+    t.HW = HW;
+    t.C = C;
+    const size_t bytes = (size_t)Rmax_ * HW * C * esize;
+    t.off = arena_.alloc(bytes);
+    sizes_.push_back(bytes);
+    refs_.push_back(1);
+    offs_.push_back(t.off);
+    return t;
+  }
+  size_t fixed(size_t bytes) { return arena_.alloc(bytes); }
+  void hold(const Ten& t) { refs_[t.id]++; }
+  void drop(const Ten& t) {
+    if (--refs_[t.id] == 0) arena_.release(offs_[t.id], sizes_[t.id]);
+  }
+  size_t peak() const { return arena_.top_peak; }
+
+  const _Float16* W16(const std::string& n) {
+    auto it = net_->w16.find(n);
+    if (it == net_->w16.end()) throw std::runtime_error("missing weight " + n);
+    return it->second;
+  }
+  const float* W32(const std::string& n) {
+    auto it = net_->w32.find(n);
+    if (it == net_->w32.end()) throw std::runtime_error("missing weight " + n);
+    return it->second;
+  }
+
+  nv_unet* net_;
+  Plan* P;
+  int Rmax_;
+  struct TrackedArena : Arena {
+    size_t top_peak = 0;
+    size_t alloc(size_t b) {
+      const size_t o = Arena::alloc(b);
+      top_peak = std::max(top_peak, top);
+      return o;
+    }
+  } arena_;
+  std::vector<size_t> sizes_, offs_;
+  std::vector<int> refs_;
+};
+
+inline _Float16* H16(const RunCtx& c, size_t off) { return (_Float16*)(c.ws + off); }
+inline float* F32(const RunCtx& c, size_t off) { return (float*)(c.ws + off); }
+
+// GEMM op helpers --------------------------------------------------------
+GemmArgs dense_args(int N, int K, const _Float16* w, const float* bias) {
+  GemmArgs g{};
+  g.N = N;
+  g.K = K;
+  g.w = w;
+  g.ldw = K;
+  g.bias = bias;
+  g.C1 = K;
+  g.lda1 = K;
+  g.rows_div = 1;
+  return g;
+}
+
+void emit_gn(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2, const std::string& n,
+             bool silu, const Ten& out) {
+  const auto& cfg = B.net_->cfg;
+  const float* g = B.W32(n + ".g");
+  const float* b = B.W32(n + ".b");
+  const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off, st = B.P->stats;
+  const int C1 = x1.C, C2 = x2 ? x2->C : 0, HW = x1.HW, G = cfg.gn_groups;
+  const float eps = cfg.gn_eps;
+  const bool has2 = x2 != nullptr;
+  ops.push_back([=](const RunCtx& c) {
+    GnArgs a{};
+    a.src1 = H16(c, o1);
+    a.src2 = has2 ? H16(c, o2) : nullptr;
+    a.C1 = C1;
+    a.C2 = C2;
+    a.HW = HW;
+    a.G = G;
+    a.eps = eps;
+    a.gamma = g;
+    a.beta = b;
+    a.silu = silu;
+    a.stats = F32(c, st);
+    a.out = H16(c, oo);
+    return gn_launch(a, c.R, c.s);
+  });
+}
+
+struct ConvSpec {
+  int Hin, Win, Ho, Wo, stride, upsample;
+};
+
+void emit_conv(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
+               const std::string& n, int cout, ConvSpec cs, const Ten& out, const Ten* residual,
+               int temb_off, bool out_f32 = false, size_t out_off_override = 0) {
+  const _Float16* w = B.W16(n + ".w");
+  const float* bias = B.W32(n + ".b");
+  const size_t o1 = x1.off, o2 = x2 ? x2->off : 0;
+  const size_t oo = out_f32 ? out_off_override : out.off;
+  const size_t ores = residual ? residual->off : 0;
+  const bool has2 = x2 != nullptr, hasr = residual != nullptr;
+  const int C1 = x1.C, C2 = x2 ? x2->C : 0;
+  const size_t tproj = B.P->tproj;
+  const int ttot = B.net_->temb_total;
+  ops.push_back([=](const RunCtx& c) {
+    GemmArgs g{};
+    g.M = (int64_t)c.R * cs.Ho * cs.Wo;
+    g.N = cout;
+    g.K = 9 * (C1 + C2);
+    g.src1 = H16(c, o1);
+    g.src2 = has2 ? H16(c, o2) : nullptr;
+    g.C1 = C1;
+    g.C2 = C2;
+    g.conv = 1;
+    g.Hin = cs.Hin;
+    g.Win = cs.Win;
+    g.Ho = cs.Ho;
+    g.Wo = cs.Wo;
+    g.stride = cs.stride;
+    g.upsample = cs.upsample;
+    g.w = w;
+    g.ldw = g.K;
+    g.bias = bias;
+    g.rows_div = (int64_t)cs.Ho * cs.Wo;
+    if (temb_off >= 0) {
+      g.rowvec = F32(c, tproj) + temb_off;
+      g.ld_rowvec = ttot;
+    }
+    if (hasr) {
+      g.residual = H16(c, ores);
+      g.ld_res = cout;
+    }
+    g.out = c.ws + oo;
+    g.ldo = cout;
+    g.out_f32 = out_f32;
+    return gemm_launch(g, c.s);
+  });
+}
+
+// y[M][N] = x[M][K] W^T (+bias) (+residual) ; x may be a 2-source concat
+void emit_linear(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
+                 const _Float16* w, const float* bias, int N, const Ten& out, const Ten* residual,
+                 bool geglu = false) {
+  const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off;
+  const size_t ores = residual ? residual->off : 0;
+  const bool has2 = x2 != nullptr, hasr = residual != nullptr;
+  const int C1 = x1.C, C2 = x2 ? x2->C : 0, HW = x1.HW, ldo = out.C;
+  ops.push_back([=](const RunCtx& c) {
+    GemmArgs g = dense_args(N, C1 + C2, w, bias);
+    g.M = (int64_t)c.R * HW;
+    g.src1 = H16(c, o1);
+    g.C1 = C1;
+    g.lda1 = C1;
+    if (has2) {
+      g.src2 = H16(c, o2);
+      g.C2 = C2;
+      g.lda2 = C2;
+    }
+    if (hasr) {
+      g.residual = H16(c, ores);
+      g.ld_res = ldo;
+    }
+    g.geglu = geglu;
+    g.out = c.ws + oo;
+    g.ldo = ldo;
+    return gemm_launch(g, c.s);
+  });
+}
+
+Ten build_res(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
+              const std::string& n, int cout, int H, int W) {
+  const int cin = x1.C + (x2 ? x2->C : 0);
+  const int HW = H * W;
+  Ten a1 = B.alloc(HW, cin);
+  emit_gn(B, ops, x1, x2, n + ".gn1", true, a1);
+  Ten h = B.alloc(HW, cout);
+  const int toff = B.net_->temb_off.at(n);
+  emit_conv(B, ops, a1, nullptr, n + ".conv1", cout, {H, W, H, W, 1, 0}, h, nullptr, toff);
+  B.drop(a1);
+  Ten a2 = B.alloc(HW, cout);
+  emit_gn(B, ops, h, nullptr, n + ".gn2", true, a2);
+  B.drop(h);
+  Ten sk;
+  bool own_sk = false;
+  if (cin != cout) {
+    sk = B.alloc(HW, cout);
+    own_sk = true;
+    emit_linear(B, ops, x1, x2, B.W16(n + ".skip.w"), B.W32(n + ".skip.b"), cout, sk, nullptr);
+  } else {
+    sk = x1;
+  }
+  Ten out = B.alloc(HW, cout);
+  emit_conv(B, ops, a2, nullptr, n + ".conv2", cout, {H, W, H, W, 1, 0}, out, &sk, -1);
+  B.drop(a2);
+  if (own_sk) B.drop(sk);
+  return out;
+}
+
+struct KvRef {
+  size_t off;
+};
+
+Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& n, int depth,
+             int H, int W, const std::map<std::string, size_t>& kv_regions) {
+  const auto& cfg = B.net_->cfg;
+  const int C = x.C, HW = H * W;
+  const int heads = heads_for(cfg, C), dh = C / heads;
+  const int Lc = cfg.ctx_len;
+  const float scale = 1.0f / std::sqrt((float)dh);
+  Ten g = B.alloc(HW, C);
+  emit_gn(B, ops, x, nullptr, n + ".gn", false, g);
+  Ten h = B.alloc(HW, C);
+  emit_linear(B, ops, g, nullptr, B.W16(n + ".proj_in.w"), B.W32(n + ".proj_in.b"), C, h, nullptr);
+  B.drop(g);
+  for (int j = 0; j < depth; ++j) {
+    const std::string b = n + ".blk" + std::to_string(j);
+    // self-attention
+    Ten t = B.alloc(HW, C);
+    {
+      const size_t xi = h.off, to = t.off;
+      const float* lg = B.W32(b + ".ln1.g");
+      const float* lb = B.W32(b + ".ln1.b");
+      const float eps = cfg.ln_eps;
+      ops.push_back([=](const RunCtx& c) {
+        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
+      });
+    }
+    Ten qkv = B.alloc(HW, 3 * C);
+    emit_linear(B, ops, t, nullptr, B.W16(b + ".attn1.qkv.w"), nullptr, 3 * C, qkv, nullptr);
+    B.drop(t);
+    Ten a = B.alloc(HW, C);
+    {
+      const size_t qo = qkv.off, ao = a.off;
+      ops.push_back([=](const RunCtx& c) {
+        AttnArgs at{};
+        at.q = H16(c, qo);
+        at.k = H16(c, qo) + C;
+        at.v = H16(c, qo) + 2 * C;
+        at.o = H16(c, ao);
+        at.ldq = at.ldk = at.ldv = 3 * C;
+        at.ldo = C;
+        at.rows = c.R;
+        at.S = HW;
+        at.L = HW;
+        at.heads = heads;
+        at.dh = dh;
+        at.scale = scale;
+        return attn_launch(at, c.s);
+      });
+    }
+    B.drop(qkv);
+    emit_linear(B, ops, a, nullptr, B.W16(b + ".attn1.o.w"), B.W32(b + ".attn1.o.b"), C, h, &h);
+    B.drop(a);
+    // cross-attention
+    t = B.alloc(HW, C);
+    {
+      const size_t xi = h.off, to = t.off;
+      const float* lg = B.W32(b + ".ln2.g");
+      const float* lb = B.W32(b + ".ln2.b");
+      const float eps = cfg.ln_eps;
+      ops.push_back([=](const RunCtx& c) {
+        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
+      });
+    }
+    Ten qc = B.alloc(HW, C);
+    emit_linear(B, ops, t, nullptr, B.W16(b + ".attn2.q.w"), nullptr, C, qc, nullptr);
+    B.drop(t);
+    // context K|V of this block: computed once per call into a region reserved
+    // before any per-step buffer, so no step op can overwrite it
+    const size_t kvoff = kv_regions.at(b);
+    a = B.alloc(HW, C);
+    {
+      const size_t qo = qc.off, ao = a.off;
+      ops.push_back([=](const RunCtx& c) {
+        AttnArgs at{};
+        at.q = H16(c, qo);
+        at.k = H16(c, kvoff);
+        at.v = H16(c, kvoff) + C;
+        at.o = H16(c, ao);
+        at.ldq = C;
+        at.ldk = at.ldv = 2 * C;
+        at.ldo = C;
+        at.rows = c.R;
+        at.S = HW;
+        at.L = Lc;
+        at.heads = heads;
+        at.dh = dh;
+        at.scale = scale;
+        return attn_launch(at, c.s);
+      });
+    }
+    B.drop(qc);
+    emit_linear(B, ops, a, nullptr, B.W16(b + ".attn2.o.w"), B.W32(b + ".attn2.o.b"), C, h, &h);
+    B.drop(a);
+    // GEGLU feed-forward
+    t = B.alloc(HW, C);
+    {
+      const size_t xi = h.off, to = t.off;
+      const float* lg = B.W32(b + ".ln3.g");
+      const float* lb = B.W32(b + ".ln3.b");
+      const float eps = cfg.ln_eps;
+      ops.push_back([=](const RunCtx& c) {
+        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
+      });
+    }
+    Ten f = B.alloc(HW, 4 * C);
+    emit_linear(B, ops, t, nullptr, B.W16(b + ".ff1.w"), B.W32(b + ".ff1.b"), 8 * C, f, nullptr,
+                true);
+    B.drop(t);
+    emit_linear(B, ops, f, nullptr, B.W16(b + ".ff2.w"), B.W32(b + ".ff2.b"), C, h, &h);
+    B.drop(f);
+  }
+  Ten out = B.alloc(HW, C);
+  emit_linear(B, ops, h, nullptr, B.W16(n + ".proj_out.w"), B.W32(n + ".proj_out.b"), C, out, &x);
+  B.drop(h);
+  return out;
+}
+
+std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
+  auto P = std::make_unique<Plan>();
+  P->Rmax = Rmax;
+  const auto& c = net->cfg;
+  Builder B(net, P.get(), Rmax);
+  const int Bs = (Rmax + 1) / 2;
+  const int HW0 = c.H * c.W, C0 = c.ch[0], td = 4 * C0, L = c.n_levels;
+  // fixed regions
+  P->x_work = B.fixed((size_t)Bs * c.in_ch * HW0 * 4);
+  P->eps = B.fixed((size_t)Rmax * HW0 * c.out_ch * 4);
+  P->ts = B.fixed(1024 * 4);
+  P->at = B.fixed(1024 * 4);
+  P->ap = B.fixed(1024 * 4);
+  P->ctx = B.fixed((size_t)Rmax * c.ctx_len * c.ctx_dim * 2);
+  P->pooled = B.fixed((size_t)Bs * std::max(c.pooled_dim, 1) * 4);
+  P->tproj = B.fixed((size_t)Rmax * net->temb_total * 4);
+  int maxG = c.gn_groups;
+  P->stats = B.fixed((size_t)Rmax * maxG * 2 * 4);
+  // per-call context K|V regions, one per transformer block
+  std::map<std::string, size_t> kv_regions;
+  std::map<std::string, int> kv_width;
+  for (auto& p : net->params) {
+    const std::string& n = p.name;
+    const std::string suf = ".attn2.k.w";
+    if (n.size() > suf.size() && n.compare(n.size() - suf.size(), suf.size(), suf) == 0) {
+      const std::string b = n.substr(0, n.size() - suf.size());
+      kv_width[b] = (int)p.shape[0];
+      kv_regions[b] = B.fixed((size_t)Rmax * c.ctx_len * 2 * p.shape[0] * 2);
+    }
+  }
+  auto& ops = P->step;
+
+  // time embedding -> SiLU(temb) -> every ResBlock's projection
+  {
+    Ten s0 = B.alloc(1, C0);
+    const size_t so = s0.off, tso = P->ts;
+    ops.push_back([=](const RunCtx& x) {
+      return temb_sin_launch(x.st, (const int32_t*)(x.ws + tso), C0, x.R, H16(x, so), x.s);
+    });
+    Ten t1 = B.alloc(1, td);
+    {
+      const _Float16* w = B.W16("time.l1.w");
+      const float* b = B.W32("time.l1.b");
+      const size_t o = t1.off;
+      ops.push_back([=](const RunCtx& x) {
+        GemmArgs g = dense_args(td, C0, w, b);
+        g.M = x.R;
+        g.src1 = H16(x, so);
+        g.silu = 1;
+        g.out = x.ws + o;
+        g.ldo = td;
+        return gemm_launch(g, x.s);
+      });
+    }
+    B.drop(s0);
+    Ten t2 = B.alloc(1, td);
+    {
+      const _Float16* w = B.W16("time.l2.w");
+      const float* b = B.W32("time.l2.b");
+      const size_t i1 = t1.off, o = t2.off, po = P->pooled;
+      const bool pooled = c.pooled_dim > 0;
+      ops.push_back([=](const RunCtx& x) {
+        GemmArgs g = dense_args(td, td, w, b);
+        g.M = x.R;
+        g.src1 = H16(x, i1);
+        if (pooled) {
+          g.rowvec = F32(x, po);
+          g.rows_div = 2;
+          g.ld_rowvec = td;
+        }
+        g.silu = 1;
+        g.out = x.ws + o;
+        g.ldo = td;
+        return gemm_launch(g, x.s);
+      });
+    }
+    B.drop(t1);
+    {
+      const _Float16* w = B.W16("temb_all.w");
+      const float* b = B.W32("temb_all.b");
+      const size_t i2 = t2.off, o = P->tproj;
+      const int N = net->temb_total;
+      ops.push_back([=](const RunCtx& x) {
+        GemmArgs g = dense_args(N, td, w, b);
+        g.M = x.R;
+        g.src1 = H16(x, i2);
+        g.out = x.ws + o;
+        g.ldo = N;
+        g.out_f32 = 1;
+        return gemm_launch(g, x.s);
+      });
+    }
+    B.drop(t2);
+  }
+  // conv_in on the float32 latent
+  Ten h = B.alloc(HW0, C0);
+  {
+    const float* w = B.W32("conv_in.w");
+    const float* b = B.W32("conv_in.b");
+    const size_t o = h.off;
+    const int cin = c.in_ch, H = c.H, W = c.W;
+    ops.push_back([=](const RunCtx& x) {
+      return conv_in_launch(x.x, w, b, cin, H, W, C0, x.R, H16(x, o), x.s);
+    });
+  }
+  std::vector<Ten> skips;
+  skips.push_back(h);
+  B.hold(h);
+  int H = c.H, W = c.W;
+  for (int lv = 0; lv < L; ++lv) {
+    const int co = c.ch[lv];
+    for (int r = 0; r < c.n_res; ++r) {
+      const std::string base = "down" + std::to_string(lv);
+      Ten nh = build_res(B, ops, h, nullptr, base + ".res" + std::to_string(r), co, H, W);
+      B.drop(h);
+      h = nh;
+      if (c.depth[lv] > 0) {
+        nh = build_tr(B, ops, h, base + ".attn" + std::to_string(r), c.depth[lv], H, W,
+                      kv_regions);
+        B.drop(h);
+        h = nh;
+      }
+      skips.push_back(h);
+      B.hold(h);
+    }
+    if (lv < L - 1) {
+      Ten nh = B.alloc((H / 2) * (W / 2), h.C);
+      emit_conv(B, ops, h, nullptr, "down" + std::to_string(lv) + ".ds", h.C,
+                {H, W, H / 2, W / 2, 2, 0}, nh, nullptr, -1);
+      B.drop(h);
+      h = nh;
+      H /= 2;
+      W /= 2;
+      skips.push_back(h);
+      B.hold(h);
+    }
+  }
+  {
+    Ten nh = build_res(B, ops, h, nullptr, "mid.res0", h.C, H, W);
+    B.drop(h);
+    h = nh;
+    if (c.mid_depth > 0) {
+      nh = build_tr(B, ops, h, "mid.attn", c.mid_depth, H, W, kv_regions);
+      B.drop(h);
+      h = nh;
+    }
+    nh = build_res(B, ops, h, nullptr, "mid.res1", h.C, H, W);
+    B.drop(h);
+    h = nh;
+  }
+  for (int lv = L - 1; lv >= 0; --lv) {
+    const int co = c.ch[lv];
+    const std::string base = "up" + std::to_string(lv);
+    for (int r = 0; r < c.n_res + 1; ++r) {
+      Ten sk = skips.back();
+      skips.pop_back();
+      Ten nh = build_res(B, ops, h, &sk, base + ".res" + std::to_string(r), co, H, W);
+      B.drop(h);
+      B.drop(sk);
+      h = nh;
+      if (c.depth[lv] > 0) {
+        nh = build_tr(B, ops, h, base + ".attn" + std::to_string(r), c.depth[lv], H, W,
+                      kv_regions);
+        B.drop(h);
+        h = nh;
+      }
+    }
+    if (lv > 0) {
+      Ten nh = B.alloc(4 * H * W, h.C);
+      emit_conv(B, ops, h, nullptr, base + ".us", h.C, {H, W, 2 * H, 2 * W, 1, 1}, nh, nullptr,
+                -1);
+      B.drop(h);
+      h = nh;
+      H *= 2;
+      W *= 2;
+    }
+  }
+  {
+    Ten a = B.alloc(HW0, h.C);
+    emit_gn(B, ops, h, nullptr, "out.gn", true, a);
+    B.drop(h);
+    emit_conv(B, ops, a, nullptr, "conv_out", c.out_ch, {H, W, H, W, 1, 0}, a, nullptr, -1, true,
+              P->eps);
+    B.drop(a);
+  }
+  // per-call context projections
+  for (auto& kr : kv_regions) {
+    const std::string b = kr.first;
+    const size_t kvoff = kr.second, ctxo = P->ctx;
+    const _Float16* w = B.W16(b + ".attn2.kv.w");
+    const int Lc = c.ctx_len, D = c.ctx_dim;
+    const int C = kv_width.at(b);
+    P->pre.push_back([=](const RunCtx& x) {
+      GemmArgs g = dense_args(2 * C, D, w, nullptr);
+      g.M = (int64_t)x.R * Lc;
+      g.src1 = H16(x, ctxo);
+      g.out = x.ws + kvoff;
+      g.ldo = 2 * C;
+      return gemm_launch(g, x.s);
+    });
+  }
+  P->bytes = align_up(B.peak(), 256);
+  return P;
+}
+
+Plan* get_plan(nv_unet* net, int Rmax) {
+  auto it = net->plans.find(Rmax);
+  if (it != net->plans.end()) return it->second.get();
+  auto p = build_plan(net, Rmax);
+  Plan* raw = p.get();
+  net->plans[Rmax] = std::move(p);
+  return raw;
+}
+
+// Host-side weight packing ------------------------------------------------
+bool pack_weights(nv_unet* net, const float* blob) {
+  const auto& c = net->cfg;
+  std::map<std::string, const ParamInfo*> by;
+  for (auto& p : net->params) by[p.name] = &p;
+  auto P = [&](const std::string& n) -> const float* { return blob + by.at(n)->offset; };
+  auto S = [&](const std::string& n) -> const std::vector<int64_t>& { return by.at(n)->shape; };
+  std::vector<_Float16> h16;
+  std::vector<float> h32;
+  std::map<std::string, size_t> o16, o32;
+  auto put32 = [&](const std::string& n, const float* src, int64_t cnt) {
+    o32[n] = h32.size();
+    h32.insert(h32.end(), src, src + cnt);
+    while (h32.size() % 64) h32.push_back(0.f);
+  };
+  auto begin16 = [&](const std::string& n) { o16[n] = h16.size(); };
+  auto end16 = [&]() {
+    while (h16.size() % 128) h16.push_back((_Float16)0.f);
+  };
+  // ResBlock time projections stacked
+  int ttot = 0;
+  for (auto& p : net->params) {
+    const std::string& n = p.name;
+    if (n.size() > 7 && n.compare(n.size() - 7, 7, ".temb.w") == 0) {
+      net->temb_off[n.substr(0, n.size() - 7)] = ttot;
+      ttot += (int)p.shape[0];
+    }
+  }
+  net->temb_total = ttot;
+  {
+    begin16("temb_all.w");
+    std::vector<float> bias;
+    for (auto& p : net->params) {
+      const std::string& n = p.name;
+      if (n.size() > 7 && n.compare(n.size() - 7, 7, ".temb.w") == 0) {
+        const float* src = blob + p.offset;
+        for (int64_t i = 0; i < p.numel(); ++i) h16.push_back((_Float16)src[i]);
+        const std::string bn = n.substr(0, n.size() - 1) + "b";
+        const float* bs = P(bn);
+        bias.insert(bias.end(), bs, bs + p.shape[0]);
+      }
+    }
+    end16();
+    put32("temb_all.b", bias.data(), (int64_t)bias.size());
+  }
+  for (auto& p : net->params) {
+    const std::string& n = p.name;
+    const float* src = blob + p.offset;
+    auto ends = [&](const char* suf) {
+      const size_t l = strlen(suf);
+      return n.size() >= l && n.compare(n.size() - l, l, suf) == 0;
+    };
+    if (ends(".temb.w") || ends(".temb.b")) continue;
+    if (n == "conv_in.w") {
+      put32(n, src, p.numel());
+      continue;
+    }
+    if (p.shape.size() == 1) {
+      if (ends(".ff1.b")) {  // GEGLU packing of the bias
+        const int C8 = (int)p.shape[0], C4 = C8 / 2;
+        std::vector<float> pk(C8);
+        for (int r = 0; r < C8; ++r) {
+          const int grp = r / 32, wi = r % 32;
+          pk[r] = wi < 16 ? src[grp * 16 + wi] : src[C4 + grp * 16 + (wi - 16)];
+        }
+        put32(n, pk.data(), C8);
+      } else {
+        put32(n, src, p.numel());
+      }
+      continue;
+    }
+    if (p.shape.size() == 4) {  // [Co][Ci][3][3] -> [Co][3][3][Ci]
+      const int co = (int)p.shape[0], ci = (int)p.shape[1];
+      begin16(n);
+      for (int o = 0; o < co; ++o)
+        for (int t = 0; t < 9; ++t)
+          for (int i = 0; i < ci; ++i) h16.push_back((_Float16)src[((int64_t)o * ci + i) * 9 + t]);
+      end16();
+      continue;
+    }
+    // 2-D linear weights
+    if (ends(".attn1.q.w")) {
+      const std::string b = n.substr(0, n.size() - 10);
+      begin16(b + ".attn1.qkv.w");
+      for (const char* part : {".attn1.q.w", ".attn1.k.w", ".attn1.v.w"}) {
+        const float* s2 = P(b + part);
+        const int64_t cnt = S(b + part)[0] * S(b + part)[1];
+        for (int64_t i = 0; i < cnt; ++i) h16.push_back((_Float16)s2[i]);
+      }
+      end16();
+      continue;
+    }
+    if (ends(".attn1.k.w") || ends(".attn1.v.w") || ends(".attn2.v.w")) continue;
+    if (ends(".attn2.k.w")) {
+      const std::string b = n.substr(0, n.size() - 10);
+      begin16(b + ".attn2.kv.w");
+      for (const char* part : {".attn2.k.w", ".attn2.v.w"}) {
+        const float* s2 = P(b + part);
+        const int64_t cnt = S(b + part)[0] * S(b + part)[1];
+        for (int64_t i = 0; i < cnt; ++i) h16.push_back((_Float16)s2[i]);
+      }
+      end16();
+      continue;
+    }
+    if (ends(".ff1.w")) {
+      const int C8 = (int)p.shape[0], C4 = C8 / 2, K = (int)p.shape[1];
+      begin16(n);
+      for (int r = 0; r < C8; ++r) {
+        const int grp = r / 32, wi = r % 32;
+        const int srow = wi < 16 ? grp * 16 + wi : C4 + grp * 16 + (wi - 16);
+        for (int k = 0; k < K; ++k) h16.push_back((_Float16)src[(int64_t)srow * K + k]);
+      }
+      end16();
+      continue;
+    }
+    begin16(n);
+    for (int64_t i = 0; i < p.numel(); ++i) h16.push_back((_Float16)src[i]);
+    end16();
+  }
+  if (hipMalloc((void**)&net->d16, std::max<size_t>(h16.size(), 1) * 2) != hipSuccess) return false;
+  if (hipMalloc((void**)&net->d32, std::max<size_t>(h32.size(), 1) * 4) != hipSuccess) return false;
+  if (hipMemcpy(net->d16, h16.data(), h16.size() * 2, hipMemcpyHostToDevice) != hipSuccess)
+    return false;
+  if (hipMemcpy(net->d32, h32.data(), h32.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return false;
+  for (auto& kv : o16) net->w16[kv.first] = net->d16 + kv.second;
+  for (auto& kv : o32) net->w32[kv.first] = net->d32 + kv.second;
+  (void)c;
+  return true;
+}
+
+int32_t check_sched(const nv_schedule* s) {
+  NV_CHECK_ARG(s, "null schedule");
+  NV_CHECK_ARG(s->N >= 1 && s->T >= 2 && s->T <= 1024, "need 1 <= N, 2 <= T <= 1024");
+  NV_CHECK_ARG(s->T % s->N == 0 && s->T / s->N >= 2, "T must be a multiple of N with T/N >= 2");
+  NV_CHECK_ARG(s->beta_start > 0 && s->beta_end > 0 && s->beta_start < 1 && s->beta_end < 1,
+               "betas must be in (0, 1)");
+  return NV_OK;
+}
+
+hipError_t run_ops(const std::vector<Op>& ops, const RunCtx& c) {
+  for (const auto& op : ops) {
+    hipError_t e = op(c);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+}  // namespace nv
+
+using namespace nv;
+
+extern "C" const char* nv_status_string(int32_t s) {
+  switch (s) {
+    case NV_OK: return "ok";
+    case NV_ERR_INVALID_ARG: return "invalid argument";
+    case NV_ERR_UNSUPPORTED: return "unsupported";
+    case NV_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case NV_ERR_HIP: return "HIP runtime error";
+    case NV_ERR_WORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* nv_last_error(void) { return g_err.c_str(); }
+extern "C" const char* nv_version(void) { return "nv 0.1 (gfx950)"; }
+
+extern "C" int64_t nv_unet_param_count(const nv_unet_config* cfg) {
+  std::string why;
+  if (!validate_cfg(cfg, &why)) {
+    set_error(why);
+    return -1;
+  }
+  std::vector<ParamInfo> ps;
+  enumerate_params(*cfg, ps);
+  int64_t n = 0;
+  for (auto& p : ps) n += p.numel();
+  return n;
+}
+
+extern "C" int32_t nv_unet_param_info(const nv_unet_config* cfg, int64_t i, char* name,
+                                      int32_t name_len, int64_t* numel) {
+  std::string why;
+  if (!validate_cfg(cfg, &why)) {
+    set_error(why);
+    return NV_ERR_INVALID_ARG;
+  }
+  std::vector<ParamInfo> ps;
+  enumerate_params(*cfg, ps);
+  NV_CHECK_ARG(i >= 0 && i < (int64_t)ps.size(), "parameter index out of range");
+  NV_CHECK_ARG(name && name_len > 0, "null name buffer");
+  snprintf(name, (size_t)name_len, "%s", ps[i].name.c_str());
+  if (numel) *numel = ps[i].numel();
+  return NV_OK;
+}
+
+extern "C" int32_t nv_unet_create(const nv_unet_config* cfg, const float* weights_host,
+                                  int64_t n_weights, nv_unet** out) {
+  clear_error();
+  NV_CHECK_ARG(out && weights_host, "null output or weights pointer");
+  std::string why;
+  if (!validate_cfg(cfg, &why)) {
+    set_error(why);
+    return NV_ERR_INVALID_ARG;
+  }
+  auto net = std::make_unique<nv_unet>();
+  net->cfg = *cfg;
+  enumerate_params(*cfg, net->params);
+  int64_t total = 0;
+  for (auto& p : net->params) total += p.numel();
+  NV_CHECK_ARG(n_weights == total, "n_weights does not match nv_unet_param_count");
+  if (!pack_weights(net.get(), weights_host)) {
+    if (net->d16) (void)hipFree(net->d16);
+    if (net->d32) (void)hipFree(net->d32);
+    set_error("device allocation or copy of the weights failed");
+    return NV_ERR_OUT_OF_MEMORY;
+  }
+  *out = net.release();
+  return NV_OK;
+}
+
+extern "C" void nv_unet_destroy(nv_unet* net) {
+  if (!net) return;
+  if (net->d16) (void)hipFree(net->d16);
+  if (net->d32) (void)hipFree(net->d32);
+  delete net;
+}
+
+extern "C" size_t nv_denoise_workspace(const nv_unet* cnet, int32_t B) {
+  if (!cnet || B < 1 || B > MAX_SAMPLES) return 0;
+  nv_unet* net = const_cast<nv_unet*>(cnet);
+  try {
+    return get_plan(net, 2 * B)->bytes;
+  } catch (const std::exception& e) {
+    set_error(e.what());
+    return 0;
+  }
+}
+
+namespace {
+int32_t prep_call(nv_unet* net, const nv_schedule* sched, int32_t B, const float* cond,
+                  const float* uncond, const float* pooled, void* workspace, size_t ws_bytes,
+                  Plan** plan) {
+  NV_CHECK_ARG(net, "null handle");
+  int32_t st = check_sched(sched);
+  if (st != NV_OK) return st;
+  NV_CHECK_ARG(B >= 1 && B <= MAX_SAMPLES, "B must be in [1, 64]");
+  NV_CHECK_ARG(cond && uncond, "null context pointer");
+  NV_CHECK_ARG(net->cfg.pooled_dim == 0 || pooled, "pooled vector required by this topology");
+  Plan* p = nullptr;
+  try {
+    p = get_plan(net, 2 * B);
+  } catch (const std::exception& e) {
+    set_error(e.what());
+    return NV_ERR_INVALID_ARG;
+  }
+  if (!workspace || ws_bytes < p->bytes || ((uintptr_t)workspace & 255)) {
+    set_error("denoise workspace missing, misaligned or smaller than nv_denoise_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  *plan = p;
+  return NV_OK;
+}
+}  // namespace
+
+extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent,
+                              const int32_t* k, int32_t B, const float* cond,
+                              const float* uncond, const float* pooled, float guidance,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(latent && k, "null latent or k");
+  NV_CHECK_ARG(std::isfinite(guidance), "guidance must be finite");
+  Plan* P = nullptr;
+  int32_t st = prep_call(net, sched, B, cond, uncond, pooled, workspace, workspace_bytes, &P);
+  if (st != NV_OK) return st;
+  const int N = sched->N;
+  for (int b = 0; b < B; ++b) NV_CHECK_ARG(k[b] >= 0 && k[b] <= N, "k[b] must be in [0, N]");
+  const auto& c = net->cfg;
+  StepArgs sa{};
+  std::vector<int> order(B);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return k[a] < k[b]; });
+  for (int b = 0; b < B; ++b) {
+    sa.perm[b] = order[b];
+    sa.kstep[b] = k[order[b]];
+  }
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const int HW = c.H * c.W;
+  const int64_t lat = (int64_t)c.in_ch * HW;
+  NV_HIP_TRY(schedule_launch(sched->T, N, sched->beta_start, sched->beta_end,
+                             (int32_t*)(ws + P->ts), (float*)(ws + P->at), (float*)(ws + P->ap),
+                             s));
+  NV_HIP_TRY(permute_launch(sa, latent, (float*)(ws + P->x_work), lat, B, 1, s));
+  NV_HIP_TRY(ctx_rows_launch(sa, cond, uncond, (int64_t)c.ctx_len * c.ctx_dim, 2 * B,
+                             (_Float16*)(ws + P->ctx), s));
+  if (c.pooled_dim > 0)
+    NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
+  RunCtx rc{ws, 2 * B, s, (const float*)(ws + P->x_work), sa};
+  NV_HIP_TRY(run_ops(P->pre, rc));
+  for (int j = 0;; ++j) {
+    int A = 0;
+    while (A < B && sa.kstep[A] + j < N) ++A;
+    if (A == 0) break;
+    rc.R = 2 * A;
+    rc.st.j = j;
+    NV_HIP_TRY(run_ops(P->step, rc));
+    NV_HIP_TRY(cfg_ddim_launch(rc.st, (const float*)(ws + P->eps), (float*)(ws + P->x_work),
+                               c.out_ch, HW, A, guidance, (const float*)(ws + P->at),
+                               (const float*)(ws + P->ap), s));
+  }
+  NV_HIP_TRY(permute_launch(sa, (const float*)(ws + P->x_work), latent, lat, B, 0, s));
+  return NV_OK;
+}
+
+extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const float* x,
+                               const int32_t* step_idx, int32_t B, const float* cond,
+                               const float* uncond, const float* pooled, float* eps_uncond,
+                               float* eps_cond, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  clear_error();
+  NV_CHECK_ARG(x && step_idx && eps_uncond && eps_cond, "null pointer argument");
+  Plan* P = nullptr;
+  int32_t st = prep_call(net, sched, B, cond, uncond, pooled, workspace, workspace_bytes, &P);
+  if (st != NV_OK) return st;
+  for (int b = 0; b < B; ++b)
+    NV_CHECK_ARG(step_idx[b] >= 0 && step_idx[b] < sched->N, "step_idx must be in [0, N)");
+  const auto& c = net->cfg;
+  StepArgs sa{};
+  for (int b = 0; b < B; ++b) {
+    sa.perm[b] = b;
+    sa.kstep[b] = step_idx[b];
+  }
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  NV_HIP_TRY(schedule_launch(sched->T, sched->N, sched->beta_start, sched->beta_end,
+                             (int32_t*)(ws + P->ts), (float*)(ws + P->at), (float*)(ws + P->ap),
+                             s));
+  NV_HIP_TRY(ctx_rows_launch(sa, cond, uncond, (int64_t)c.ctx_len * c.ctx_dim, 2 * B,
+                             (_Float16*)(ws + P->ctx), s));
+  if (c.pooled_dim > 0)
+    NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
+  RunCtx rc{ws, 2 * B, s, x, sa};
+  NV_HIP_TRY(run_ops(P->pre, rc));
+  NV_HIP_TRY(run_ops(P->step, rc));
+  NV_HIP_TRY(eps_split_launch((const float*)(ws + P->eps), c.out_ch, c.H * c.W, B, eps_uncond,
+                              eps_cond, s));
+  return NV_OK;
+}

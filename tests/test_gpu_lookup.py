@@ -1,0 +1,162 @@
+"""GPU parity of the cache lookup and state fetch against the oracle.
+
+Bar: idx, sim and K bit-identical to the oracle (Sec. 4.3 Alg. 1 search +
+Sec. 5.3.1 selector), at small sizes spanning several 256-row tiles with
+ragged tails, on the edge cases (ties, overflowing candidate lists, empty
+cache, threshold boundaries) and at the workloads' full sizes.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import lookup as LK
+
+pytestmark = pytest.mark.gpu
+
+TP = [t for t, _ in synth.THRESHOLDS_PAPER]
+KP = [k for _, k in synth.THRESHOLDS_PAPER]
+
+
+def _gpu_lookup(q, cache, thr=TP, kv=KP):
+    import paper_2312_04429_amd as P
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    if cache.dtype == np.uint16:
+        cd = torch.from_numpy(cache.view(np.int16)).cuda() if cache.size else \
+            torch.empty((0, cache.shape[1]), dtype=torch.int16, device="cuda")
+    else:
+        cd = torch.from_numpy(np.ascontiguousarray(cache)).cuda()
+    idx, sim, kk = P.nv_cache_lookup(qd, cd, thr, kv)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), sim.cpu().numpy(), kk.cpu().numpy()
+
+
+def _check(q, cache, thr=TP, kv=KP):
+    gi, gs, gk = _gpu_lookup(q, cache, thr, kv)
+    oi, os_, ok = LK.lookup(q, cache, thr, kv)
+    np.testing.assert_array_equal(gi, oi)
+    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32))
+    np.testing.assert_array_equal(gk, ok)
+    return gi, gs, gk
+
+
+def _rand(n, d, seed, dtype):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((n, d)).astype(np.float32)
+    x /= np.linalg.norm(x, axis=1, keepdims=True) + 1e-30
+    return synth.to_bf16_bits(x) if dtype == "bf16" else x
+
+
+def test_tiny_workload():
+    w = synth.WORKLOADS["tiny"]
+    print("lookup tiny workload", flush=True)
+    cache = synth.make_cache(w["n_cache"], w["d"], w["clusters"], w["sigma"], w["cache_seed"],
+                             "f32", dup_pairs=((300, 700),))
+    tg = [700, 5, 100, 900, 512, 40]
+    q = synth.make_queries_at_sims(cache[tg], w["query_sims"], w["query_seed"])
+    q2 = synth.make_cluster_queries(w["n_cluster_queries"], w["d"], w["clusters"], w["sigma"],
+                                    w["cache_seed"], w["query_seed"])
+    q = np.concatenate([q, q2])
+    thr = [t for t, _ in w["thresholds"]]
+    kv = [k for _, k in w["thresholds"]]
+    gi, _, gk = _check(q, cache, thr, kv)
+    assert gi[0] == 300                      # duplicate rows: lowest index
+    assert list(gk[:2]) == [10, 10]
+
+
+@pytest.mark.parametrize("n,d,m", [(1, 64, 1), (255, 64, 3), (257, 768, 8), (5000, 768, 17),
+                                   (1500, 40, 40), (777, 2048, 2)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_random_caches(n, d, m, dtype):
+    print(f"lookup random n={n} d={d} m={m} {dtype}", flush=True)
+    cache = _rand(n, d, n + d, dtype)
+    rows = synth.cache_rows_f32(cache, np.arange(min(n, m)) * 7 % n)
+    q = np.concatenate([synth.make_queries_at_sims(rows, np.linspace(0.99, 0.6, len(rows)), 3),
+                        _rand(max(0, m - len(rows)), d, 9, "f32")])
+    _check(q, cache)
+
+
+def test_overflowing_candidate_lists():
+    """200 identical rows inside one tile and whole tiles of identical rows."""
+    print("lookup overflow", flush=True)
+    cache = _rand(4000, 768, 1, "bf16")
+    cache[50:250] = cache[1234]
+    q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, [1234]), [0.97], 4)
+    gi, _, gk = _check(q, cache)
+    assert gi[0] == 50 and gk[0] == 25
+    same = np.repeat(_rand(1, 64, 2, "bf16"), 700 * 256 + 3, axis=0)  # > 512 overflowing tiles
+    q = synth.make_queries_at_sims(synth.cache_rows_f32(same, [0]), [0.9], 5)
+    gi, _, _ = _check(q, same)
+    assert gi[0] == 0
+
+
+def test_empty_cache_and_boundaries():
+    print("lookup empty + boundaries", flush=True)
+    q = _rand(3, 64, 1, "f32")
+    gi, gs, gk = _gpu_lookup(q, np.zeros((0, 64), dtype=np.float32))
+    assert list(gi) == [-1] * 3 and np.all(np.isneginf(gs)) and list(gk) == [0] * 3
+    gi, gs, gk = _gpu_lookup(q, np.zeros((0, 64), dtype=np.uint16))
+    assert list(gi) == [-1] * 3
+    # one-hot queries against rows scoring exactly at / one ulp above each threshold
+    vals = []
+    for t in TP:
+        t32 = np.float32(t)
+        vals += [t32, np.nextafter(t32, np.float32(2))]
+    d = 64
+    cache = np.zeros((len(vals), d), dtype=np.float32)
+    q = np.zeros((len(vals), d), dtype=np.float32)
+    for i, v in enumerate(vals):
+        cache[i, i] = v
+        q[i, i] = 1.0
+    gi, gs, gk = _check(q, cache)
+    assert list(gk) == [20, 25, 15, 20, 10, 15, 5, 10, 0, 5]
+
+
+def test_sd15_b1_cache_full_size():
+    w = synth.WORKLOADS["sd15_b1"]
+    print("lookup 100k x 768 bf16", flush=True)
+    cache = synth.make_cache(w["n_cache"], w["d"], w["clusters"], w["sigma"], w["cache_seed"])
+    q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, [31337]), w["query_sims"],
+                                   w["query_seed"])
+    gi, _, gk = _check(q, cache)
+    assert gi[0] == 31337 and gk[0] == 25
+
+
+def test_sd15_b8_cache_full_size_sampled():
+    """1M x 768 bf16 with 8 queries (launch configuration of the benchmark); the oracle
+    scores every row canonically for each query."""
+    w = synth.WORKLOADS["sd15_b8_mixed"]
+    print("lookup 1M x 768 bf16, 8 queries", flush=True)
+    cache = synth.make_cache(w["n_cache"], w["d"], w["clusters"], w["sigma"], w["cache_seed"])
+    tg = np.arange(8) * 123457 % w["n_cache"]
+    sims = [0.97, 0.92, 0.87, 0.8, 0.7, 0.6, 0.99, 0.95]
+    q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, tg), sims, w["query_seed"])
+    gi, gs, gk = _gpu_lookup(q, cache)
+    for j in range(8):
+        sc = LK.canonical_scores(q[j], cache)
+        i, v = LK.top1_fast(sc)
+        assert gi[j] == i and gs[j] == np.float32(v)
+        assert gk[j] == LK.select_k(np.float32(v), TP, KP)
+        print(f"  q{j}: idx {i} sim {v:.6f} K {gk[j]}", flush=True)
+
+
+def test_gather_states():
+    import paper_2312_04429_amd as P
+    print("gather states", flush=True)
+    rng = np.random.default_rng(0)
+    n_store, slots, lat = 6, [5, 10, 15, 20, 25], (4, 8, 8)
+    store = rng.standard_normal((n_store, len(slots)) + lat).astype(np.float32)
+    noise = rng.standard_normal((5,) + lat).astype(np.float32)
+    payload = np.array([3, 1, 5, 0, -1, 2, 4, 7], dtype=np.int32)  # row -> store entry
+    idx = np.array([0, 2, 4, 1, 7], dtype=np.int64)
+    kk = np.array([10, 25, 5, 0, 5], dtype=np.int32)
+    t = lambda a: torch.from_numpy(a).cuda()
+    kd = t(kk.copy())
+    out = P.nv_gather_states(t(store), slots, t(payload), 8, t(idx), kd, t(noise)).cpu().numpy()
+    kout = kd.cpu().numpy()
+    np.testing.assert_array_equal(out[0], store[3, 1])
+    np.testing.assert_array_equal(out[1], store[5, 4])
+    np.testing.assert_array_equal(out[2], noise[2])   # payload -1: miss
+    np.testing.assert_array_equal(out[3], noise[3])   # K = 0
+    np.testing.assert_array_equal(out[4], noise[4])   # payload 7 out of range
+    assert list(kout) == [10, 25, 0, 0, 0]
