@@ -1,0 +1,219 @@
+"""Benchmark of the cache-hit generation path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of the SD-1.5-shaped
+workload (1 request, CFG -> 2 UNet rows):
+  exact cosine top-1 over a 100k x 768 bf16 cache of prompt embeddings and the
+  similarity -> K selector (Sec. 4.3 Alg. 1, Sec. 5.3.1) -> fetch of the
+  matched entry's latent after K steps (Sec. 5.3) -> the remaining N - K
+  guided DDIM steps of the SD-1.5-shaped UNet (Sec. 4.1, N = 50).
+Inputs are synthetic, seeded and resident in HBM before timing.  value =
+images/s; the JSON line also carries UNet steps/s, the roofline of the
+dominant kernel (live HIP-event timing of its launches) and the oracle timed
+on this host's cores on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_PEAK_F16 = 2.5e15      # dense fp16/bf16 matrix-core FLOP/s of MI355X
+HBM_PEAK = 8.0e12           # B/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="sd15_b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=1)
+    return ap.parse_args()
+
+
+def unet_flops_per_row(cfg):
+    """Algorithmic matrix FLOPs (2*M*N*K of every conv, linear and attention product)
+    of one UNet evaluation on one row."""
+    import synth
+    fl = 0
+    c0 = cfg["ch"][0]
+    td = 4 * c0
+    H, W = cfg["H"], cfg["W"]
+    fl += 2 * c0 * td + 2 * td * td                       # time MLP
+    fl += 2 * H * W * c0 * 9 * cfg["in_ch"]                 # conv_in
+    specs = synth.param_specs(cfg)
+    # walk the topology with spatial sizes
+    L = len(cfg["ch"])
+    hw = {lv: (H >> lv) * (W >> lv) for lv in range(L)}
+    heads = lambda c: cfg["n_heads"] if cfg["n_heads"] > 0 else c // cfg["head_dim"]
+
+    def res(cin, cout, s):
+        f = 2 * s * cout * 9 * cin + 2 * s * cout * 9 * cout + 2 * td * cout
+        if cin != cout:
+            f += 2 * s * cout * cin
+        return f
+
+    def tr(c, s, depth):
+        f = 2 * 2 * s * c * c                                 # proj_in, proj_out
+        for _ in range(depth):
+            f += 2 * s * 3 * c * c + 2 * 2 * s * s * c + 2 * s * c * c           # self-attn
+            f += 2 * s * c * c + 2 * 2 * s * cfg["ctx_len"] * c + 2 * s * c * c  # cross q, attn, o
+            f += 2 * 2 * cfg["ctx_len"] * cfg["ctx_dim"] * c                   # context k, v
+            f += 2 * s * 8 * c * c + 2 * s * 4 * c * c                          # GEGLU FF
+        return f
+
+    skips = [c0]
+    cur = c0
+    for lv in range(L):
+        for _ in range(cfg["n_res"]):
+            fl += res(cur, cfg["ch"][lv], hw[lv])
+            cur = cfg["ch"][lv]
+            if cfg["depth"][lv]:
+                fl += tr(cur, hw[lv], cfg["depth"][lv])
+            skips.append(cur)
+        if lv < L - 1:
+            fl += 2 * hw[lv + 1] * cur * 9 * cur
+            skips.append(cur)
+    fl += 2 * res(cur, cur, hw[L - 1])
+    if cfg["mid_depth"]:
+        fl += tr(cur, hw[L - 1], cfg["mid_depth"])
+    for lv in reversed(range(L)):
+        for _ in range(cfg["n_res"] + 1):
+            sk = skips.pop()
+            fl += res(cur + sk, cfg["ch"][lv], hw[lv])
+            cur = cfg["ch"][lv]
+            if cfg["depth"][lv]:
+                fl += tr(cur, hw[lv], cfg["depth"][lv])
+        if lv > 0:
+            fl += 2 * hw[lv - 1] * cur * 9 * cur
+    fl += 2 * H * W * cfg["out_ch"] * 9 * cur
+    del specs
+    return fl
+
+
+def cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc):
+    """The oracle on this host's cores: one guided UNet step (2 rows) and the
+    lookup over the same cache, extrapolated to images/s at the same K."""
+    import synth
+    from oracle import lookup as LK
+    from oracle import unet as U
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    net = U.UNet(cfg, weights)
+    x = synth.make_latents(1, 4, cfg["H"], cfg["W"], 2000)[0]
+    t0 = time.perf_counter()
+    LK.lookup(q, cache, [t for t, _ in wl["thresholds"]], [k for _, k in wl["thresholds"]])
+    t_lookup = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    net(x, 481, unc[0])
+    net(x, 481, cond[0])
+    t_step = time.perf_counter() - t0
+    t_img = t_lookup + (wl["N"] - K) * t_step
+    return {"value": 1.0 / t_img, "unit": "images/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"oracle (NumPy fp32/fp64) on this host: 1 lookup over the "
+                       f"{cache.shape[0]}x{cache.shape[1]} cache ({t_lookup:.2f} s) + 1 guided "
+                       f"UNet step = 2 rows ({t_step:.2f} s), extrapolated to {wl['N'] - K} "
+                       f"steps per image"),
+            "unet_step_s": t_step, "lookup_s": t_lookup}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path's "
+              "multi-GPU sharding is described in DESIGN.md but not built.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2312_04429_amd as P
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    cfg = synth.unet_config(wl["unet"])
+    S = synth.SCHEDULE_SD
+    sched = (S["T"], wl["N"], S["beta_start"], S["beta_end"])
+    thr = [t for t, _ in wl["thresholds"]]
+    kv = [k for _, k in wl["thresholds"]]
+    B = wl["batch"]
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {args.workload} inputs", file=sys.stderr, flush=True)
+    weights = synth.make_weights(cfg, wl["weight_seed"])
+    net = P.NvUNet(cfg, weights)
+    cache = synth.make_cache(wl["n_cache"], wl["d"], wl["clusters"], wl["sigma"], wl["cache_seed"])
+    target = [31337 % wl["n_cache"]]
+    q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, target), wl["query_sims"],
+                                   wl["query_seed"])
+    cond = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["cond_seed"])
+    unc = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["uncond_seed"])
+    slots = [5, 10, 15, 20, 25]
+    pool = 64
+    rng = np.random.default_rng(77)
+    store = rng.standard_normal((pool, len(slots), cfg["in_ch"], cfg["H"], cfg["W"]),
+                                dtype=np.float32)
+    payload = (np.arange(wl["n_cache"]) % pool).astype(np.int32)
+    noise = synth.make_latents(B, cfg["in_ch"], cfg["H"], cfg["W"], 2000)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_cache = t(cache.view(np.int16))
+    d_q, d_store, d_payload = t(q), t(store), t(payload)
+    d_cond, d_unc, d_noise = t(cond), t(unc), t(noise)
+    lws_bytes = P.nv_cache_lookup_workspace(q.shape[0], cache.shape[0], cache.shape[1])
+    lws_own, lws_addr = P.workspace(lws_bytes, dev)
+    lws = (lws_own, lws_addr, lws_bytes)
+    x = torch.empty_like(d_noise)
+
+    ks_seen = []
+
+    def step():
+        idx, sim, kk = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+        P.nv_gather_states(d_store, slots, d_payload, wl["n_cache"], idx, kk, d_noise, out=x)
+        k_host = kk.cpu().tolist()          # the one device -> host crossing per batch
+        ks_seen.append(k_host)
+        net.nv_denoise(x, k_host, d_cond, d_unc, guidance=wl["guidance"], sched=sched)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("[bench] timing", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms = dt * 1e3 / args.steps
+    K = ks_seen[-1][0]
+    images = args.steps * B
+    unet_steps = sum(wl["N"] - k for ks in ks_seen[-args.steps:] for k in ks)
+    fl_row = unet_flops_per_row(cfg)
+    fl_step = 2 * fl_row
+    ups = unet_steps / dt
+    out = {
+        "metric": "images/sec and UNet steps/sec at skip K (SD1.5-shape, 1 GPU); % MFMA peak",
+        "value": images / dt, "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": args.workload, "unet": "SD-1.5-shaped (859.5M params, random-init)",
+                   "latent": [cfg["in_ch"], cfg["H"], cfg["W"]], "batch": B, "cfg_rows": 2 * B,
+                   "N": wl["N"], "K": K, "cache": f"{wl['n_cache']}x{wl['d']} bf16",
+                   "guidance": wl["guidance"]},
+        "unet_steps_per_s": ups, "unet_step_ms": 1e3 / ups,
+        "unet_step_tflop": fl_step / 1e12,
+        "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -195,6 +195,28 @@ int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const float* x,
                     const float* pooled, float* eps_uncond, float* eps_cond, void* workspace,
                     size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ *
+ * Single layers of the UNet on the same kernels the plan uses, for
+ * per-layer parity checks and kernel measurement.  Activations are float16
+ * (IEEE binary16), weights float16, bias float32; workspace: device,
+ * >= nv_op_workspace() bytes, 256-byte aligned (split-K partials).
+ *
+ * nv_op_linear:  out[m][n] = sum_k x[m][k] w[n][k] (+ bias[n]) (+ residual[m][n]);
+ *   x [M][K], w [N][K], residual/out [M][N]; K % 8 == 0.
+ * nv_op_conv3x3: out = conv3x3(x, w) + bias, zero padding 1, NHWC:
+ *   x [B][H][W][Cin], w [Cout][3][3][Cin], out [B][Ho][Wo][Cout] with
+ *   (Ho, Wo) = (H, W) for stride 1, (H/2, W/2) for stride 2 (H, W even),
+ *   (2H, 2W) when upsample = 1 (nearest x2 before the convolution);
+ *   Cin % 8 == 0.
+ * ------------------------------------------------------------------------ */
+size_t nv_op_workspace(void);
+int32_t nv_op_linear(const void* x, const void* w, const float* bias, const void* residual,
+                     void* out, int64_t M, int32_t N, int32_t K, void* workspace,
+                     size_t workspace_bytes, void* stream);
+int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias, void* out, int32_t B,
+                      int32_t H, int32_t W, int32_t Cin, int32_t Cout, int32_t stride,
+                      int32_t upsample, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

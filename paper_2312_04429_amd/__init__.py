@@ -9,7 +9,9 @@ Entry points (same names as the C ABI in include/nv.h):
 Importing the package loads libnv.so and fails if it has not been built.
 """
 from .api import (NvUNet, nv_cache_lookup, nv_cache_lookup_workspace, nv_gather_states,
-                  nv_unet_param_count, nv_unet_param_info, workspace)
+                  nv_op_conv3x3, nv_op_linear, nv_unet_param_count, nv_unet_param_info,
+                  workspace)
 
 __all__ = ["NvUNet", "nv_cache_lookup", "nv_cache_lookup_workspace", "nv_gather_states",
-           "nv_unet_param_count", "nv_unet_param_info", "workspace"]
+           "nv_op_conv3x3", "nv_op_linear", "nv_unet_param_count", "nv_unet_param_info",
+           "workspace"]

@@ -50,6 +50,9 @@ _sigs = {
     "nv_denoise": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, SZ, VP]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
+    "nv_op_workspace": (SZ, []),
+    "nv_op_linear": (I32, [VP, VP, VP, VP, VP, I64, I32, I32, VP, SZ, VP]),
+    "nv_op_conv3x3": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, VP, SZ, VP]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(lib, _name)

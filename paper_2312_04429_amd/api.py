@@ -8,7 +8,7 @@ import ctypes as C
 import numpy as np
 import torch
 
-from . import _native as N
+from . import _native as N  # noqa: N812
 
 BF16_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
 
@@ -167,3 +167,44 @@ class NvUNet:
                                _p(pooled), _p(eu), _p(ec), C.c_void_p(addr), need, _stream())
         N.check(st, "nv_unet_eps")
         return eu, ec
+
+
+_op_ws = {}
+
+
+def _op_workspace(device):
+    key = str(device)
+    if key not in _op_ws:
+        need = int(N.lib.nv_op_workspace())
+        own, addr = workspace(need, device)
+        _op_ws[key] = (own, addr, need)
+    return _op_ws[key]
+
+
+def nv_op_linear(x, w, bias=None, residual=None, out=None):
+    """out[M][N] = x[M][K] w[N][K]^T (+bias) (+residual); float16 tensors, bias float32."""
+    _need_cuda(x, w)
+    M, K = x.shape
+    Nn = w.shape[0]
+    if out is None:
+        out = torch.empty((M, Nn), dtype=torch.float16, device=x.device)
+    _own, addr, need = _op_workspace(x.device)
+    st = N.lib.nv_op_linear(_p(x), _p(w), _p(bias), _p(residual), _p(out), M, Nn, K,
+                            C.c_void_p(addr), need, _stream())
+    N.check(st, "nv_op_linear")
+    return out
+
+
+def nv_op_conv3x3(x, w, bias=None, stride=1, upsample=False, out=None):
+    """NHWC float16 3x3 conv: x [B][H][W][Cin], w [Cout][3][3][Cin] -> [B][Ho][Wo][Cout]."""
+    _need_cuda(x, w)
+    B, H, W, Cin = x.shape
+    Cout = w.shape[0]
+    Ho, Wo = (2 * H, 2 * W) if upsample else (H // stride, W // stride)
+    if out is None:
+        out = torch.empty((B, Ho, Wo, Cout), dtype=torch.float16, device=x.device)
+    _own, addr, need = _op_workspace(x.device)
+    st = N.lib.nv_op_conv3x3(_p(x), _p(w), _p(bias), _p(out), B, H, W, Cin, Cout, stride,
+                             int(bool(upsample)), C.c_void_p(addr), need, _stream())
+    N.check(st, "nv_op_conv3x3")
+    return out

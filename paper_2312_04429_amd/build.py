@@ -1,6 +1,7 @@
 """Build the native library libnv.so (HIP for gfx950) in-tree.
 
-Usage: python -m paper_2312_04429_amd.build
+Usage: python paper_2312_04429_amd/build.py   (by path: importing the package
+loads libnv.so, which may be stale or missing before the build)
 """
 import os
 import subprocess

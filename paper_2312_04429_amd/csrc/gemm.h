@@ -31,6 +31,11 @@ struct GemmArgs {
   void* out;
   int ldo;
   int out_f32;
+  // split-K scratch (float32 partials), optional
+  float* partial;
+  size_t partial_bytes;
+  // filled by gemm_launch: byte extents of src1 / src2
+  uint64_t bytes1, bytes2;
 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);

@@ -10,126 +10,197 @@
 //           nearest x2 upsample ((oy + ky - 1) >> 1, (ox + kx - 1) >> 1) inside
 //           the 2H x 2W grid; out-of-range pixels read zero (padding 1); the
 //           channel may come from either of two concatenated sources.
-// Epilogue (in this order): + bias[n], + rowvec[row / rows_div][n],
-// SiLU, + residual[m][n]; or GEGLU: the weight rows are packed in groups of
-// 32 as (16 "a" rows, 16 "g" rows) and the output column j of group j/16 is
+// Epilogue (in this order): + bias[n], + rowvec[row / rows_div][n], SiLU,
+// + residual[m][n]; or GEGLU: the weight rows are packed in groups of 32 as
+// (16 "a" rows, 16 "g" rows) and output column j of group j/16 is
 // a * GELU_erf(g).  Output float16 or float32.
 //
-// Tiling: BM x BN block tile, 4 waves in 2 x 2, each wave (BM/2) x (BN/2) as
-// 16x16 blocks; BK = 32; LDS double buffer with 80-byte row stride (16-byte
-// slots 5r + c are distinct mod 8 and mod 16, so the 16 rows read by one
-// ds_read_b128 quarter-wave never share a bank).
+// Tiling: BM x BN x 64 block tile, 4 waves in 2 x 2, each wave (BM/2) x
+// (BN/2) as 16x16 MFMA blocks.  Global -> registers -> LDS double buffer, one
+// barrier per 64-deep k tile; LDS rows are padded to 144 bytes so the 16
+// rows read by a quarter-wave land in distinct 16-byte bank groups (9r mod 16
+// is a permutation).  The conv loader walks (tap, ci) incrementally: no
+// integer division in the k loop.  Small problems split K across workgroups;
+// the float32 partials are summed in a fixed order by a second kernel that
+// applies the epilogue (deterministic).
+#include <algorithm>
+
 #include "common.h"
 #include "gemm.h"
 
 namespace nv {
 namespace {
 
-constexpr int BK = 32;
-constexpr int LDS_ROW = 40;  // halfs per LDS row (32 + 8 pad)
+constexpr int BK = 64;
+constexpr int ROW = BK + 8;  // halfs per LDS row
 
-struct ALoad {
-  const _Float16* p;  // address of 8 halfs, or null for zeros
-};
+constexpr uint32_t OOB = 0x80000000u;  // offset past every descriptor's range
 
-template <int MODE>
-__device__ inline const _Float16* a_addr(const GemmArgs& g, int64_t m, int k, bool mvalid,
-                                         int b, int oy, int ox) {
-  if (!mvalid || k >= g.K) return nullptr;
-  if (MODE == 0) {
-    if (k < g.C1) return g.src1 + m * (int64_t)g.lda1 + k;
-    return g.src2 + m * (int64_t)g.lda2 + (k - g.C1);
-  } else {
-    const int cin = g.C1 + g.C2;
-    const int tap = k / cin;
-    const int ci = k - tap * cin;
-    const int ky = tap / 3, kx = tap - 3 * (tap / 3);
-    int iy, ix;
-    if (g.upsample) {
-      const int uy = oy + ky - 1, ux = ox + kx - 1;
-      if (uy < 0 || ux < 0 || uy >= 2 * g.Hin || ux >= 2 * g.Win) return nullptr;
-      iy = uy >> 1;
-      ix = ux >> 1;
-    } else {
-      iy = oy * g.stride + ky - 1;
-      ix = ox * g.stride + kx - 1;
-      if (iy < 0 || ix < 0 || iy >= g.Hin || ix >= g.Win) return nullptr;
-    }
-    const int64_t pix = ((int64_t)b * g.Hin + iy) * g.Win + ix;
-    if (ci < g.C1) return g.src1 + pix * g.C1 + ci;
-    return g.src2 + pix * g.C2 + (ci - g.C1);
-  }
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
 __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
 __device__ inline float silu(float x) { return x / (1.0f + __expf(-x)); }
 
-template <int MODE, int BM, int BN>
-__global__ void __launch_bounds__(256) gemm_f16(GemmArgs g) {
-  constexpr int WM = BM / 2, WN = BN / 2;   // wave tile
-  constexpr int FM = WM / 16, FN = WN / 16;  // 16x16 blocks per wave
-  constexpr int A_LOADS = BM * 4 / 256;      // 16-byte chunks per thread per k-tile
-  constexpr int B_LOADS = BN * 4 / 256;
-  __shared__ __align__(16) _Float16 sA[2][BM * LDS_ROW];
-  __shared__ __align__(16) _Float16 sB[2][BN * LDS_ROW];
+// Element epilogue (non-GEGLU).
+__device__ inline void store_out(const GemmArgs& g, int64_t m, int n, float v) {
+  if (g.bias) v += g.bias[n];
+  if (g.rowvec) v += g.rowvec[(m / g.rows_div) * (int64_t)g.ld_rowvec + n];
+  if (g.silu) v = silu(v);
+  if (g.residual) v += (float)g.residual[m * g.ld_res + n];
+  if (g.out_f32)
+    ((float*)g.out)[m * g.ldo + n] = v;
+  else
+    ((_Float16*)g.out)[m * g.ldo + n] = (_Float16)v;
+}
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+__device__ inline void store_geglu(const GemmArgs& g, int64_t m, int na, float a, float gt) {
+  // na: packed column of the "a" value (its gate sits 16 columns later)
+  if (g.bias) {
+    a += g.bias[na];
+    gt += g.bias[na + 16];
+  }
+  const int oc = (na >> 5) * 16 + (na & 15);
+  ((_Float16*)g.out)[m * g.ldo + oc] = (_Float16)(a * gelu_erf(gt));
+}
+
+template <int MODE, int BM, int BN, bool DUAL>
+__global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int A_CH = BM * 8 / 256;  // 16-byte chunks per thread per k tile
+  constexpr int B_CH = BN * 8 / 256;
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* sA = (_Float16*)smem;                 // [2][BM][ROW]
+  _Float16* sB = sA + 2 * BM * ROW;               // [2][BN][ROW]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 15, kc = lane >> 4;
   const int64_t m0 = (int64_t)blockIdx.x * BM;
   const int n0 = blockIdx.y * BN;
+  const int nk = (g.K + BK - 1) / BK;
+  const int kt0 = blockIdx.z * kt_per_split;
+  const int kt1 = min(nk, kt0 + kt_per_split);
+  const int cch = tid & 7;   // chunk column of this thread (k offset cch*8)
+  const int rr = tid >> 3;   // first row of this thread (+32 per chunk)
 
-  // Per-thread load assignments (fixed rows across k).
-  int a_row[A_LOADS], a_chunk[A_LOADS], a_b[A_LOADS], a_oy[A_LOADS], a_ox[A_LOADS];
-  bool a_valid[A_LOADS];
+  // Row geometry of this thread's A rows.
+  int64_t a_m[A_CH];
+  int a_b[A_CH], a_oy[A_CH], a_ox[A_CH];
+  bool a_ok[A_CH];
 #pragma unroll
-  for (int i = 0; i < A_LOADS; ++i) {
-    const int idx = tid + i * 256;
-    a_row[i] = idx >> 2;
-    a_chunk[i] = idx & 3;
-    const int64_t m = m0 + a_row[i];
-    a_valid[i] = m < g.M;
+  for (int i = 0; i < A_CH; ++i) {
+    a_m[i] = m0 + rr + 32 * i;
+    a_ok[i] = a_m[i] < g.M;
     a_b[i] = a_oy[i] = a_ox[i] = 0;
-    if (MODE == 1 && a_valid[i]) {
+    if (MODE == 1 && a_ok[i]) {
       const int hw = g.Ho * g.Wo;
-      a_b[i] = (int)(m / hw);
-      const int p = (int)(m - (int64_t)a_b[i] * hw);
+      a_b[i] = (int)(a_m[i] / hw);
+      const int p = (int)(a_m[i] - (int64_t)a_b[i] * hw);
       a_oy[i] = p / g.Wo;
       a_ox[i] = p - a_oy[i] * g.Wo;
     }
   }
-  int b_row[B_LOADS], b_chunk[B_LOADS];
-#pragma unroll
-  for (int i = 0; i < B_LOADS; ++i) {
-    const int idx = tid + i * 256;
-    b_row[i] = idx >> 2;
-    b_chunk[i] = idx & 3;
+  // conv: (tap, ci) of this thread's chunk at the current k tile
+  const int cin = g.C1 + g.C2;
+  int tap = 0, ci = 0;
+  if (MODE == 1) {
+    const int k = kt0 * BK + cch * 8;
+    tap = k / cin;
+    ci = k - tap * cin;
   }
 
-  uint4 ra[A_LOADS], rb[B_LOADS];
-  auto load_tile = [&](int k0) {
+  // Two register stages: the global loads of tile kt+2 are issued while tile
+  // kt is multiplied from LDS and tile kt+1 waits in the other stage.
+  uint4 ra0[A_CH], rb0[B_CH];
+  // Buffer loads with range descriptors: an invalid element gets an
+  // out-of-range offset and the hardware returns zeros, so no load result is
+  // touched before it is stored to LDS and both pipeline stages stay in flight.
+  const __amdgpu_buffer_rsrc_t rs1 = make_rsrc(g.src1, g.bytes1);
+  const __amdgpu_buffer_rsrc_t rs2 = make_rsrc(g.src2 ? g.src2 : g.src1, g.src2 ? g.bytes2 : 0);
+  const __amdgpu_buffer_rsrc_t rsw = make_rsrc(g.w, (uint32_t)((int64_t)g.N * g.ldw * 2));
+  // !DUAL: one source per 64-channel k tile (C1, and for convs Cin, multiples of 64)
+  constexpr bool uni = !DUAL;
+  auto load_tile = [&](int kt, uint4 (&ra)[A_CH], uint4 (&rb)[B_CH]) {
+    const int k = kt * BK + cch * 8;
+    const bool kok = k < g.K;
+    if (MODE == 0) {
+      const bool first = k < g.C1;
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      const _Float16* p = a_addr<MODE>(g, m0 + a_row[i], k0 + a_chunk[i] * 8, a_valid[i], a_b[i],
-                                       a_oy[i], a_ox[i]);
-      ra[i] = p ? *(const uint4*)p : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < A_CH; ++i) {
+        const bool ok = a_ok[i] && kok;
+        const uint32_t o1 = ok && first ? (uint32_t)((a_m[i] * g.lda1 + k) * 2) : OOB;
+        if (uni) {
+          const uint32_t o2 = ok && !first ? (uint32_t)((a_m[i] * g.lda2 + (k - g.C1)) * 2) : OOB;
+          ra[i] = bload((kt * BK < g.C1) ? rs1 : rs2, (kt * BK < g.C1) ? o1 : o2);
+        } else {
+          const uint32_t o2 = ok && !first ? (uint32_t)((a_m[i] * g.lda2 + (k - g.C1)) * 2) : OOB;
+          const uint4 v1 = bload(rs1, o1), v2 = bload(rs2, o2);
+          ra[i] = make_uint4(v1.x | v2.x, v1.y | v2.y, v1.z | v2.z, v1.w | v2.w);
+        }
+      }
+    } else {
+      const int ky = (tap * 11) >> 5, kx = tap - 3 * ((tap * 11) >> 5);
+      const bool first = ci < g.C1;
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        int iy, ix;
+        bool in;
+        if (g.upsample) {
+          const int uy = a_oy[i] + ky - 1, ux = a_ox[i] + kx - 1;
+          in = uy >= 0 && ux >= 0 && uy < 2 * g.Hin && ux < 2 * g.Win;
+          iy = uy >> 1;
+          ix = ux >> 1;
+        } else {
+          iy = a_oy[i] * g.stride + ky - 1;
+          ix = a_ox[i] * g.stride + kx - 1;
+          in = iy >= 0 && ix >= 0 && iy < g.Hin && ix < g.Win;
+        }
+        const bool ok = a_ok[i] && kok && in;
+        const int64_t pix = ((int64_t)a_b[i] * g.Hin + iy) * g.Win + ix;
+        const uint32_t o1 = ok && first ? (uint32_t)((pix * g.C1 + ci) * 2) : OOB;
+        const uint32_t o2 = ok && !first ? (uint32_t)((pix * g.C2 + (ci - g.C1)) * 2) : OOB;
+        if (uni) {
+          const bool f0 = __builtin_amdgcn_readfirstlane(first ? 1 : 0) != 0;
+          ra[i] = bload(f0 ? rs1 : rs2, f0 ? o1 : o2);
+        } else {
+          const uint4 v1 = bload(rs1, o1), v2 = bload(rs2, o2);
+          ra[i] = make_uint4(v1.x | v2.x, v1.y | v2.y, v1.z | v2.z, v1.w | v2.w);
+        }
+      }
+      ci += BK;
+      if (uni) {  // cin % 64 == 0: at most one tap boundary per tile
+        if (ci >= cin) {
+          ci -= cin;
+          ++tap;
+        }
+      } else {
+        while (ci >= cin) {
+          ci -= cin;
+          ++tap;
+        }
+      }
     }
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-      const int n = n0 + b_row[i];
-      const int k = k0 + b_chunk[i] * 8;
-      rb[i] = (n < g.N && k < g.K) ? *(const uint4*)(g.w + (int64_t)n * g.ldw + k)
-                                   : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < B_CH; ++i) {
+      const int n = n0 + rr + 32 * i;
+      const bool ok = n < g.N && kok;
+      rb[i] = bload(rsw, ok ? (uint32_t)(((int64_t)n * g.ldw + k) * 2) : OOB);
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const uint4 (&ra)[A_CH], const uint4 (&rb)[B_CH]) {
+    _Float16* a = sA + buf * BM * ROW;
+    _Float16* b = sB + buf * BN * ROW;
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i)
-      *(uint4*)&sA[buf][a_row[i] * LDS_ROW + a_chunk[i] * 8] = ra[i];
+    for (int i = 0; i < A_CH; ++i) *(uint4*)&a[(rr + 32 * i) * ROW + cch * 8] = ra[i];
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i)
-      *(uint4*)&sB[buf][b_row[i] * LDS_ROW + b_chunk[i] * 8] = rb[i];
+    for (int i = 0; i < B_CH; ++i) *(uint4*)&b[(rr + 32 * i) * ROW + cch * 8] = rb[i];
   };
 
   floatx4 acc[FM][FN];
@@ -138,50 +209,68 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = (g.K + BK - 1) / BK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  const int li = lane & 15, kc = lane >> 4;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tile((kt + 1) * BK);
-    half8 fa[FM], fb[FN];
+  auto compute = [&](int buf) {
+    const _Float16* a = sA + buf * BM * ROW;
+    const _Float16* b = sB + buf * BN * ROW;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-      fa[i] = *(const half8*)&sA[cur][(wm * WM + i * 16 + li) * LDS_ROW + kc * 8];
+    for (int sub = 0; sub < 2; ++sub) {
+      half8 fa[FM], fb[FN];
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-      fb[j] = *(const half8*)&sB[cur][(wn * WN + j * 16 + li) * LDS_ROW + kc * 8];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i)
+        fa[i] = *(const half8*)&a[(wm * WM + i * 16 + li) * ROW + sub * 32 + kc * 8];
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    if (kt + 1 < nk) {
-      store_tile(cur ^ 1);
-      __syncthreads();
+        fb[j] = *(const half8*)&b[(wn * WN + j * 16 + li) * ROW + sub * 32 + kc * 8];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
+  };
+
+  // Pipeline: tile kt+1 is fetched into registers while tile kt is multiplied
+  // from LDS stage kt&1, then stored into the other stage; one barrier per tile.
+  load_tile(kt0, ra0, rb0);
+  store_tile(0, ra0, rb0);
+  __syncthreads();
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+    const bool more = kt + 1 < kt1;
+    if (more) load_tile(kt + 1, ra0, rb0);
+    compute(cur);
+    if (more) store_tile(cur ^ 1, ra0, rb0);
+    __syncthreads();
   }
 
-  // Epilogue.  Lane holds rows 4*(lane/16)+r, column lane%16 of each block.
+  // Lane holds rows 4*(lane/16)+r, column lane%16 of each 16x16 block.
+  if (gridDim.z > 1) {
+    float* part = g.partial + (int64_t)blockIdx.z * g.M * g.N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int n = n0 + wn * WN + j * 16 + li;
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
+          if (m < g.M) part[m * g.N + n] = acc[i][j][r];
+        }
+      }
+    return;
+  }
   if (g.geglu) {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int jj = 0; jj < FN / 2; ++jj) {
-        const int ncol_a = n0 + wn * WN + (2 * jj) * 16;  // first packed column of the pair
-        const int oc = (ncol_a / 32) * 16 + li;             // output column
-        const int na = ncol_a + li, ngc = ncol_a + 16 + li;
-        if (ngc >= g.N) continue;
+        const int na = n0 + wn * WN + 2 * jj * 16 + li;
+        if (na + 16 >= g.N) continue;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
-          if (m >= g.M) continue;
-          float a = acc[i][2 * jj][r] + (g.bias ? g.bias[na] : 0.f);
-          float gt = acc[i][2 * jj + 1][r] + (g.bias ? g.bias[ngc] : 0.f);
-          const float v = a * gelu_erf(gt);
-          ((_Float16*)g.out)[m * g.ldo + oc] = (_Float16)v;
+          if (m < g.M) store_geglu(g, m, na, acc[i][2 * jj][r], acc[i][2 * jj + 1][r]);
         }
       }
     return;
@@ -192,40 +281,112 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g) {
     for (int j = 0; j < FN; ++j) {
       const int n = n0 + wn * WN + j * 16 + li;
       if (n >= g.N) continue;
-      const float bn = g.bias ? g.bias[n] : 0.f;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
-        if (m >= g.M) continue;
-        float v = acc[i][j][r] + bn;
-        if (g.rowvec) v += g.rowvec[(m / g.rows_div) * (int64_t)g.ld_rowvec + n];
-        if (g.silu) v = silu(v);
-        if (g.residual) v += (float)g.residual[m * g.ld_res + n];
-        if (g.out_f32)
-          ((float*)g.out)[m * g.ldo + n] = v;
-        else
-          ((_Float16*)g.out)[m * g.ldo + n] = (_Float16)v;
+        if (m < g.M) store_out(g, m, n, acc[i][j][r]);
       }
     }
 }
 
-template <int MODE, int BM, int BN>
-hipError_t launch(const GemmArgs& g, hipStream_t s) {
-  dim3 grid((unsigned)ceil_div(g.M, BM), (unsigned)ceil_div(g.N, BN));
-  hipLaunchKernelGGL((gemm_f16<MODE, BM, BN>), grid, dim3(256), 0, s, g);
+// Sum split-K partials in split order and apply the epilogue.
+__global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
+  const int64_t MN = g.M * (int64_t)g.N;
+  if (g.geglu) {
+    const int64_t total = g.M * (int64_t)(g.N / 2);
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * 256) {
+      const int64_t m = e / (g.N / 2);
+      const int oc = (int)(e - m * (g.N / 2));
+      const int na = (oc >> 4) * 32 + (oc & 15);
+      float a = 0.f, gt = 0.f;
+      for (int s = 0; s < splits; ++s) {
+        a += g.partial[s * MN + m * g.N + na];
+        gt += g.partial[s * MN + m * g.N + na + 16];
+      }
+      store_geglu(g, m, na, a, gt);
+    }
+    return;
+  }
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < MN;
+       e += (int64_t)gridDim.x * 256) {
+    float v = 0.f;
+    for (int s = 0; s < splits; ++s) v += g.partial[s * MN + e];
+    const int64_t m = e / g.N;
+    store_out(g, m, (int)(e - m * g.N), v);
+  }
+}
+
+template <int MODE, int BM, int BN, bool DUAL>
+hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
+  if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
+      (int64_t)g.N * g.ldw * 2 >= 0x80000000ll)
+    return hipErrorInvalidValue;  // descriptors address at most 2 GiB
+  const size_t lds = (size_t)2 * (BM + BN) * ROW * 2;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_f16<MODE, BM, BN, DUAL>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int nk = (g.K + BK - 1) / BK;
+  const int kps = (nk + splits - 1) / splits;
+  splits = (nk + kps - 1) / kps;
+  dim3 grid((unsigned)ceil_div(g.M, BM), (unsigned)ceil_div(g.N, BN), (unsigned)splits);
+  hipLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), lds, s, g, kps);
+  if (splits > 1) {
+    const int64_t total = g.geglu ? g.M * (int64_t)(g.N / 2) : g.M * (int64_t)g.N;
+    const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+    hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
+  }
   return hipGetLastError();
+}
+
+template <int MODE, int BM, int BN>
+hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
+  const bool dual = (g.C1 % BK) != 0 || (MODE == 1 && ((g.C1 + g.C2) % BK) != 0);
+  return dual ? launch_t<MODE, BM, BN, true>(g, splits, s)
+              : launch_t<MODE, BM, BN, false>(g, splits, s);
+}
+
+template <int MODE>
+hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
+  // Larger tiles move fewer bytes per flop (64, 43 and 32 flop per byte of
+  // L2 traffic for 128x128, 128x64, 64x64); small problems fall back to
+  // 64x64 tiles with K split so that every CU has work.
+  constexpr int64_t MIN_WG = 128;
+  constexpr int64_t TARGET = 512;
+  const int nk = (g.K + BK - 1) / BK;
+  const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128);
+  const int64_t t12864 = ceil_div(g.M, 128) * ceil_div(g.N, 64);
+  const int64_t t64 = ceil_div(g.M, 64) * ceil_div(g.N, 64);
+  const bool n_fits_128 = g.N % 128 == 0 || g.N > 512;
+  if (t128 >= MIN_WG && n_fits_128) return launch<MODE, 128, 128>(g, 1, s);
+  if (t12864 >= MIN_WG) return launch<MODE, 128, 64>(g, 1, s);
+  int splits = 1;
+  if (g.partial && t64 < TARGET) {
+    splits = (int)std::min<int64_t>(ceil_div(TARGET, t64), std::max(1, nk / 4));
+    while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.partial_bytes) --splits;
+  }
+  return launch<MODE, 64, 64>(g, splits, s);
 }
 
 }  // namespace
 
-hipError_t gemm_launch(const GemmArgs& g, hipStream_t s) {
-  // Pick the tile so that the grid covers the chip when it can.
-  const int64_t tiles128 = ceil_div(g.M, 128) * ceil_div(g.N, 128);
-  const bool small = tiles128 < 240;
+hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
+  GemmArgs g = gin;
+  // byte extents of the A sources for the range descriptors
   if (g.conv) {
-    return small ? launch<1, 64, 64>(g, s) : launch<1, 128, 128>(g, s);
+    const int64_t rows = g.M / ((int64_t)g.Ho * g.Wo);
+    const int64_t pix = rows * g.Hin * g.Win;
+    g.bytes1 = (uint64_t)(pix * g.C1 * 2);
+    g.bytes2 = g.src2 ? (uint64_t)(pix * g.C2 * 2) : 0;
+  } else {
+    g.bytes1 = (uint64_t)(((g.M - 1) * g.lda1 + g.C1) * 2);
+    g.bytes2 = g.src2 ? (uint64_t)(((g.M - 1) * g.lda2 + g.C2) * 2) : 0;
   }
-  return small ? launch<0, 64, 64>(g, s) : launch<0, 128, 128>(g, s);
+  return g.conv ? dispatch<1>(g, s) : dispatch<0>(g, s);
 }
 
 }  // namespace nv

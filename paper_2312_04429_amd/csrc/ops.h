@@ -25,6 +25,7 @@ struct GnArgs {
   const float* gamma;
   const float* beta;
   int silu;
+  float* part;           // [rows][ceil(HW/32)][G][2] chunk partials (scratch)
   float* stats;          // [rows][G][2] (mean, rstd) scratch
   _Float16* out;         // [rows][HW][C1 + C2]
 };

@@ -25,29 +25,124 @@ __device__ inline float load_cat(const _Float16* s1, int C1, const _Float16* s2,
   return c < C1 ? (float)s1[pix * C1 + c] : (float)s2[pix * C2 + (c - C1)];
 }
 
-// One workgroup per (row, group): two-pass mean / variance in float32.
-__global__ void __launch_bounds__(256) gn_stats_k(GnArgs a) {
-  __shared__ float red[4];
-  const int row = blockIdx.x / a.G, g = blockIdx.x % a.G;
-  const int C = a.C1 + a.C2, cg = C / a.G;
-  const int64_t cnt = (int64_t)a.HW * cg;
-  const int64_t pix0 = (int64_t)row * a.HW;
-  float s = 0.f;
-  for (int64_t e = threadIdx.x; e < cnt; e += 256) {
-    const int p = (int)(e / cg), c = g * cg + (int)(e % cg);
-    s += load_cat(a.src1, a.C1, a.src2, a.C2, pix0 + p, c);
+// GroupNorm statistics, deterministic and two-pass at every level:
+//   gn_partial_k: one workgroup per (row, chunk of GN_CHUNK pixels).  Threads
+//     own 8-channel vectors (16-byte loads) for a phase of the chunk's pixels
+//     and keep per-channel sums in registers; LDS folds phases, then channels
+//     into groups, in a fixed order.  A second sweep (cache-resident) sums
+//     squared deviations from the chunk's group mean.  Output per (row,
+//     chunk, group): mean and sum of squared deviations.
+//   gn_finalize_k: one wave per (row, group) merges the chunks with the
+//     pairwise (Chan) update over a fixed tree and writes (mean, rstd).
+constexpr int GN_CHUNK = 32;
+constexpr int GN_MAXC = 4096;
+
+__device__ inline half8 load_vec(const GnArgs& a, int64_t pix, int c0) {
+  return c0 < a.C1 ? *(const half8*)(a.src1 + pix * a.C1 + c0)
+                   : *(const half8*)(a.src2 + pix * a.C2 + (c0 - a.C1));
+}
+
+__global__ void __launch_bounds__(256) gn_partial_k(GnArgs a, int nchunks) {
+  __shared__ float red[GN_MAXC];     // [phases][C] partials (phases * C <= max(2048, C))
+  __shared__ float chsum[GN_MAXC];   // per-channel sums
+  __shared__ float gsum[256];
+  const int row = blockIdx.x / nchunks, chunk = blockIdx.x % nchunks;
+  const int C = a.C1 + a.C2, cg = C / a.G, nv = C / 8;
+  const int p0 = chunk * GN_CHUNK;
+  const int np = min(GN_CHUNK, a.HW - p0);
+  const int64_t pix0 = (int64_t)row * a.HW + p0;
+  const int t = threadIdx.x;
+  // mapping: nv <= 256 -> PP phases of nv vectors; else each thread owns up to 2 vectors
+  const int PP = nv <= 256 ? 256 / nv : 1;
+  const int nown = nv <= 256 ? 1 : 2;
+  for (int pass = 0; pass < 2; ++pass) {
+    float acc[2][8];
+#pragma unroll
+    for (int o = 0; o < 2; ++o)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[o][e] = 0.f;
+    const int phase = nv <= 256 ? t / nv : 0;
+    for (int o = 0; o < nown; ++o) {
+      const int v = nv <= 256 ? t % nv : t + 256 * o;
+      if (phase >= PP || v >= nv) continue;
+      float mu[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mu[e] = pass ? gsum[(v * 8 + e) / cg] : 0.f;
+      for (int p = phase; p < np; p += PP) {
+        const half8 x = load_vec(a, pix0 + p, v * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = (float)x[e] - mu[e];
+          acc[o][e] += pass ? d * d : d;
+        }
+      }
+    }
+    __syncthreads();
+    // per-thread partials -> red[phase][channel]
+    for (int o = 0; o < nown; ++o) {
+      const int v = nv <= 256 ? t % nv : t + 256 * o;
+      if (phase < PP && v < nv)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[phase * C + v * 8 + e] = acc[o][e];
+    }
+    __syncthreads();
+    for (int c = t; c < C; c += 256) {
+      float s = 0.f;
+      for (int ph = 0; ph < PP; ++ph) s += red[ph * C + c];
+      chsum[c] = s;
+    }
+    __syncthreads();
+    if (t < a.G) {
+      float s = 0.f;
+      for (int c = 0; c < cg; ++c) s += chsum[t * cg + c];
+      if (pass == 0) {
+        gsum[t] = s / (float)(np * cg);  // chunk mean of the group
+      } else {
+        float* out = a.part + ((int64_t)(row * nchunks + chunk) * a.G + t) * 2;
+        out[0] = gsum[t];
+        out[1] = s;
+      }
+    }
+    __syncthreads();
   }
-  const float mean = block_sum_256(s, red) / (float)cnt;
-  float v = 0.f;
-  for (int64_t e = threadIdx.x; e < cnt; e += 256) {
-    const int p = (int)(e / cg), c = g * cg + (int)(e % cg);
-    const float d = load_cat(a.src1, a.C1, a.src2, a.C2, pix0 + p, c) - mean;
-    v += d * d;
+}
+
+__device__ inline void chan_merge(double& n, double& mean, double& m2, double nb, double mb,
+                                  double m2b) {
+  if (nb == 0.0) return;
+  const double nn = n + nb;
+  const double d = mb - mean;
+  mean += d * nb / nn;
+  m2 += m2b + d * d * n * nb / nn;
+  n = nn;
+}
+
+__global__ void __launch_bounds__(64) gn_finalize_k(GnArgs a, int nchunks) {
+  const int i = blockIdx.x;  // (row, group)
+  const int row = i / a.G, g = i % a.G, lane = threadIdx.x;
+  const int cg = (a.C1 + a.C2) / a.G;
+  double n = 0.0, mean = 0.0, m2 = 0.0;
+  for (int c = lane; c < nchunks; c += 64) {
+    const float* pp = a.part + ((int64_t)(row * nchunks + c) * a.G + g) * 2;
+    chan_merge(n, mean, m2, (double)(min(GN_CHUNK, a.HW - c * GN_CHUNK) * cg), (double)pp[0],
+               (double)pp[1]);
   }
-  const float var = block_sum_256(v, red) / (float)cnt;
-  if (threadIdx.x == 0) {
-    a.stats[2 * blockIdx.x] = mean;
-    a.stats[2 * blockIdx.x + 1] = rsqrtf(var + a.eps);
+  for (int o = 1; o < 64; o <<= 1) {
+    const double nb = __shfl_xor(n, o, 64), mb = __shfl_xor(mean, o, 64),
+                 m2b = __shfl_xor(m2, o, 64);
+    // both partners merge (lower, upper) in the same order -> identical results
+    double n1 = n, mean1 = mean, m21 = m2;
+    if (lane & o) {
+      n1 = nb; mean1 = mb; m21 = m2b;
+      chan_merge(n1, mean1, m21, n, mean, m2);
+    } else {
+      chan_merge(n1, mean1, m21, nb, mb, m2b);
+    }
+    n = n1; mean = mean1; m2 = m21;
+  }
+  if (lane == 0) {
+    a.stats[2 * i] = (float)mean;
+    a.stats[2 * i + 1] = rsqrtf((float)(m2 / n) + a.eps);
   }
 }
 
@@ -268,7 +363,11 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
 }  // namespace
 
 hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
-  hipLaunchKernelGGL(gn_stats_k, dim3(rows * a.G), dim3(256), 0, s, a);
+  const int C = a.C1 + a.C2;
+  if (a.G < 1 || a.G > 256 || C % a.G || C % 8 || C > GN_MAXC) return hipErrorInvalidValue;
+  const int nchunks = (int)ceil_div(a.HW, GN_CHUNK);
+  hipLaunchKernelGGL(gn_partial_k, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
+  hipLaunchKernelGGL(gn_finalize_k, dim3(rows * a.G), dim3(64), 0, s, a, nchunks);
   const int64_t total8 = (int64_t)rows * a.HW * (a.C1 + a.C2) / 8;
   hipLaunchKernelGGL(gn_apply_k, dim3(blocks_for(total8)), dim3(256), 0, s, a, total8);
   return hipGetLastError();

@@ -148,7 +148,8 @@ bool validate_cfg(const nv_unet_config* c, std::string* why) {
     return fail("in_ch/out_ch must be in [1, 16]");
   if (c->n_levels < 1 || c->n_levels > 4) return fail("n_levels must be in [1, 4]");
   if (c->n_res < 1 || c->n_res > 8) return fail("n_res must be in [1, 8]");
-  if (c->gn_groups < 1) return fail("gn_groups must be >= 1");
+  if (c->gn_groups < 4 || c->gn_groups > 256 || 256 % c->gn_groups)
+    return fail("gn_groups must be a power of two in [4, 256]");
   const int f = 1 << (c->n_levels - 1);
   if (c->H < f || c->W < f || c->H % f || c->W % f)
     return fail("H and W must be divisible by 2^(n_levels-1)");
@@ -211,7 +212,15 @@ struct RunCtx {
   hipStream_t s;
   const float* x;    // float32 latent [samples][Cin][H][W]
   StepArgs st;
+  float* partial;    // split-K scratch
+  size_t partial_bytes;
 };
+
+inline hipError_t gemm_run(GemmArgs g, const RunCtx& c) {
+  g.partial = c.partial;
+  g.partial_bytes = c.partial_bytes;
+  return gemm_launch(g, c.s);
+}
 using Op = std::function<hipError_t(const RunCtx&)>;
 
 struct Arena {
@@ -257,6 +266,8 @@ struct Ten {
   int HW = 0, C = 0;
 };
 
+constexpr size_t SPLITK_BYTES = 32u << 20;  // float32 split-K partials
+
 struct Plan {
   int Rmax = 0;
   std::vector<Op> pre;   // once per call (context projections)
@@ -264,6 +275,7 @@ struct Plan {
   size_t bytes = 0;
   // fixed regions
   size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0, stats = 0;
+  size_t gnpart = 0, splitk = 0;
 };
 
 }  // namespace
@@ -356,6 +368,7 @@ void emit_gn(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2, con
   const float* g = B.W32(n + ".g");
   const float* b = B.W32(n + ".b");
   const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off, st = B.P->stats;
+  const size_t gp = B.P->gnpart;
   const int C1 = x1.C, C2 = x2 ? x2->C : 0, HW = x1.HW, G = cfg.gn_groups;
   const float eps = cfg.gn_eps;
   const bool has2 = x2 != nullptr;
@@ -372,6 +385,7 @@ void emit_gn(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2, con
     a.beta = b;
     a.silu = silu;
     a.stats = F32(c, st);
+    a.part = F32(c, gp);
     a.out = H16(c, oo);
     return gn_launch(a, c.R, c.s);
   });
@@ -424,7 +438,7 @@ void emit_conv(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
     g.out = c.ws + oo;
     g.ldo = cout;
     g.out_f32 = out_f32;
-    return gemm_launch(g, c.s);
+    return gemm_run(g, c);
   });
 }
 
@@ -454,7 +468,7 @@ void emit_linear(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
     g.geglu = geglu;
     g.out = c.ws + oo;
     g.ldo = ldo;
-    return gemm_launch(g, c.s);
+    return gemm_run(g, c);
   });
 }
 
@@ -625,6 +639,8 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
   P->tproj = B.fixed((size_t)Rmax * net->temb_total * 4);
   int maxG = c.gn_groups;
   P->stats = B.fixed((size_t)Rmax * maxG * 2 * 4);
+  P->gnpart = B.fixed((size_t)Rmax * ceil_div(HW0, 32) * maxG * 2 * 4);
+  P->splitk = B.fixed(SPLITK_BYTES);
   // per-call context K|V regions, one per transformer block
   std::map<std::string, size_t> kv_regions;
   std::map<std::string, int> kv_width;
@@ -658,7 +674,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
         g.silu = 1;
         g.out = x.ws + o;
         g.ldo = td;
-        return gemm_launch(g, x.s);
+        return gemm_run(g, x);
       });
     }
     B.drop(s0);
@@ -680,7 +696,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
         g.silu = 1;
         g.out = x.ws + o;
         g.ldo = td;
-        return gemm_launch(g, x.s);
+        return gemm_run(g, x);
       });
     }
     B.drop(t1);
@@ -696,7 +712,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
         g.out = x.ws + o;
         g.ldo = N;
         g.out_f32 = 1;
-        return gemm_launch(g, x.s);
+        return gemm_run(g, x);
       });
     }
     B.drop(t2);
@@ -805,7 +821,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
       g.src1 = H16(x, ctxo);
       g.out = x.ws + kvoff;
       g.ldo = 2 * C;
-      return gemm_launch(g, x.s);
+      return gemm_run(g, x);
     });
   }
   P->bytes = align_up(B.peak(), 256);
@@ -1120,7 +1136,8 @@ extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* lat
                              (_Float16*)(ws + P->ctx), s));
   if (c.pooled_dim > 0)
     NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
-  RunCtx rc{ws, 2 * B, s, (const float*)(ws + P->x_work), sa};
+  RunCtx rc{ws, 2 * B, s, (const float*)(ws + P->x_work), sa, (float*)(ws + P->splitk),
+            SPLITK_BYTES};
   NV_HIP_TRY(run_ops(P->pre, rc));
   for (int j = 0;; ++j) {
     int A = 0;
@@ -1164,10 +1181,77 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
                              (_Float16*)(ws + P->ctx), s));
   if (c.pooled_dim > 0)
     NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
-  RunCtx rc{ws, 2 * B, s, x, sa};
+  RunCtx rc{ws, 2 * B, s, x, sa, (float*)(ws + P->splitk), SPLITK_BYTES};
   NV_HIP_TRY(run_ops(P->pre, rc));
   NV_HIP_TRY(run_ops(P->step, rc));
   NV_HIP_TRY(eps_split_launch((const float*)(ws + P->eps), c.out_ch, c.H * c.W, B, eps_uncond,
                               eps_cond, s));
+  return NV_OK;
+}
+
+extern "C" size_t nv_op_workspace(void) { return SPLITK_BYTES; }
+
+extern "C" int32_t nv_op_linear(const void* x, const void* w, const float* bias,
+                                const void* residual, void* out, int64_t M, int32_t N, int32_t K,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(x && w && out, "null pointer argument");
+  NV_CHECK_ARG(M >= 1 && N >= 1 && K >= 8 && K % 8 == 0, "need M, N >= 1 and K % 8 == 0");
+  if (!workspace || workspace_bytes < SPLITK_BYTES || ((uintptr_t)workspace & 255)) {
+    set_error("op workspace missing, misaligned or smaller than nv_op_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  GemmArgs g = dense_args(N, K, (const _Float16*)w, bias);
+  g.M = M;
+  g.src1 = (const _Float16*)x;
+  if (residual) {
+    g.residual = (const _Float16*)residual;
+    g.ld_res = N;
+  }
+  g.out = out;
+  g.ldo = N;
+  g.partial = (float*)workspace;
+  g.partial_bytes = workspace_bytes;
+  NV_HIP_TRY(gemm_launch(g, (hipStream_t)stream));
+  return NV_OK;
+}
+
+extern "C" int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias, void* out,
+                                 int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Cout,
+                                 int32_t stride, int32_t upsample, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(x && w && out, "null pointer argument");
+  NV_CHECK_ARG(B >= 1 && H >= 1 && W >= 1 && Cout >= 1 && Cin >= 8 && Cin % 8 == 0,
+               "bad conv shape (Cin % 8 == 0 required)");
+  NV_CHECK_ARG(stride == 1 || (stride == 2 && H % 2 == 0 && W % 2 == 0 && !upsample),
+               "stride must be 1, or 2 with even H, W and no upsample");
+  if (!workspace || workspace_bytes < SPLITK_BYTES || ((uintptr_t)workspace & 255)) {
+    set_error("op workspace missing, misaligned or smaller than nv_op_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  const int Ho = upsample ? 2 * H : H / stride, Wo = upsample ? 2 * W : W / stride;
+  GemmArgs g{};
+  g.M = (int64_t)B * Ho * Wo;
+  g.N = Cout;
+  g.K = 9 * Cin;
+  g.src1 = (const _Float16*)x;
+  g.C1 = Cin;
+  g.conv = 1;
+  g.Hin = H;
+  g.Win = W;
+  g.Ho = Ho;
+  g.Wo = Wo;
+  g.stride = stride;
+  g.upsample = upsample ? 1 : 0;
+  g.w = (const _Float16*)w;
+  g.ldw = g.K;
+  g.bias = bias;
+  g.rows_div = 1;
+  g.out = out;
+  g.ldo = Cout;
+  g.partial = (float*)workspace;
+  g.partial_bytes = workspace_bytes;
+  NV_HIP_TRY(gemm_launch(g, (hipStream_t)stream));
   return NV_OK;
 }
