@@ -33,7 +33,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="sd15_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=1)
+    ap.add_argument("--no-trace", action="store_true",
+                    help="skip the event tracing of kernel launches (for counter passes)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after timing, run one 1 GiB read + 1 GiB write elementwise kernel "
+                         "(calibration dispatch for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -95,6 +99,29 @@ def unet_flops_per_row(cfg):
     fl += 2 * H * W * cfg["out_ch"] * 9 * cur
     del specs
     return fl
+
+
+def kernel_source_sha(family):
+    """Hash of the sources that define a kernel family (to tie stored counters to code)."""
+    import hashlib
+    files = {"conv3x3_igemm": ["gemm.hip", "gemm.h"], "linear_gemm": ["gemm.hip", "gemm.h"],
+             "attention": ["attention.hip"], "cache_scan": ["lookup.hip"]}[family]
+    h = hashlib.sha256()
+    for f in files:
+        h.update(open(os.path.join(ROOT, "paper_2312_04429_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(family):
+    """HBM bytes per launch from stored FETCH_SIZE / WRITE_SIZE counters, if they were
+    taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{family}.json")
+    if not os.path.exists(p):
+        return None
+    rec = json.load(open(p))
+    if rec.get("kernel_source_sha") != kernel_source_sha(family):
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc):
@@ -184,11 +211,24 @@ def main():
         step()
     torch.cuda.synchronize()
     print("[bench] timing", file=sys.stderr, flush=True)
+    fams = {"conv3x3_igemm": P.FAM_CONV, "linear_gemm": P.FAM_LINEAR, "attention": P.FAM_ATTN,
+            "cache_scan": P.FAM_SCAN}
+    if not args.no_trace:
+        P.nv_trace_enable(sum(fams.values()), min(1 << 19, 8000 * args.steps * B + 64))
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    P.nv_trace_disable()
+    kern = {}
+    for name, f in fams.items():
+        n, kms, kfl, kby = P.nv_trace_read(f) if not args.no_trace else (0, 0, 0, 0)
+        if n:
+            kern[name] = {"launches": n, "avg_us": 1e3 * kms / n, "total_ms_per_step": kms / args.steps,
+                          "tflops": kfl / (kms * 1e-3) / 1e12 if kms else None,
+                          "gbps": kby / (kms * 1e-3) / 1e9 if kms else None}
     ms = dt * 1e3 / args.steps
     K = ks_seen[-1][0]
     images = args.steps * B
@@ -208,7 +248,27 @@ def main():
         "unet_steps_per_s": ups, "unet_step_ms": 1e3 / ups,
         "unet_step_tflop": fl_step / 1e12,
         "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16,
+        "kernels": kern,
     }
+    dom = max(kern, key=lambda k: kern[k]["total_ms_per_step"]) if kern else None
+    d = kern.get(dom)
+    if dom is None:
+        out["roofline"] = None
+    elif dom == "cache_scan":
+        out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": d["gbps"], "peak": HBM_PEAK / 1e9,
+                           "unit": "GB/s", "frac": d["gbps"] / (HBM_PEAK / 1e9),
+                           "traffic": traffic_for(dom)}
+    else:
+        out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": d["tflops"],
+                           "peak": MFMA_PEAK_F16 / 1e12, "unit": "TFLOP/s",
+                           "frac": d["tflops"] / (MFMA_PEAK_F16 / 1e12), "traffic": traffic_for(dom),
+                           "launches_per_step": d["launches"] / args.steps,
+                           "avg_launch_us": d["avg_us"]}
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = src * 2.0                      # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc)

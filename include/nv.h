@@ -217,6 +217,26 @@ int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias, void* out
                       int32_t H, int32_t W, int32_t Cin, int32_t Cout, int32_t stride,
                       int32_t upsample, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ *
+ * Launch tracing for measurement.  While enabled, the library records a
+ * pair of HIP events on the launch stream around every kernel launch of the
+ * families in family_mask (the first max_launches launches are kept); each
+ * record carries the launch's algorithmic FLOPs (2 M N K for matrix
+ * products) and bytes.  nv_trace_read waits for the recorded events and
+ * returns the sums over the launches of `family` (a mask).  Enabling again
+ * discards earlier records.  Process-wide, not thread-safe across streams.
+ * ------------------------------------------------------------------------ */
+enum {
+  NV_FAM_CONV = 1,    /* 3x3 implicit-GEMM convolutions (main kernel) */
+  NV_FAM_LINEAR = 2,  /* dense GEMMs (main kernel) */
+  NV_FAM_ATTN = 4,    /* attention */
+  NV_FAM_SCAN = 8     /* cache scan of the lookup */
+};
+int32_t nv_trace_enable(int32_t family_mask, int32_t max_launches);
+int32_t nv_trace_disable(void);
+int32_t nv_trace_read(int32_t family, int64_t* launches, double* ms, double* flops,
+                      double* bytes);
+
 #ifdef __cplusplus
 }
 #endif

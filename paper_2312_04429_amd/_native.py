@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(HERE, "libnv.so")
 NV_OK, NV_ERR_INVALID_ARG, NV_ERR_UNSUPPORTED = 0, -1, -2
 NV_ERR_OUT_OF_MEMORY, NV_ERR_HIP, NV_ERR_WORKSPACE = -3, -4, -5
 NV_F32, NV_BF16 = 0, 1
+NV_FAM_CONV, NV_FAM_LINEAR, NV_FAM_ATTN, NV_FAM_SCAN = 1, 2, 4, 8
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2312_04429_amd.build`")
@@ -50,6 +51,10 @@ _sigs = {
     "nv_denoise": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, SZ, VP]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
+    "nv_trace_enable": (I32, [I32, I32]),
+    "nv_trace_disable": (I32, []),
+    "nv_trace_read": (I32, [I32, C.POINTER(I64), C.POINTER(C.c_double), C.POINTER(C.c_double),
+                            C.POINTER(C.c_double)]),
     "nv_op_workspace": (SZ, []),
     "nv_op_linear": (I32, [VP, VP, VP, VP, VP, I64, I32, I32, VP, SZ, VP]),
     "nv_op_conv3x3": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, VP, SZ, VP]),

@@ -208,3 +208,20 @@ def nv_op_conv3x3(x, w, bias=None, stride=1, upsample=False, out=None):
                              int(bool(upsample)), C.c_void_p(addr), need, _stream())
     N.check(st, "nv_op_conv3x3")
     return out
+
+
+def nv_trace_enable(family_mask, max_launches=65536):
+    N.check(N.lib.nv_trace_enable(family_mask, max_launches), "nv_trace_enable")
+
+
+def nv_trace_disable():
+    N.lib.nv_trace_disable()
+
+
+def nv_trace_read(family):
+    """(launches, ms, flops, bytes) summed over the recorded launches of `family`."""
+    n = C.c_int64()
+    ms, fl, by = C.c_double(), C.c_double(), C.c_double()
+    N.check(N.lib.nv_trace_read(family, C.byref(n), C.byref(ms), C.byref(fl), C.byref(by)),
+            "nv_trace_read")
+    return int(n.value), ms.value, fl.value, by.value

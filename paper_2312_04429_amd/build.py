@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libnv.so")
-SOURCES = ["lookup.hip", "gemm.hip", "attention.hip", "ops.hip", "unet.hip"]
+SOURCES = ["lookup.hip", "gemm.hip", "attention.hip", "ops.hip", "unet.hip", "trace.hip"]
 ARCH = os.environ.get("NV_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -3,149 +3,236 @@
 // latent tokens and cross-attention to the text context (Sec. 2.1: text
 // conditioning enters the UNet through cross-attention).
 //
-// Work split: one workgroup = 64 queries of one (row, head); each wave owns
-// 16 queries.  Keys stream in blocks of 32 through LDS.  The kernel computes
-// the transposed score block S^T = K Q^T so that a lane's accumulator entries
-// all belong to one query (column l % 16): the running max / sum and the
+// Work split: one workgroup = 128 queries of one (row, head); each wave owns
+// 32 queries (two 16-query column blocks).  Keys stream in blocks of 64:
+// the next block is fetched into registers while the current one is used
+// from LDS (double buffer, one barrier per block).  The kernel computes the
+// transposed score block S^T = K Q^T so that every accumulator entry of a
+// lane belongs to one query (column l % 16): the running max / sum and the
 // output rescale are per-lane scalars, and the probabilities P^T are already
-// in the B-operand layout of O^T = V^T P^T (the 8 keys a lane contributes are
-// the 2 x 4 keys it holds; V^T supplies the same 8 keys for its row d).
+// in the B-operand layout of O^T = V^T P^T (the 8 keys a lane contributes to
+// one 32-key MFMA step are the 2 x 4 keys it holds; V^T supplies the same 8
+// keys for its row d).
 #include "common.h"
 #include "attention.h"
+#include "trace.h"
 
 namespace nv {
 namespace {
 
-constexpr int QPW = 16;  // queries per wave
-constexpr int KB = 32;   // keys per block
+constexpr int QB = 2;    // 16-query column blocks per wave
+constexpr int KB = 64;   // keys per block
 constexpr float LOG2E = 1.4426950408889634f;
 
 template <int DP, int DV>
 __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
-  constexpr int KROW = DP + 8;   // halfs per LDS key row
-  constexpr int VROW = KB + 8;   // halfs per LDS V^T row
-  __shared__ __align__(16) _Float16 sK[KB * KROW];
-  __shared__ __align__(16) _Float16 sVt[DV * VROW];
+  constexpr int KROW = DP + 8;          // halfs per LDS key row (16-byte slots 4k+1 apart)
+  constexpr int VROW = KB + 8;          // halfs per LDS V^T row
+  constexpr int KCH = KB * (DP / 8);    // 16-byte chunks of a K block
+  constexpr int VCH = KB * (DV / 8);
+  constexpr int KPT = (KCH + 255) / 256;  // chunks per thread
+  constexpr int VPT = (VCH + 255) / 256;
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                      // [2]
+  _Float16 (*sVt)[DV * VROW] = (_Float16 (*)[DV * VROW])(smem + 2 * KB * KROW * 2);  // [2]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, kc = lane >> 4;
-  const int head = blockIdx.y, row = blockIdx.z;
-  const int q = blockIdx.x * 64 + wave * QPW + li;
-  const bool qv = q < a.S;
+  // 1-D grid; an XCD owns a contiguous range of (row, head, query block) ids so
+  // the query blocks of one head share its K / V through that XCD's L2
+  const int nqb = (a.S + 64 * QB - 1) / (64 * QB);
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int qblk = id % nqb, head = (id / nqb) % a.heads, row = id / (nqb * a.heads);
   const int dh = a.dh;
+  const int q0 = qblk * (64 * QB) + wave * (16 * QB);
 
-  // Q^T fragments (B operand): query li, dims ks*32 + kc*8 .. +8.
-  half8 fq[DP / 32];
-  const _Float16* qrow = a.q + ((int64_t)row * a.S + (qv ? q : 0)) * a.ldq + head * dh;
+  // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8.
+  half8 fq[QB][DP / 32];
 #pragma unroll
-  for (int ks = 0; ks < DP / 32; ++ks) {
-    const int d0 = ks * 32 + kc * 8;
-    if (qv && d0 < dh)
-      fq[ks] = *(const half8*)(qrow + d0);
-    else
-      fq[ks] = half8{0, 0, 0, 0, 0, 0, 0, 0};
+  for (int qb = 0; qb < QB; ++qb) {
+    const int q = q0 + qb * 16 + li;
+    const _Float16* qrow = a.q + ((int64_t)row * a.S + (q < a.S ? q : 0)) * a.ldq + head * dh;
+#pragma unroll
+    for (int ks = 0; ks < DP / 32; ++ks) {
+      const int d0 = ks * 32 + kc * 8;
+      if (q < a.S && d0 < dh)
+        fq[qb][ks] = *(const half8*)(qrow + d0);
+      else
+        fq[qb][ks] = half8{0, 0, 0, 0, 0, 0, 0, 0};
+    }
   }
 
-  floatx4 acc[DV / 16];
+  floatx4 acc[QB][DV / 16];
 #pragma unroll
-  for (int j = 0; j < DV / 16; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  float mrun = -INFINITY, lrun = 0.f;
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int j = 0; j < DV / 16; ++j) acc[qb][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float mrun[QB], lrun[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    mrun[qb] = -INFINITY;
+    lrun[qb] = 0.f;
+  }
   const float sc = a.scale * LOG2E;
 
   const _Float16* kbase = a.k + (int64_t)row * a.L * a.ldk + head * dh;
   const _Float16* vbase = a.v + (int64_t)row * a.L * a.ldv + head * dh;
   const int nkb = (a.L + KB - 1) / KB;
-  for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    // K block -> sK[key][d]; V block -> sVt[d][key] (zero padded).
-    for (int c = tid; c < KB * (DP / 8); c += 256) {
+
+  uint4 rk[KPT], rv[VPT];
+  auto fetch = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * 256;
       const int kr = c / (DP / 8), d0 = (c % (DP / 8)) * 8;
       const int j = kb * KB + kr;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (j < a.L && d0 < dh) v = *(const uint4*)(kbase + (int64_t)j * a.ldk + d0);
-      *(uint4*)&sK[kr * KROW + d0] = v;
+      rk[i] = (c < KCH && j < a.L && d0 < dh) ? *(const uint4*)(kbase + (int64_t)j * a.ldk + d0)
+                                             : make_uint4(0, 0, 0, 0);
     }
-    for (int c = tid; c < KB * (DV / 8); c += 256) {
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int c = tid + i * 256;
       const int kr = c / (DV / 8), d0 = (c % (DV / 8)) * 8;
       const int j = kb * KB + kr;
-      half8 v = half8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (j < a.L && d0 < dh) v = *(const half8*)(vbase + (int64_t)j * a.ldv + d0);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sVt[(d0 + e) * VROW + kr] = v[e];
+      rv[i] = (c < VCH && j < a.L && d0 < dh) ? *(const uint4*)(vbase + (int64_t)j * a.ldv + d0)
+                                             : make_uint4(0, 0, 0, 0);
     }
-    __syncthreads();
-    // S^T for the two 16-key halves.
-    floatx4 s[2];
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      s[h] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < DP / 32; ++ks) {
-        const half8 fk = *(const half8*)&sK[(h * 16 + li) * KROW + ks * 32 + kc * 8];
-        s[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk, fq[ks], s[h], 0, 0, 0);
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * 256;
+      if (c < KCH) {
+        const int kr = c / (DP / 8), d0 = (c % (DP / 8)) * 8;
+        *(uint4*)&sK[buf][kr * KROW + d0] = rk[i];
       }
     }
-    // Lane holds keys h*16 + 4*kc + r for query li.
-    float mloc = -INFINITY;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int i = 0; i < VPT; ++i) {
+      const int c = tid + i * 256;
+      if (c < VCH) {
+        const int kr = c / (DV / 8), d0 = (c % (DV / 8)) * 8;
+        const half8 v = *(const half8*)&rv[i];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = kb * KB + h * 16 + kc * 4 + r;
-        const float v = j < a.L ? s[h][r] * sc : -INFINITY;
-        s[h][r] = v;
-        mloc = fmaxf(mloc, v);
+        for (int e = 0; e < 8; ++e) sVt[buf][(d0 + e) * VROW + kr] = v[e];
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float mnew = fmaxf(mrun, mloc);
-    const float alpha = exp2f(mrun - mnew);
-    mrun = mnew;
-    half8 fp;
-    float psum = 0.f;
+    }
+  };
+
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int cur = kb & 1;
+    const bool more = kb + 1 < nkb;
+    if (more) fetch(kb + 1);
+    const _Float16* K_ = sK[cur];
+    const _Float16* V_ = sVt[cur];
+    // S^T for 4 key quarters x QB query blocks; lane holds keys h*16 + 4*kc + r.
+    floatx4 s[QB][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 4; ++h) {
+      half8 fk[DP / 32];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(s[h][r] - mnew);
-        psum += p;
-        fp[h * 4 + r] = (_Float16)p;
+      for (int ks = 0; ks < DP / 32; ++ks)
+        fk[ks] = *(const half8*)&K_[(h * 16 + li) * KROW + ks * 32 + kc * 8];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        s[qb][h] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < DP / 32; ++ks)
+          s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
       }
-    lrun = lrun * alpha + psum;
+    }
+    const bool tail = (kb + 1) * KB > a.L;
+    half8 fp[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = s[qb][h][r] * sc;
+          if (tail && kb * KB + h * 16 + kc * 4 + r >= a.L) v = -INFINITY;
+          s[qb][h][r] = v;
+          mloc = fmaxf(mloc, v);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float mnew = fmaxf(mrun[qb], mloc);
+      const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
+      mrun[qb] = mnew;
+      float psum = 0.f;
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = __builtin_amdgcn_exp2f(s[qb][h][r] - mnew);
+          psum += p;
+          fp[qb][h >> 1][(h & 1) * 4 + r] = (_Float16)p;
+        }
+      lrun[qb] = lrun[qb] * alpha + psum;
+#pragma unroll
+      for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
+    }
+    // O^T += V^T P^T over two 32-key steps
 #pragma unroll
     for (int j = 0; j < DV / 16; ++j) {
-      acc[j] *= alpha;
-      // V^T rows d = j*16 + li, keys {4kc..4kc+3} and {16+4kc..16+4kc+3}
-      const _Float16* vr = &sVt[(j * 16 + li) * VROW];
-      half8 fv;
-      const half4 lo = *(const half4*)(vr + kc * 4);
-      const half4 hi = *(const half4*)(vr + 16 + kc * 4);
-      fv[0] = lo[0]; fv[1] = lo[1]; fv[2] = lo[2]; fv[3] = lo[3];
-      fv[4] = hi[0]; fv[5] = hi[1]; fv[6] = hi[2]; fv[7] = hi[3];
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp, acc[j], 0, 0, 0);
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const _Float16* vr = &V_[(j * 16 + li) * VROW + st * 32];
+        const half4 lo = *(const half4*)(vr + kc * 4);
+        const half4 hi = *(const half4*)(vr + 16 + kc * 4);
+        half8 fv;
+        fv[0] = lo[0]; fv[1] = lo[1]; fv[2] = lo[2]; fv[3] = lo[3];
+        fv[4] = hi[0]; fv[5] = hi[1]; fv[6] = hi[2]; fv[7] = hi[3];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          acc[qb][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp[qb][st], acc[qb][j], 0, 0, 0);
+      }
     }
+    if (more) stash(cur ^ 1);
+    __syncthreads();
   }
-  lrun += __shfl_xor(lrun, 16, 64);
-  lrun += __shfl_xor(lrun, 32, 64);
-  if (!qv) return;
-  const float inv = 1.0f / lrun;
-  _Float16* orow = a.o + ((int64_t)row * a.S + q) * a.ldo + head * dh;
 #pragma unroll
-  for (int j = 0; j < DV / 16; ++j) {
-    const int d0 = j * 16 + kc * 4;
-    if (d0 < dh) {
-      half4 o;
+  for (int qb = 0; qb < QB; ++qb) {
+    float l = lrun[qb];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const int q = q0 + qb * 16 + li;
+    if (q >= a.S) continue;
+    const float inv = 1.0f / l;
+    _Float16* orow = a.o + ((int64_t)row * a.S + q) * a.ldo + head * dh;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o[r] = (_Float16)(acc[j][r] * inv);
-      *(half4*)(orow + d0) = o;
+    for (int j = 0; j < DV / 16; ++j) {
+      const int d0 = j * 16 + kc * 4;
+      if (d0 < dh) {
+        half4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (_Float16)(acc[qb][j][r] * inv);
+        *(half4*)(orow + d0) = o;
+      }
     }
   }
 }
 
 template <int DP, int DV>
 hipError_t launch(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)ceil_div(a.S, 64), (unsigned)a.heads, (unsigned)a.rows);
-  hipLaunchKernelGGL((attn_f16<DP, DV>), grid, dim3(256), 0, s, a);
+  const size_t lds = (size_t)2 * (KB * (DP + 8) + DV * (KB + 8)) * 2;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DP, DV>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  dim3 grid((unsigned)(ceil_div(a.S, 64 * QB) * a.heads * a.rows));
+  const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
+  const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
+  trace_pre(NV_FAM_ATTN, flops, bytes, s);
+  hipLaunchKernelGGL((attn_f16<DP, DV>), grid, dim3(256), lds, s, a);
+  trace_post(NV_FAM_ATTN, s);
   return hipGetLastError();
 }
 

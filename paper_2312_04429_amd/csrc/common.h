@@ -49,6 +49,17 @@ void clear_error();
     }                                                                             \
   } while (0)
 
+// Workgroups are dealt round-robin to the XCDs (hardware id b runs on XCD
+// b % NXCD), each with its own L2.  xcd_remap turns the hardware id into a
+// logical id so that each XCD owns one contiguous range of logical ids: tiles
+// that share operands then share an L2.  Bijective on [0, total).
+constexpr int NXCD = 8;
+__device__ inline int xcd_remap(int b, int total) {
+  const int x = b % NXCD, local = b / NXCD;
+  const int base = total / NXCD, rem = total % NXCD;
+  return x * base + (x < rem ? x : rem) + local;
+}
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

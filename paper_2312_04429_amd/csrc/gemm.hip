@@ -27,6 +27,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "trace.h"
 
 namespace nv {
 namespace {
@@ -82,8 +83,14 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 15, kc = lane >> 4;
-  const int64_t m0 = (int64_t)blockIdx.x * BM;
-  const int n0 = blockIdx.y * BN;
+  // 1-D grid of tiles; each XCD owns a contiguous range of logical tiles.  When
+  // the activations are the larger operand an XCD owns M-rows (N fastest), else
+  // it owns weight columns (M fastest), so the big operand is read once.
+  const int ntn = (g.N + BN - 1) / BN;
+  const int mtn = (int)((g.M + BM - 1) / BM);
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t m0 = (int64_t)(g.n_major ? tile % mtn : tile / ntn) * BM;
+  const int n0 = (g.n_major ? tile / mtn : tile % ntn) * BN;
   const int nk = (g.K + BK - 1) / BK;
   const int kt0 = blockIdx.z * kt_per_split;
   const int kt1 = min(nk, kt0 + kt_per_split);
@@ -229,19 +236,27 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
     }
   };
 
-  // Pipeline: tile kt+1 is fetched into registers while tile kt is multiplied
-  // from LDS stage kt&1, then stored into the other stage; one barrier per tile.
+  // Pipeline, two tiles deep: while tile kt is multiplied from LDS stage kt&1,
+  // tile kt+1 waits in one register set and tile kt+2 is being fetched into
+  // the other; loads past the last tile re-read the last tile (never used).
+  uint4 ra1[A_CH], rb1[B_CH];
+  const int klast = max(kt0, kt1 - 1);
   load_tile(kt0, ra0, rb0);
   store_tile(0, ra0, rb0);
+  load_tile(min(kt0 + 1, klast), ra1, rb1);
   __syncthreads();
-  for (int kt = kt0; kt < kt1; ++kt) {
-    const int cur = (kt - kt0) & 1;
-    const bool more = kt + 1 < kt1;
-    if (more) load_tile(kt + 1, ra0, rb0);
-    compute(cur);
-    if (more) store_tile(cur ^ 1, ra0, rb0);
+  int kt = kt0;
+  for (; kt + 1 < kt1; kt += 2) {
+    load_tile(min(kt + 2, klast), ra0, rb0);
+    compute(0);
+    store_tile(1, ra1, rb1);
+    __syncthreads();
+    load_tile(min(kt + 3, klast), ra1, rb1);
+    compute(1);
+    store_tile(0, ra0, rb0);
     __syncthreads();
   }
+  if (kt < kt1) compute(0);
 
   // Lane holds rows 4*(lane/16)+r, column lane%16 of each 16x16 block.
   if (gridDim.z > 1) {
@@ -333,8 +348,14 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   const int nk = (g.K + BK - 1) / BK;
   const int kps = (nk + splits - 1) / splits;
   splits = (nk + kps - 1) / kps;
-  dim3 grid((unsigned)ceil_div(g.M, BM), (unsigned)ceil_div(g.N, BN), (unsigned)splits);
+  dim3 grid((unsigned)(ceil_div(g.M, BM) * ceil_div(g.N, BN)), 1, (unsigned)splits);
+  const int fam = MODE == 1 ? NV_FAM_CONV : NV_FAM_LINEAR;
+  const double flops = 2.0 * (double)g.M * g.N * g.K;
+  const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
+                       (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
+  trace_pre(fam, flops, bytes, s);
   hipLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), lds, s, g, kps);
+  trace_post(fam, s);
   if (splits > 1) {
     const int64_t total = g.geglu ? g.M * (int64_t)(g.N / 2) : g.M * (int64_t)g.N;
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
@@ -362,8 +383,13 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
   const int64_t t12864 = ceil_div(g.M, 128) * ceil_div(g.N, 64);
   const int64_t t64 = ceil_div(g.M, 64) * ceil_div(g.N, 64);
   const bool n_fits_128 = g.N % 128 == 0 || g.N > 512;
-  if (t128 >= MIN_WG && n_fits_128) return launch<MODE, 128, 128>(g, 1, s);
-  if (t12864 >= MIN_WG) return launch<MODE, 128, 64>(g, 1, s);
+  // mid-size problems: two K halves when the grid would leave CUs idle
+  auto halves = [&](int64_t tiles) {
+    return (tiles < 256 && nk >= 16 && g.partial &&
+            (size_t)2 * g.M * g.N * 4 <= g.partial_bytes) ? 2 : 1;
+  };
+  if (t128 >= MIN_WG && n_fits_128) return launch<MODE, 128, 128>(g, halves(t128), s);
+  if (t12864 >= MIN_WG) return launch<MODE, 128, 64>(g, halves(t12864), s);
   int splits = 1;
   if (g.partial && t64 < TARGET) {
     splits = (int)std::min<int64_t>(ceil_div(TARGET, t64), std::max(1, nk / 4));
@@ -386,6 +412,7 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
     g.bytes1 = (uint64_t)(((g.M - 1) * g.lda1 + g.C1) * 2);
     g.bytes2 = g.src2 ? (uint64_t)(((g.M - 1) * g.lda2 + g.C2) * 2) : 0;
   }
+  g.n_major = (int64_t)g.N >= g.M;  // weights at least as large as the activation rows
   return g.conv ? dispatch<1>(g, s) : dispatch<0>(g, s);
 }
 

@@ -20,6 +20,7 @@
 #include <cmath>
 
 #include "common.h"
+#include "trace.h"
 
 namespace nv {
 namespace {
@@ -441,12 +442,16 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
       if (lds > 65536)
         NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
       hipLaunchKernelGGL(lk_scan_bf16, dim3(T), dim3(256), lds, s, (const uint16_t*)cache, n, d,
                          m, T, ws);
+      trace_post(NV_FAM_SCAN, s);
       NV_LAUNCH_CHECK("lk_scan_bf16");
     } else {
+      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 4.0 * (double)n * d, s);
       hipLaunchKernelGGL(lk_scan_f32, dim3(T), dim3(256), 0, s, (const float*)cache, n, d,
                          queries, m, T, ws);
+      trace_post(NV_FAM_SCAN, s);
       NV_LAUNCH_CHECK("lk_scan_f32");
     }
   }
