@@ -201,21 +201,23 @@ int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const float* x,
  * (IEEE binary16), weights float16, bias float32; workspace: device,
  * >= nv_op_workspace() bytes, 256-byte aligned (split-K partials).
  *
- * nv_op_linear:  out[m][n] = sum_k x[m][k] w[n][k] (+ bias[n]) (+ residual[m][n]);
- *   x [M][K], w [N][K], residual/out [M][N]; K % 8 == 0.
- * nv_op_conv3x3: out = conv3x3(x, w) + bias, zero padding 1, NHWC:
- *   x [B][H][W][Cin], w [Cout][3][3][Cin], out [B][Ho][Wo][Cout] with
- *   (Ho, Wo) = (H, W) for stride 1, (H/2, W/2) for stride 2 (H, W even),
- *   (2H, 2W) when upsample = 1 (nearest x2 before the convolution);
- *   Cin % 8 == 0.
+ * nv_op_linear:  out[m][n] = sum_k a[m][k] w[n][k] (+ bias[n]) (+ residual[m][n]),
+ *   a = [x | x2] the channel concatenation of x [M][K1] and x2 [M][K2] (x2 NULL,
+ *   K2 = 0 for one source); w [N][K1+K2], residual/out [M][N]; K1, K2 % 8 == 0.
+ * nv_op_conv3x3: out = conv3x3([x | x2], w) + bias, zero padding 1, NHWC:
+ *   x [B][H][W][Cin1], x2 [B][H][W][Cin2] (NULL, 0 for one source),
+ *   w [Cout][3][3][Cin1+Cin2], out [B][Ho][Wo][Cout] with (Ho, Wo) = (H, W) for
+ *   stride 1, (H/2, W/2) for stride 2 (H, W even), (2H, 2W) when upsample = 1
+ *   (nearest x2 before the convolution); Cin1, Cin2 % 8 == 0.
  * ------------------------------------------------------------------------ */
 size_t nv_op_workspace(void);
-int32_t nv_op_linear(const void* x, const void* w, const float* bias, const void* residual,
-                     void* out, int64_t M, int32_t N, int32_t K, void* workspace,
-                     size_t workspace_bytes, void* stream);
-int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias, void* out, int32_t B,
-                      int32_t H, int32_t W, int32_t Cin, int32_t Cout, int32_t stride,
-                      int32_t upsample, void* workspace, size_t workspace_bytes, void* stream);
+int32_t nv_op_linear(const void* x, const void* x2, const void* w, const float* bias,
+                     const void* residual, void* out, int64_t M, int32_t N, int32_t K1,
+                     int32_t K2, void* workspace, size_t workspace_bytes, void* stream);
+int32_t nv_op_conv3x3(const void* x, const void* x2, const void* w, const float* bias, void* out,
+                      int32_t B, int32_t H, int32_t W, int32_t Cin1, int32_t Cin2, int32_t Cout,
+                      int32_t stride, int32_t upsample, void* workspace, size_t workspace_bytes,
+                      void* stream);
 
 /* ------------------------------------------------------------------------ *
  * Launch tracing for measurement.  While enabled, the library records a

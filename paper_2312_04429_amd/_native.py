@@ -56,8 +56,9 @@ _sigs = {
     "nv_trace_read": (I32, [I32, C.POINTER(I64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                             C.POINTER(C.c_double)]),
     "nv_op_workspace": (SZ, []),
-    "nv_op_linear": (I32, [VP, VP, VP, VP, VP, I64, I32, I32, VP, SZ, VP]),
-    "nv_op_conv3x3": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, VP, SZ, VP]),
+    "nv_op_linear": (I32, [VP, VP, VP, VP, VP, VP, I64, I32, I32, I32, VP, SZ, VP]),
+    "nv_op_conv3x3": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, I32, VP, SZ,
+                            VP]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(lib, _name)

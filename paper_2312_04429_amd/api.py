@@ -181,34 +181,35 @@ def _op_workspace(device):
     return _op_ws[key]
 
 
-def nv_op_linear(x, w, bias=None, residual=None, out=None):
-    """out[M][N] = x[M][K] w[N][K]^T (+bias) (+residual); float16 tensors, bias float32."""
-    _need_cuda(x, w)
-    M, K = x.shape
+def nv_op_linear(x, w, bias=None, residual=None, out=None, x2=None):
+    """out[M][N] = [x | x2][M][K] w[N][K]^T (+bias) (+residual); float16, bias float32."""
+    _need_cuda(x, w, x2)
+    M, K1 = x.shape
+    K2 = x2.shape[1] if x2 is not None else 0
     Nn = w.shape[0]
     if out is None:
         out = torch.empty((M, Nn), dtype=torch.float16, device=x.device)
     _own, addr, need = _op_workspace(x.device)
-    st = N.lib.nv_op_linear(_p(x), _p(w), _p(bias), _p(residual), _p(out), M, Nn, K,
+    st = N.lib.nv_op_linear(_p(x), _p(x2), _p(w), _p(bias), _p(residual), _p(out), M, Nn, K1, K2,
                             C.c_void_p(addr), need, _stream())
     N.check(st, "nv_op_linear")
     return out
 
 
-def nv_op_conv3x3(x, w, bias=None, stride=1, upsample=False, out=None):
-    """NHWC float16 3x3 conv: x [B][H][W][Cin], w [Cout][3][3][Cin] -> [B][Ho][Wo][Cout]."""
-    _need_cuda(x, w)
-    B, H, W, Cin = x.shape
+def nv_op_conv3x3(x, w, bias=None, stride=1, upsample=False, out=None, x2=None):
+    """NHWC float16 3x3 conv of [x | x2]: x [B][H][W][Cin1], w [Cout][3][3][Cin] -> [B][Ho][Wo][Cout]."""
+    _need_cuda(x, w, x2)
+    B, H, W, Cin1 = x.shape
+    Cin2 = x2.shape[3] if x2 is not None else 0
     Cout = w.shape[0]
     Ho, Wo = (2 * H, 2 * W) if upsample else (H // stride, W // stride)
     if out is None:
         out = torch.empty((B, Ho, Wo, Cout), dtype=torch.float16, device=x.device)
     _own, addr, need = _op_workspace(x.device)
-    st = N.lib.nv_op_conv3x3(_p(x), _p(w), _p(bias), _p(out), B, H, W, Cin, Cout, stride,
-                             int(bool(upsample)), C.c_void_p(addr), need, _stream())
+    st = N.lib.nv_op_conv3x3(_p(x), _p(x2), _p(w), _p(bias), _p(out), B, H, W, Cin1, Cin2, Cout,
+                             stride, int(bool(upsample)), C.c_void_p(addr), need, _stream())
     N.check(st, "nv_op_conv3x3")
     return out
-
 
 def nv_trace_enable(family_mask, max_launches=65536):
     N.check(N.lib.nv_trace_enable(family_mask, max_launches), "nv_trace_enable")

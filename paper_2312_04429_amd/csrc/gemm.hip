@@ -134,6 +134,91 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
   const __amdgpu_buffer_rsrc_t rsw = make_rsrc(g.w, (uint32_t)((int64_t)g.N * g.ldw * 2));
   // !DUAL: one source per 64-channel k tile (C1, and for convs Cin, multiples of 64)
   constexpr bool uni = !DUAL;
+  // Incremental addressing (one source and one tap per 64-deep k tile): the
+  // per-row byte offsets are recomputed only when the tile enters a new tap or
+  // source, and otherwise advance by 128 bytes; out-of-range rows carry an
+  // offset past the descriptor's range, which stays out of range.
+  int t_k0 = kt0 * BK;
+  int t_tap = 0, t_ci = 0;
+  bool t_first = true;
+  uint32_t aoff[A_CH], boff[B_CH];
+  auto a_offsets = [&]() {
+    if (MODE == 0) {
+      t_first = t_k0 < g.C1;
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        const bool ok = a_ok[i] && t_k0 < g.K;
+        aoff[i] = !ok ? OOB
+                : t_first ? (uint32_t)((a_m[i] * g.lda1 + t_k0 + cch * 8) * 2)
+                          : (uint32_t)((a_m[i] * g.lda2 + (t_k0 - g.C1) + cch * 8) * 2);
+      }
+    } else {
+      t_first = t_ci < g.C1;
+      const int ky = (t_tap * 11) >> 5, kx = t_tap - 3 * ((t_tap * 11) >> 5);
+      const int ld = t_first ? g.C1 : g.C2;
+      const int cs = (t_first ? t_ci : t_ci - g.C1) + cch * 8;
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        int iy, ix;
+        bool in;
+        if (g.upsample) {
+          const int uy = a_oy[i] + ky - 1, ux = a_ox[i] + kx - 1;
+          in = uy >= 0 && ux >= 0 && uy < 2 * g.Hin && ux < 2 * g.Win;
+          iy = uy >> 1;
+          ix = ux >> 1;
+        } else {
+          iy = a_oy[i] * g.stride + ky - 1;
+          ix = a_ox[i] * g.stride + kx - 1;
+          in = iy >= 0 && ix >= 0 && iy < g.Hin && ix < g.Win;
+        }
+        const bool ok = a_ok[i] && in && t_tap < 9;
+        const int64_t pix = ((int64_t)a_b[i] * g.Hin + iy) * g.Win + ix;
+        aoff[i] = ok ? (uint32_t)((pix * ld + cs) * 2) : OOB;
+      }
+    }
+  };
+  if (!DUAL) {
+    if (MODE == 1) {
+      t_tap = t_k0 / cin;
+      t_ci = t_k0 - t_tap * cin;
+    }
+    a_offsets();
+#pragma unroll
+    for (int i = 0; i < B_CH; ++i) {
+      const int n = n0 + rr + 32 * i;
+      boff[i] = (n < g.N) ? (uint32_t)(((int64_t)n * g.ldw + t_k0 + cch * 8) * 2) : OOB;
+    }
+  }
+  auto load_inc = [&](uint4 (&ra)[A_CH], uint4 (&rb)[B_CH]) {
+    const __amdgpu_buffer_rsrc_t rsa = t_first ? rs1 : rs2;
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i) ra[i] = bload(rsa, aoff[i]);
+#pragma unroll
+    for (int i = 0; i < B_CH; ++i) rb[i] = bload(rsw, boff[i]);
+    // advance to the next tile
+    t_k0 += BK;
+#pragma unroll
+    for (int i = 0; i < B_CH; ++i) boff[i] += 2 * BK;
+    bool fresh;
+    if (MODE == 0) {
+      fresh = t_k0 == g.C1 || t_k0 >= g.K;
+    } else {
+      t_ci += BK;
+      fresh = false;
+      if (t_ci >= cin) {
+        t_ci -= cin;
+        ++t_tap;
+        fresh = true;
+      }
+      if (t_ci == g.C1) fresh = true;
+    }
+    if (fresh) {
+      a_offsets();
+    } else {
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) aoff[i] += 2 * BK;
+    }
+  };
   auto load_tile = [&](int kt, uint4 (&ra)[A_CH], uint4 (&rb)[B_CH]) {
     const int k = kt * BK + cch * 8;
     const bool kok = k < g.K;
@@ -241,17 +326,23 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
   // the other; loads past the last tile re-read the last tile (never used).
   uint4 ra1[A_CH], rb1[B_CH];
   const int klast = max(kt0, kt1 - 1);
-  load_tile(kt0, ra0, rb0);
+  auto fetch = [&](int kt, uint4 (&ra)[A_CH], uint4 (&rb)[B_CH]) {
+    if (DUAL)
+      load_tile(kt, ra, rb);
+    else
+      load_inc(ra, rb);  // tiles arrive in order; fetches past the last tile are unused
+  };
+  fetch(kt0, ra0, rb0);
   store_tile(0, ra0, rb0);
-  load_tile(min(kt0 + 1, klast), ra1, rb1);
+  fetch(min(kt0 + 1, klast), ra1, rb1);
   __syncthreads();
   int kt = kt0;
   for (; kt + 1 < kt1; kt += 2) {
-    load_tile(min(kt + 2, klast), ra0, rb0);
+    fetch(min(kt + 2, klast), ra0, rb0);
     compute(0);
     store_tile(1, ra1, rb1);
     __syncthreads();
-    load_tile(min(kt + 3, klast), ra1, rb1);
+    fetch(min(kt + 3, klast), ra1, rb1);
     compute(1);
     store_tile(0, ra0, rb0);
     __syncthreads();
@@ -366,7 +457,10 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
 
 template <int MODE, int BM, int BN>
 hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
-  const bool dual = (g.C1 % BK) != 0 || (MODE == 1 && ((g.C1 + g.C2) % BK) != 0);
+  // the incremental single-source path needs every 64-deep tile inside one
+  // source and inside K: C1 and K (dense) or C1 and Cin (conv) multiples of 64
+  const bool dual = (g.C1 % BK) != 0 || (MODE == 0 && (g.K % BK) != 0) ||
+                    (MODE == 1 && ((g.C1 + g.C2) % BK) != 0);
   return dual ? launch_t<MODE, BM, BN, true>(g, splits, s)
               : launch_t<MODE, BM, BN, false>(g, splits, s);
 }
@@ -374,8 +468,10 @@ hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
 template <int MODE>
 hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
   // Larger tiles move fewer bytes per flop (64, 43 and 32 flop per byte of
-  // L2 traffic for 128x128, 128x64, 64x64); small problems fall back to
-  // 64x64 tiles with K split so that every CU has work.
+  // L2 traffic for 128x128, 128x64, 64x64).  At these problem sizes a
+  // workgroup is bound by load latency (about one wave per SIMD), so K is
+  // split until about two workgroups per CU are resident, keeping at least
+  // MIN_KT k tiles per split.
   constexpr int64_t MIN_WG = 128;
   constexpr int64_t TARGET = 512;
   const int nk = (g.K + BK - 1) / BK;
@@ -383,19 +479,17 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
   const int64_t t12864 = ceil_div(g.M, 128) * ceil_div(g.N, 64);
   const int64_t t64 = ceil_div(g.M, 64) * ceil_div(g.N, 64);
   const bool n_fits_128 = g.N % 128 == 0 || g.N > 512;
-  // mid-size problems: two K halves when the grid would leave CUs idle
-  auto halves = [&](int64_t tiles) {
-    return (tiles < 256 && nk >= 16 && g.partial &&
-            (size_t)2 * g.M * g.N * 4 <= g.partial_bytes) ? 2 : 1;
+  auto split_for = [&](int64_t tiles, int min_kt) {
+    int sp = 1;
+    if (!g.partial) return 1;
+    while (tiles * sp < TARGET && nk / (sp + 1) >= min_kt &&
+           (size_t)(sp + 1) * g.M * g.N * 4 <= g.partial_bytes)
+      ++sp;
+    return sp;
   };
-  if (t128 >= MIN_WG && n_fits_128) return launch<MODE, 128, 128>(g, halves(t128), s);
-  if (t12864 >= MIN_WG) return launch<MODE, 128, 64>(g, halves(t12864), s);
-  int splits = 1;
-  if (g.partial && t64 < TARGET) {
-    splits = (int)std::min<int64_t>(ceil_div(TARGET, t64), std::max(1, nk / 4));
-    while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.partial_bytes) --splits;
-  }
-  return launch<MODE, 64, 64>(g, splits, s);
+  if (t128 >= MIN_WG && n_fits_128) return launch<MODE, 128, 128>(g, split_for(t128, 8), s);
+  if (t12864 >= MIN_WG) return launch<MODE, 128, 64>(g, split_for(t12864, 8), s);
+  return launch<MODE, 64, 64>(g, split_for(t64, 4), s);
 }
 
 }  // namespace

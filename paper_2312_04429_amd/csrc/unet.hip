@@ -1191,19 +1191,29 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
 
 extern "C" size_t nv_op_workspace(void) { return SPLITK_BYTES; }
 
-extern "C" int32_t nv_op_linear(const void* x, const void* w, const float* bias,
-                                const void* residual, void* out, int64_t M, int32_t N, int32_t K,
-                                void* workspace, size_t workspace_bytes, void* stream) {
+extern "C" int32_t nv_op_linear(const void* x, const void* x2, const void* w, const float* bias,
+                                const void* residual, void* out, int64_t M, int32_t N, int32_t K1,
+                                int32_t K2, void* workspace, size_t workspace_bytes,
+                                void* stream) {
   clear_error();
   NV_CHECK_ARG(x && w && out, "null pointer argument");
-  NV_CHECK_ARG(M >= 1 && N >= 1 && K >= 8 && K % 8 == 0, "need M, N >= 1 and K % 8 == 0");
+  NV_CHECK_ARG(M >= 1 && N >= 1 && K1 >= 8 && K1 % 8 == 0 && K2 >= 0 && K2 % 8 == 0,
+               "need M, N >= 1, K1 >= 8 and K1, K2 multiples of 8");
+  NV_CHECK_ARG((K2 == 0) == (x2 == nullptr), "x2 must be given exactly when K2 > 0");
   if (!workspace || workspace_bytes < SPLITK_BYTES || ((uintptr_t)workspace & 255)) {
     set_error("op workspace missing, misaligned or smaller than nv_op_workspace()");
     return NV_ERR_WORKSPACE;
   }
-  GemmArgs g = dense_args(N, K, (const _Float16*)w, bias);
+  GemmArgs g = dense_args(N, K1 + K2, (const _Float16*)w, bias);
   g.M = M;
   g.src1 = (const _Float16*)x;
+  g.C1 = K1;
+  g.lda1 = K1;
+  if (x2) {
+    g.src2 = (const _Float16*)x2;
+    g.C2 = K2;
+    g.lda2 = K2;
+  }
   if (residual) {
     g.residual = (const _Float16*)residual;
     g.ld_res = N;
@@ -1216,14 +1226,16 @@ extern "C" int32_t nv_op_linear(const void* x, const void* w, const float* bias,
   return NV_OK;
 }
 
-extern "C" int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias, void* out,
-                                 int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Cout,
-                                 int32_t stride, int32_t upsample, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
+extern "C" int32_t nv_op_conv3x3(const void* x, const void* x2, const void* w, const float* bias,
+                                 void* out, int32_t B, int32_t H, int32_t W, int32_t Cin1,
+                                 int32_t Cin2, int32_t Cout, int32_t stride, int32_t upsample,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
   clear_error();
   NV_CHECK_ARG(x && w && out, "null pointer argument");
-  NV_CHECK_ARG(B >= 1 && H >= 1 && W >= 1 && Cout >= 1 && Cin >= 8 && Cin % 8 == 0,
-               "bad conv shape (Cin % 8 == 0 required)");
+  NV_CHECK_ARG(B >= 1 && H >= 1 && W >= 1 && Cout >= 1 && Cin1 >= 8 && Cin1 % 8 == 0 &&
+                   Cin2 >= 0 && Cin2 % 8 == 0,
+               "bad conv shape (Cin1, Cin2 multiples of 8)");
+  NV_CHECK_ARG((Cin2 == 0) == (x2 == nullptr), "x2 must be given exactly when Cin2 > 0");
   NV_CHECK_ARG(stride == 1 || (stride == 2 && H % 2 == 0 && W % 2 == 0 && !upsample),
                "stride must be 1, or 2 with even H, W and no upsample");
   if (!workspace || workspace_bytes < SPLITK_BYTES || ((uintptr_t)workspace & 255)) {
@@ -1234,9 +1246,11 @@ extern "C" int32_t nv_op_conv3x3(const void* x, const void* w, const float* bias
   GemmArgs g{};
   g.M = (int64_t)B * Ho * Wo;
   g.N = Cout;
-  g.K = 9 * Cin;
+  g.K = 9 * (Cin1 + Cin2);
   g.src1 = (const _Float16*)x;
-  g.C1 = Cin;
+  g.C1 = Cin1;
+  g.src2 = (const _Float16*)x2;
+  g.C2 = Cin2;
   g.conv = 1;
   g.Hin = H;
   g.Win = W;

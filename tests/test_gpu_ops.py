@@ -52,3 +52,42 @@ def test_conv3x3(B, H, W, Cin, Cout, stride, up):
             xi = U.upsample_nearest2(xi)
         ref = U.conv3x3(xi, w.astype(np.float32), b, stride).transpose(1, 2, 0)
         np.testing.assert_allclose(got[bi], ref, rtol=2e-3, atol=2e-3 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("M,C1,C2,N", [(200, 64, 32, 48), (130, 64, 64, 64), (77, 32, 96, 40),
+                                       (8192, 1280, 640, 640), (512, 1280, 1280, 1280)])
+def test_linear_two_sources(M, C1, C2, N):
+    """Channel-concatenated A operand (the 1x1 skip projection of up-path ResBlocks)."""
+    import paper_2312_04429_amd as P
+    print(f"op linear concat M={M} C1={C1} C2={C2} N={N}", flush=True)
+    rng = np.random.default_rng(M + C1 + C2)
+    x1 = _h(rng.standard_normal((M, C1)))
+    x2 = _h(rng.standard_normal((M, C2)))
+    w = _h(rng.standard_normal((N, C1 + C2)) * 0.05)
+    r = _h(rng.standard_normal((M, N)))
+    t = lambda a: torch.from_numpy(a).cuda()
+    ref = U.linear(np.concatenate([x1, x2], 1).astype(np.float32), w.astype(np.float32)) + \
+        r.astype(np.float32)
+    got = P.nv_op_linear(t(x1), t(w), residual=t(r), x2=t(x2)).float().cpu().numpy()
+    np.testing.assert_allclose(got, ref, rtol=2e-3, atol=2e-3 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("B,H,C1,C2,Cout,up", [(2, 8, 64, 32, 64, 0), (1, 16, 32, 64, 32, 0),
+                                               (2, 8, 128, 64, 64, 1), (2, 16, 640, 320, 320, 0)])
+def test_conv3x3_two_sources(B, H, C1, C2, Cout, up):
+    import paper_2312_04429_amd as P
+    print(f"op conv concat B={B} H={H} {C1}+{C2}->{Cout} up{up}", flush=True)
+    rng = np.random.default_rng(H + C1 + C2)
+    x1 = _h(rng.standard_normal((B, H, H, C1)))
+    x2 = _h(rng.standard_normal((B, H, H, C2)))
+    w = _h(rng.standard_normal((Cout, C1 + C2, 3, 3)) * (1.0 / np.sqrt(9 * (C1 + C2))))
+    b = rng.standard_normal(Cout).astype(np.float32)
+    wk = np.ascontiguousarray(w.transpose(0, 2, 3, 1))
+    t = lambda a: torch.from_numpy(a).cuda()
+    got = P.nv_op_conv3x3(t(x1), t(wk), t(b), upsample=bool(up), x2=t(x2)).float().cpu().numpy()
+    for bi in range(B):
+        xi = np.concatenate([x1[bi], x2[bi]], 2).astype(np.float32).transpose(2, 0, 1)
+        if up:
+            xi = U.upsample_nearest2(xi)
+        ref = U.conv3x3(xi, w.astype(np.float32), b, 1).transpose(1, 2, 0)
+        np.testing.assert_allclose(got[bi], ref, rtol=2e-3, atol=2e-3 * np.abs(ref).max())
