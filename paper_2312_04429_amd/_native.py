@@ -8,7 +8,7 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libnv.so")
+LIB_PATH = os.environ.get("NV_LIB_PATH") or os.path.join(HERE, "libnv.so")
 
 NV_OK, NV_ERR_INVALID_ARG, NV_ERR_UNSUPPORTED = 0, -1, -2
 NV_ERR_OUT_OF_MEMORY, NV_ERR_HIP, NV_ERR_WORKSPACE = -3, -4, -5

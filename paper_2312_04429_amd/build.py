@@ -9,9 +9,9 @@ import sys
 from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(HERE, "csrc")
-OUT_DIR = os.path.join(HERE, "_build")
-LIB = os.path.join(HERE, "libnv.so")
+SRC = os.environ.get("NV_BUILD_SRC") or os.path.join(HERE, "csrc")
+OUT_DIR = os.environ.get("NV_BUILD_DIR") or os.path.join(HERE, "_build")
+LIB = os.environ.get("NV_BUILD_OUT") or os.path.join(HERE, "libnv.so")
 SOURCES = ["lookup.hip", "gemm.hip", "attention.hip", "ops.hip", "unet.hip", "trace.hip"]
 ARCH = os.environ.get("NV_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

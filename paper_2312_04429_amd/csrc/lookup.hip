@@ -8,9 +8,10 @@
 //      |s~ - s64| <= |c_i| * E_q, with E_q = |q - bf16(q)| + (2 d 2^-24 +
 //      d 2^-52) |q~| (Cauchy-Schwarz on the rounding of q plus the worst-case
 //      accumulation error of any summation order, plus the float64 canonical
-//      sum's own error).  Per 256-row tile the kernel keeps the best lower
-//      bound L_t, the best upper bound U_t and the rows whose upper bound
-//      reaches L_t (at most CAP; more sets an overflow count).
+//      sum's own error).  Per tile (128 rows for bf16 with d <= 768, else
+//      256) the kernel keeps the best lower bound L_t, the best upper bound
+//      U_t and the rows whose upper bound reaches L_t (at most CAP, in row
+//      order; more sets an overflow count).
 //   2. select: per query, L = max_t L_t; every row whose upper bound can reach
 //      L lives in a tile with U_t >= L and is listed there (or the tile
 //      overflowed and is rescanned whole).  Those rows are rescored with the
@@ -25,7 +26,7 @@
 namespace nv {
 namespace {
 
-constexpr int TILE = 256;    // cache rows per scan workgroup
+constexpr int TILE = 256;    // cache rows per workgroup of the f32 and wide-d bf16 scans
 constexpr int QB = 16;       // queries per matrix-core column block
 constexpr int CAP = 16;      // listed candidates per (query, tile)
 constexpr int OVF_CAP = 512; // overflowed tiles handled per select pass
@@ -106,102 +107,268 @@ __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int 
   }
 }
 
-// Shared tail of both scans: scores sS[q][r] and row norms sN[r] are in LDS.
+// Shared tail of the scans: the block's scores sS[q][r] (row stride TR + TPQ)
+// and row norms sN[r] are in LDS; Eq is the margin factor of the calling
+// thread's query (threadIdx.x / (NT / QB)).  NT / QB consecutive threads own one query;
+// each covers TR / (NT / QB) rows of the tile, forms their bounds, and the
+// group maxima come from lane shuffles.  Rows whose upper bound reaches the
+// group's best lower bound are listed in row order through a wave ballot, so
+// the list is deterministic.  No barrier inside: the scans double-buffer sS
+// and sN.
+template <int NT, int TR>
 __device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_t n, int q0,
-                              int qcount, int T, const double* __restrict__ E, double* red,
-                              int* scnt, LookupWs ws) {
-  const int r = threadIdx.x;
-  const int64_t row = (int64_t)tile * TILE + r;
-  const bool valid = row < n;
-  if (r < QB) scnt[r] = 0;
-  for (int q = 0; q < qcount; ++q) {
-    const int qg = q0 + q;
-    const double s = (double)sS[q * TILE + r];
-    const double dd = (double)sN[r] * E[qg];
-    const double lo = valid ? s - dd : -INFINITY;
-    const double up = valid ? s + dd : -INFINITY;
-    const double L = block_max_256(lo, red);
-    const double U = block_max_256(up, red + 4);
-    if (valid && up >= L) {
-      int pos = atomicAdd(&scnt[q], 1);
-      if (pos < CAP) ws.cand[((int64_t)qg * T + tile) * CAP + pos] = (int32_t)row;
-    }
-    if (r == 0) {
-      ws.tileL[(int64_t)qg * T + tile] = L;
-      ws.tileU[(int64_t)qg * T + tile] = U;
+                              int qcount, int T, double Eq, LookupWs ws) {
+  constexpr int TPQ = NT / QB, RPT = TR / TPQ, SS = TR + TPQ;
+  static_assert(TPQ <= 64 && (TPQ & (TPQ - 1)) == 0 && TR % TPQ == 0, "group shape");
+  const int t = threadIdx.x, q = t / TPQ, sub = t % TPQ, lane = t & 63;
+  const int64_t row0 = (int64_t)tile * TR;
+  const bool act = q < qcount;
+  const float* sq = sS + q * SS;
+  double L = -INFINITY, U = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const int r = sub + j * TPQ;
+    if (act && row0 + r < n) {
+      const double sc = (double)sq[r], dd = (double)sN[r] * Eq;
+      L = fmax(L, sc - dd);
+      U = fmax(U, sc + dd);
     }
   }
-  __syncthreads();
-  if (r < qcount) ws.cnt[(int64_t)(q0 + r) * T + tile] = scnt[r];
+#pragma unroll
+  for (int o = TPQ / 2; o > 0; o >>= 1) {
+    L = fmax(L, __shfl_xor(L, o, 64));
+    U = fmax(U, __shfl_xor(U, o, 64));
+  }
+  const int gbase = lane & ~(TPQ - 1);
+  const uint64_t gmask = (TPQ == 64 ? ~0ull : ((1ull << (TPQ & 63)) - 1)) << gbase;
+  const uint64_t below = (1ull << lane) - 1;
+  int32_t* list = ws.cand + ((int64_t)(q0 + q) * T + tile) * CAP;
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const int r = sub + j * TPQ;
+    bool p = false;
+    if (act && row0 + r < n) {
+      const double sc = (double)sq[r], dd = (double)sN[r] * Eq;
+      p = sc + dd >= L;
+    }
+    const uint64_t bal = __ballot(p);
+    if (p) {
+      const int pos = cnt + __popcll(bal & gmask & below);
+      if (pos < CAP) list[pos] = (int32_t)(row0 + r);
+    }
+    cnt += __popcll(bal & gmask);
+  }
+  if (act && sub == 0) {
+    ws.tileL[(int64_t)(q0 + q) * T + tile] = L;
+    ws.tileU[(int64_t)(q0 + q) * T + tile] = U;
+    ws.cnt[(int64_t)(q0 + q) * T + tile] = cnt;
+  }
 }
 
-// bf16 cache: 4 waves x 64 rows; each wave runs 4 row blocks of 16 through
-// v_mfma_f32_16x16x32_bf16 with the 16-query block as the B operand.
-// Operand layout (16x16x32): lane l feeds row/column (l % 16) with the 8
-// consecutive k of chunk (l / 16); result lane l, register r holds
-// D[4 (l / 16) + r][l % 16].
-__global__ void __launch_bounds__(256) lk_scan_bf16(const uint16_t* __restrict__ cache, int64_t n,
+constexpr uint32_t OOB = 0x80000000u;  // offset past the tile descriptor's range
+constexpr int KS = 24;                 // 32-element k steps per register chunk (768 elements)
+constexpr int SS_WIDE = TILE + 16;    // score row stride, 256 threads x 256 rows
+constexpr int RR_TILE = 128;           // cache rows per many-query workgroup
+constexpr int SS_RR = RR_TILE + 16;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// Stage one 16-query block of bf16 queries into LDS.
+__device__ inline void stage_queries(uint16_t* sQ, const uint16_t* __restrict__ qbf, int q0, int d) {
+  for (int i = threadIdx.x; i < QB * d / 8; i += blockDim.x)
+    ((uint4*)sQ)[i] = ((const uint4*)(qbf + (int64_t)q0 * d))[i];
+}
+
+// Margin factor of this thread's query in the 16-query block at q0 (threads
+// NT / QB apart share a query), 0 past m.
+template <int NT>
+__device__ inline double query_margin(const double* __restrict__ E, int q0, int m) {
+  const int q = q0 + (int)threadIdx.x / (NT / QB);
+  return q < m ? E[q] : 0.0;
+}
+
+// bf16 cache with d > 768: 4 waves x 64 rows per 256-row tile; each wave runs
+// its 4 row blocks of 16 through v_mfma_f32_16x16x32_bf16 with the 16-query
+// block as the B operand, k in register chunks of 768 requested one chunk
+// ahead of the one being multiplied.  Operand layout (16x16x32): lane l feeds
+// row/column (l % 16) with the 8 consecutive k of chunk (l / 16); result lane
+// l, register r holds D[4 (l / 16) + r][l % 16].  Loads go through a
+// range-checked descriptor of the tile (rows past n read zero).
+__global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restrict__ cache, int64_t n,
                                                     int d, int m, int T, LookupWs ws) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint16_t* sQ = (uint16_t*)smem;                       // [QB][d]
-  float* sS = (float*)(smem + QB * d * 2);              // [QB][TILE]
-  float* sN = sS + QB * TILE;                           // [TILE]
-  double* red = (double*)(sN + TILE);                   // [8]
-  int* scnt = (int*)(red + 8);                          // [QB]
+  float* sS = (float*)(smem + QB * d * 2);              // [2][QB][SS_WIDE]
+  float* sN = sS + 2 * QB * SS_WIDE;                   // [TILE]
   const int tile = blockIdx.x;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int li = lane & 15;
-  const int kc = lane >> 4;
-  const int ksteps = (d + 31) / 32;
-  bool first = true;  // row norms are computed during the first query block
-  for (int q0 = 0; q0 < m; q0 += QB) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, kc = lane >> 4;
+  const int64_t row0 = (int64_t)tile * TILE;
+  const int rows = (int)min((int64_t)TILE, n - row0);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(cache + row0 * d, (uint32_t)rows * d * 2);
+  const int nchunk = (d + 32 * KS - 1) / (32 * KS);  // register chunks per row block
+  const int steps = 4 * nchunk;                       // (block, chunk) steps of this wave
+  auto fetch = [&](int st, u32x4(&a)[KS]) {
+    const int blk = st / nchunk, ch = st % nchunk;
+    const int rloc = wave * 64 + blk * 16 + li;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int k = ch * 32 * KS + j * 32 + kc * 8;
+      const uint32_t off = (rloc < rows && k < d) ? (uint32_t)((rloc * d + k) * 2) : OOB;
+      a[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    }
+  };
+  for (int q0 = 0, par = 0; q0 < m; q0 += QB, par ^= 1) {
+    const double Eq = query_margin<256>(ws.E, q0, m);
+    __syncthreads();  // every wave is past the previous block's multiplies
+    stage_queries(sQ, ws.qbf, q0, d);
     __syncthreads();
-    for (int i = threadIdx.x; i < QB * d / 8; i += 256)
-      ((uint4*)sQ)[i] = ((const uint4*)(ws.qbf + (int64_t)q0 * d))[i];
-    __syncthreads();
-    for (int blk = 0; blk < 4; ++blk) {
-      const int rloc = wave * 64 + blk * 16 + li;
-      const int64_t row = (int64_t)tile * TILE + rloc;
-      const bool rv = row < n;
-      const uint16_t* crow = cache + (rv ? row : 0) * (int64_t)d;
-      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-      float nn = 0.f;
-#pragma unroll 4
-      for (int ks = 0; ks < ksteps; ++ks) {
-        const int k = ks * 32 + kc * 8;
-        uint4 a = make_uint4(0, 0, 0, 0);
+    const bool norms = q0 == 0;  // row norms during the first query block
+    float* S = sS + par * QB * SS_WIDE;
+    u32x4 a0[KS], a1[KS];
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    float nn = 0.f;
+    auto consume = [&](int st, const u32x4(&a)[KS]) {
+      const int blk = st / nchunk, ch = st % nchunk;
+#pragma unroll
+      for (int j = 0; j < KS; ++j) {
+        const int k = ch * 32 * KS + j * 32 + kc * 8;
         uint4 b = make_uint4(0, 0, 0, 0);
-        if (k < d) {
-          if (rv) {
-            const u32x4 t = __builtin_nontemporal_load((const u32x4*)(crow + k));
-            a = make_uint4(t[0], t[1], t[2], t[3]);
-          }
-          b = *(const uint4*)(sQ + li * d + k);
-        }
-        if (first) {
-          const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+        if (k < d) b = *(const uint4*)(sQ + li * d + k);
+        if (norms) {
+          const u32x4 w = a[j];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            float lo = __uint_as_float(w[e] << 16), hi = __uint_as_float(w[e] & 0xFFFF0000u);
-            nn = fmaf(lo, lo, nn);
-            nn = fmaf(hi, hi, nn);
+            const bf16x2 v = __builtin_bit_cast(bf16x2, w[e]);
+            nn = __builtin_amdgcn_fdot2_f32_bf16(v, v, nn, false);
           }
         }
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8*)&a, *(bf16x8*)&b, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j], *(bf16x8*)&b, acc, 0, 0,
+                                                      0);
       }
-      if (first) {
-        nn += __shfl_xor(nn, 16, 64);
-        nn += __shfl_xor(nn, 32, 64);
-        if (kc == 0) sN[rloc] = sqrtf(nn * 1.001f);
-      }
+      if (ch == nchunk - 1) {  // block complete
+        const int rb = wave * 64 + blk * 16;
+        if (norms) {
+          nn += __shfl_xor(nn, 16, 64);
+          nn += __shfl_xor(nn, 32, 64);
+          if (kc == 0) sN[rb + li] = sqrtf(nn * 1.001f);
+        }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sS[li * TILE + wave * 64 + blk * 16 + kc * 4 + r] = acc[r];
+        for (int r = 0; r < 4; ++r) S[li * SS_WIDE + rb + kc * 4 + r] = acc[r];
+        acc = floatx4{0.f, 0.f, 0.f, 0.f};
+        nn = 0.f;
+      }
+    };
+    fetch(0, a0);
+    for (int st = 0; st < steps; st += 2) {
+      fetch(st + 1, a1);
+      consume(st, a0);
+      if (st + 2 < steps) fetch(st + 2, a0);
+      consume(st + 1, a1);
     }
-    first = false;
     __syncthreads();
-    const int qcount = min(QB, m - q0);
-    tile_finalize(sS, sN, tile, n, q0, qcount, T, ws.E, red, scnt, ws);
+    tile_finalize<256, TILE>(S, sN, tile, n, q0, min(QB, m - q0), T, Eq, ws);
+  }
+}
+
+// bf16 cache with d <= 768, any m: 4 waves, each holding its 32
+// cache rows (two 16-row blocks, the whole k range) in registers for the
+// entire query range, so the cache is read from HBM once; 16-query blocks
+// stream through a double-buffered LDS and each query fragment read feeds both
+// row blocks.  128-row tiles let two workgroups share a CU, so one loads while
+// the other multiplies.
+__global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restrict__ cache,
+                                                          int64_t n, int d, int m, int T,
+                                                          LookupWs ws) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint16_t* sQ = (uint16_t*)smem;                       // [2][QB][d]
+  float* sS = (float*)(smem + 2 * QB * d * 2);          // [2][QB][SS_RR]
+  float* sN = sS + 2 * QB * SS_RR;                      // [RR_TILE]
+  const int tile = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 15, kc = lane >> 4;
+  const int64_t row0 = (int64_t)tile * RR_TILE;
+  const int rows = (int)min((int64_t)RR_TILE, n - row0);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(cache + row0 * d, (uint32_t)rows * d * 2);
+  u32x4 a[KS][2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int rloc = wave * 32 + b * 16 + li;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int k = j * 32 + kc * 8;
+      const uint32_t off = (rloc < rows && k < d) ? (uint32_t)((rloc * d + k) * 2) : OOB;
+      a[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    }
+  }
+  // next query block travels through registers: QB * d / 8 chunks of 16 bytes
+  const int nqc = QB * d / 8;
+  constexpr int QPT = (QB * 32 * KS / 8 + 255) / 256;
+  uint4 qr[QPT];
+  auto qfetch = [&](int q0) {
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+      const int c = tid + i * 256;
+      if (c < nqc) qr[i] = ((const uint4*)(ws.qbf + (int64_t)q0 * d))[c];
+    }
+  };
+  auto qstash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+      const int c = tid + i * 256;
+      if (c < nqc) ((uint4*)(sQ + buf * QB * d))[c] = qr[i];
+    }
+  };
+  stage_queries(sQ, ws.qbf, 0, d);
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    float nn = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 v = __builtin_bit_cast(bf16x2, a[j][b][e]);
+        nn = __builtin_amdgcn_fdot2_f32_bf16(v, v, nn, false);
+      }
+    nn += __shfl_xor(nn, 16, 64);
+    nn += __shfl_xor(nn, 32, 64);
+    if (kc == 0) sN[wave * 32 + b * 16 + li] = sqrtf(nn * 1.001f);
+  }
+  // Query block i + 1 (registers) and the margin factors of block i + 1 are
+  // requested a whole block ahead: after the barrier of block i - 1.
+  if (QB < m) qfetch(QB);
+  double Ecur = query_margin<256>(ws.E, 0, m), Enext = query_margin<256>(ws.E, QB, m);
+  __syncthreads();
+  for (int q0 = 0, i = 0; q0 < m; q0 += QB, ++i) {
+    const uint16_t* Q = sQ + (i & 1) * QB * d;
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int k = j * 32 + kc * 8;
+      uint4 qv = make_uint4(0, 0, 0, 0);
+      if (k < d) qv = *(const uint4*)(Q + li * d + k);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(bf16x8*)&qv, acc0,
+                                                     0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(bf16x8*)&qv, acc1,
+                                                     0, 0, 0);
+    }
+    float* S = sS + (i & 1) * QB * SS_RR;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      S[li * SS_RR + wave * 32 + kc * 4 + r] = acc0[r];
+      S[li * SS_RR + wave * 32 + 16 + kc * 4 + r] = acc1[r];
+    }
+    // block i + 1 -> the other LDS buffer, last read by block i - 1's multiplies
+    if (q0 + QB < m) qstash((i + 1) & 1);
+    __syncthreads();
+    if (q0 + 2 * QB < m) qfetch(q0 + 2 * QB);
+    const double Eq = Ecur;
+    Ecur = Enext;
+    Enext = query_margin<256>(ws.E, q0 + 2 * QB, m);
+    tile_finalize<256, RR_TILE>(S, sN, tile, n, q0, min(QB, m - q0), T, Eq, ws);
   }
 }
 
@@ -210,10 +377,8 @@ __global__ void __launch_bounds__(256) lk_scan_f32(const float* __restrict__ cac
                                                    int d, const float* __restrict__ queries, int m,
                                                    int T, LookupWs ws) {
   __shared__ float sQ[QB * 256];
-  __shared__ float sS[QB * TILE];
+  __shared__ float sS[2][QB * SS_WIDE];
   __shared__ float sN[TILE];
-  __shared__ double red[8];
-  __shared__ int scnt[QB];
   const int tile = blockIdx.x;
   const int r = threadIdx.x;
   const int64_t row = (int64_t)tile * TILE + r;
@@ -240,11 +405,12 @@ __global__ void __launch_bounds__(256) lk_scan_f32(const float* __restrict__ cac
         for (int q = 0; q < QB; ++q) acc[q] = fmaf(sQ[q * 256 + k], c, acc[q]);
       }
     }
+    float* S = sS[(q0 / QB) & 1];
 #pragma unroll
-    for (int q = 0; q < QB; ++q) sS[q * TILE + r] = acc[q];
-    sN[r] = sqrtf(nn * 1.001f);
+    for (int q = 0; q < QB; ++q) S[q * SS_WIDE + r] = acc[q];
+    if (q0 == 0) sN[r] = sqrtf(nn * 1.001f);
     __syncthreads();
-    tile_finalize(sS, sN, tile, n, q0, qcount, T, ws.E, red, scnt, ws);
+    tile_finalize<256, TILE>(S, sN, tile, n, q0, qcount, T, query_margin<256>(ws.E, q0, m), ws);
   }
 }
 
@@ -277,7 +443,8 @@ __device__ inline void better(double& bs, int64_t& bi, double s, int64_t i) {
 
 __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queries, int d,
                                                  const void* __restrict__ cache, int cache_bf16,
-                                                 int64_t n, int T, Thresholds th, LookupWs ws,
+                                                 int64_t n, int T, int tr, Thresholds th,
+                                                 LookupWs ws,
                                                  int64_t* __restrict__ idx_out,
                                                  float* __restrict__ sim_out,
                                                  int32_t* __restrict__ k_out) {
@@ -323,8 +490,8 @@ __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queri
     }
   } else {
     for (int o = 0; o < no; ++o) {
-      const int64_t row = (int64_t)ovf[o] * TILE + threadIdx.x;
-      if (row < n) {
+      const int64_t row = (int64_t)ovf[o] * tr + threadIdx.x;
+      if ((int)threadIdx.x < tr && row < n) {
         const double s = cache_bf16
                              ? canon_bf16(qd, (const uint16_t*)cache + row * (int64_t)d, d)
                              : canon_f32(qd, (const float*)cache + row * (int64_t)d, d);
@@ -370,9 +537,12 @@ struct WsPlan {
   size_t off_qbf, off_E, off_L, off_U, off_cnt, off_cand, total;
 };
 
-WsPlan plan_ws(int32_t m, int64_t n, int32_t d) {
+// bf16 scans with d <= 768 (register-resident rows) use 128-row tiles, the rest 256.
+inline bool rows_in_registers(int32_t m, int32_t d, bool bf16) { return bf16 && d <= 32 * KS; }
+
+WsPlan plan_ws(int32_t m, int64_t n, int32_t d, int tr) {
   WsPlan p{};
-  const int64_t T = ceil_div(n, TILE);
+  const int64_t T = ceil_div(n, (int64_t)tr);
   const int64_t mq = ceil_div(m, QB) * QB;
   size_t o = 0;
   p.off_qbf = o;  o = align_up(o + (size_t)mq * d * 2, 256);
@@ -392,7 +562,8 @@ using namespace nv;
 
 extern "C" size_t nv_cache_lookup_workspace(int32_t m, int64_t n, int32_t d) {
   if (m <= 0 || n < 0 || d <= 0) return 0;
-  return plan_ws(m, n, d).total;
+  const size_t small = plan_ws(m, n, d, TILE).total;
+  return rows_in_registers(m, d, true) ? std::max(small, plan_ws(m, n, d, RR_TILE).total) : small;
 }
 
 extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache,
@@ -422,7 +593,10 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
     set_error("d must be a multiple of 8 and at most 2048");
     return NV_ERR_UNSUPPORTED;
   }
-  const WsPlan p = plan_ws(m, n, d);
+  const int bf = c_dtype == NV_BF16;
+  const bool rr = rows_in_registers(m, d, bf);
+  const int tr = rr ? RR_TILE : TILE;
+  const WsPlan p = plan_ws(m, n, d, tr);
   if (!workspace || workspace_bytes < p.total || ((uintptr_t)workspace & 255)) {
     set_error("lookup workspace missing, misaligned or smaller than nv_cache_lookup_workspace()");
     return NV_ERR_WORKSPACE;
@@ -431,22 +605,30 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
   char* w = (char*)workspace;
   LookupWs ws{(uint16_t*)(w + p.off_qbf), (double*)(w + p.off_E),  (double*)(w + p.off_L),
               (double*)(w + p.off_U),     (int32_t*)(w + p.off_cnt), (int32_t*)(w + p.off_cand)};
-  const int T = (int)ceil_div(n, TILE);
-  const int mq = (int)ceil_div(m, QB) * QB;
-  const int bf = c_dtype == NV_BF16;
-  hipLaunchKernelGGL(lk_prep, dim3(mq), dim3(256), 0, s, queries, m, mq, d, bf, ws.qbf, ws.E);
+  const int T = (int)ceil_div(n, (int64_t)tr);
+  const int mq_pad = (int)ceil_div(m, QB) * QB;
+  hipLaunchKernelGGL(lk_prep, dim3(mq_pad), dim3(256), 0, s, queries, m, mq_pad, d, bf, ws.qbf,
+                     ws.E);
   NV_LAUNCH_CHECK("lk_prep");
   if (T > 0) {
-    if (bf) {
-      const size_t lds = (size_t)QB * d * 2 + (size_t)QB * TILE * 4 + TILE * 4 + 8 * 8 + QB * 4;
-      if (lds > 65536)
-        NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    if (rr) {
+      const size_t lds = (size_t)2 * QB * d * 2 + (size_t)2 * QB * SS_RR * 4 + RR_TILE * 4;
+      NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
       trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
       hipLaunchKernelGGL(lk_scan_bf16, dim3(T), dim3(256), lds, s, (const uint16_t*)cache, n, d,
                          m, T, ws);
       trace_post(NV_FAM_SCAN, s);
       NV_LAUNCH_CHECK("lk_scan_bf16");
+    } else if (bf) {
+      const size_t lds = (size_t)QB * d * 2 + (size_t)2 * QB * SS_WIDE * 4 + TILE * 4;
+      NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16_wide,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
+      hipLaunchKernelGGL(lk_scan_bf16_wide, dim3(T), dim3(256), lds, s, (const uint16_t*)cache, n, d, m,
+                         T, ws);
+      trace_post(NV_FAM_SCAN, s);
+      NV_LAUNCH_CHECK("lk_scan_bf16_wide");
     } else {
       trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 4.0 * (double)n * d, s);
       hipLaunchKernelGGL(lk_scan_f32, dim3(T), dim3(256), 0, s, (const float*)cache, n, d,
@@ -455,7 +637,7 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
       NV_LAUNCH_CHECK("lk_scan_f32");
     }
   }
-  hipLaunchKernelGGL(lk_select, dim3(m), dim3(256), 0, s, queries, d, cache, bf, n, T, th, ws,
+  hipLaunchKernelGGL(lk_select, dim3(m), dim3(256), 0, s, queries, d, cache, bf, n, T, tr, th, ws,
                      idx_out, sim_out, k_out);
   NV_LAUNCH_CHECK("lk_select");
   return NV_OK;

@@ -268,33 +268,44 @@ __global__ void temb_sin_k(StepArgs st, const int32_t* __restrict__ ts, int C0, 
 }
 
 // conv_in in float32 from the float32 latent x [samples][Cin][H][W]; output
-// [rows][H*W][C0] float16, rows 2b and 2b+1 read sample b.
+// [rows][H*W][C0] float16, rows 2b and 2b+1 read sample b.  One workgroup per
+// 64 output pixels of a row: the 3x3xCin input patch of each pixel is gathered
+// once into registers and the weights sit in LDS.
+template <int CIN>
 __global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
                                                  const float* __restrict__ w,
-                                                 const float* __restrict__ bias, int Cin, int H,
+                                                 const float* __restrict__ bias, int Cin_rt, int H,
                                                  int W, int C0, int rows,
                                                  _Float16* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = (int64_t)rows * H * W * C0;
-  if (i >= total) return;
-  const int co = (int)(i % C0);
-  const int64_t pix = i / C0;
-  const int r = (int)(pix / (H * W));
-  const int p = (int)(pix % (H * W));
+  const int Cin = CIN > 0 ? CIN : Cin_rt;  // CIN > 0: patch stays in registers
+  extern __shared__ float sw[];  // [C0][Cin*9] weights then [C0] bias
+  const int nk = Cin * 9;
+  for (int i = threadIdx.x; i < C0 * nk; i += 256) sw[i] = w[i];
+  for (int i = threadIdx.x; i < C0; i += 256) sw[C0 * nk + i] = bias[i];
+  __syncthreads();
+  const int HW = H * W;
+  const int pblocks = (HW + 63) / 64;
+  const int r = blockIdx.x / pblocks;
+  const int p = (blockIdx.x % pblocks) * 64 + (threadIdx.x & 63);
+  if (r >= rows || p >= HW) return;
   const int y = p / W, xx = p % W;
-  const float* xs = x + (int64_t)(r >> 1) * Cin * H * W;
-  float acc = bias[co];
+  const float* xs = x + (int64_t)(r >> 1) * Cin * HW;
+  float patch[(CIN > 0 ? CIN : 16) * 9];
+#pragma unroll
   for (int ci = 0; ci < Cin; ++ci)
-    for (int ky = 0; ky < 3; ++ky) {
-      const int iy = y + ky - 1;
-      if (iy < 0 || iy >= H) continue;
-      for (int kx = 0; kx < 3; ++kx) {
-        const int ix = xx + kx - 1;
-        if (ix < 0 || ix >= W) continue;
-        acc = fmaf(w[((co * Cin + ci) * 3 + ky) * 3 + kx], xs[((int64_t)ci * H + iy) * W + ix], acc);
-      }
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int iy = y + t / 3 - 1, ix = xx + t % 3 - 1;
+      patch[ci * 9 + t] = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? xs[(int64_t)ci * HW + iy * W + ix] : 0.f;
     }
-  out[i] = (_Float16)acc;
+  // the 4 waves split the output channels
+  for (int co = threadIdx.x >> 6; co < C0; co += 4) {
+    const float* wr = sw + co * nk;
+    float acc = sw[C0 * nk + co];
+#pragma unroll
+    for (int k = 0; k < nk; ++k) acc = fmaf(wr[k], patch[k], acc);
+    out[((int64_t)r * HW + p) * C0 + co] = (_Float16)acc;
+  }
 }
 
 // eps = eps_u + s (eps_c - eps_u); x <- sqrt(a_p) (x - sqrt(1-a_t) eps)/sqrt(a_t) + sqrt(1-a_p) eps
@@ -394,9 +405,27 @@ hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int ro
 
 hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Cin, int H, int W,
                           int C0, int rows, _Float16* out, hipStream_t s) {
-  const int64_t total = (int64_t)rows * H * W * C0;
-  hipLaunchKernelGGL(conv_in_k, dim3(blocks_for(total)), dim3(256), 0, s, x, w, b, Cin, H, W, C0,
-                     rows, out);
+  if (Cin > 16) return hipErrorInvalidValue;
+  const size_t lds = ((size_t)C0 * Cin * 9 + C0) * 4;
+  if (lds > 65536) {
+    static bool attr = false;
+    if (!attr) {
+      hipError_t e = hipFuncSetAttribute((const void*)conv_in_k<0>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute((const void*)conv_in_k<4>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+  }
+  const int pblocks = (H * W + 63) / 64;
+  if (Cin == 4)
+    hipLaunchKernelGGL(conv_in_k<4>, dim3((unsigned)(rows * pblocks)), dim3(256), lds, s, x, w, b,
+                       Cin, H, W, C0, rows, out);
+  else
+    hipLaunchKernelGGL(conv_in_k<0>, dim3((unsigned)(rows * pblocks)), dim3(256), lds, s, x, w, b,
+                       Cin, H, W, C0, rows, out);
   return hipGetLastError();
 }
 

@@ -155,6 +155,8 @@ bool validate_cfg(const nv_unet_config* c, std::string* why) {
     return fail("H and W must be divisible by 2^(n_levels-1)");
   if (c->ctx_len < 1 || c->ctx_dim < 8 || c->ctx_dim % 8) return fail("bad context shape");
   if (!(c->gn_eps > 0) || !(c->ln_eps > 0)) return fail("eps must be > 0");
+  if ((size_t)c->ch[0] * c->in_ch * 36 + (size_t)c->ch[0] * 4 > 160 * 1024)
+    return fail("conv_in weights must fit in LDS (ch[0] * in_ch * 9 floats)");
   if (c->pooled_dim != 0 && c->pooled_dim != 4 * c->ch[0])
     return fail("pooled_dim must be 0 or 4*ch[0]");
   for (int l = 0; l < c->n_levels; ++l) {

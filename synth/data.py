@@ -16,8 +16,9 @@ CHUNK = 65536
 def to_bf16_bits(x):
     """float32 -> uint16 bfloat16 bit patterns, round to nearest even."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = x.view(np.uint32)
+    # finite inputs cannot overflow: 0xFF7FFFFF + 0x8000 < 2**32
+    u = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return u.astype(np.uint16)
 
 
@@ -37,23 +38,38 @@ def cluster_centres(clusters, d, seed):
 def _chunk_rows(mu, sigma, seed, chunk_index, rows):
     rng = np.random.default_rng([seed, 1, chunk_index])
     cid = rng.integers(0, mu.shape[0], size=rows)
-    x = mu[cid] + np.float32(sigma) * rng.standard_normal((rows, mu.shape[1]), dtype=np.float32)
-    nrm = np.sqrt(np.einsum("ij,ij->i", x.astype(np.float64), x.astype(np.float64)))
-    return (x / nrm[:, None]).astype(np.float32)
+    x = rng.standard_normal((rows, mu.shape[1]), dtype=np.float32)
+    x *= np.float32(sigma)
+    x += mu[cid]
+    nrm = np.sqrt(np.einsum("ij,ij->i", x, x, dtype=np.float32))
+    x /= nrm[:, None]
+    return x
 
 
-def make_cache(n, d, clusters, sigma, seed, dtype="bf16", dup_pairs=()):
+def make_cache(n, d, clusters, sigma, seed, dtype="bf16", dup_pairs=(), threads=16):
     """Cache of n unit-norm embeddings.
 
     dtype "f32" -> float32 [n][d]; "bf16" -> uint16 bit patterns [n][d].
     dup_pairs: (i, j) pairs; row j is overwritten with an exact copy of row i.
+    Chunks have their own streams, so the values do not depend on `threads`.
     """
+    from concurrent.futures import ThreadPoolExecutor
     mu = cluster_centres(clusters, d, seed)
     out = np.empty((n, d), dtype=np.float32 if dtype == "f32" else np.uint16)
-    for c, start in enumerate(range(0, n, CHUNK)):
+
+    def fill(c):
+        start = c * CHUNK
         rows = min(CHUNK, n - start)
         x = _chunk_rows(mu, sigma, seed, c, rows)
         out[start:start + rows] = x if dtype == "f32" else to_bf16_bits(x)
+
+    nchunks = (n + CHUNK - 1) // CHUNK
+    if threads > 1 and nchunks > 1:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(fill, range(nchunks)))
+    else:
+        for c in range(nchunks):
+            fill(c)
     for i, j in dup_pairs:
         out[j] = out[i]
     return out
@@ -83,7 +99,13 @@ def make_queries_at_sims(targets, sims, seed):
 
 def make_cluster_queries(m, d, clusters, sigma, cache_seed, seed):
     """Fresh draws from the cache's cluster process (new prompts of a popular theme)."""
-    mu = cluster_centres(clusters, d, cache_seed)
+    return cluster_queries_from(cluster_centres(clusters, d, cache_seed), m, sigma, seed)
+
+
+def cluster_queries_from(mu, m, sigma, seed):
+    """Fresh draws normalize(mu_c + sigma * g) around given centres mu [clusters][d]."""
+    mu = np.asarray(mu, dtype=np.float32)
+    clusters, d = mu.shape
     rng = np.random.default_rng([seed, 3])
     cid = rng.integers(0, clusters, size=m)
     x = mu[cid].astype(np.float64) + sigma * rng.standard_normal((m, d))
@@ -106,3 +128,37 @@ def make_latents(b, c, h, w, seed):
 def make_k_values(b, choices, seed):
     rng = np.random.default_rng([seed, 6])
     return rng.choice(np.asarray(choices, dtype=np.int32), size=b)
+
+
+def _device_centres(g, clusters, d, device):
+    import torch
+    mu = torch.randn(clusters, d, generator=g, device=device, dtype=torch.float32)
+    return mu / mu.norm(dim=1, keepdim=True)
+
+
+def cluster_centres_device(clusters, d, seed, device):
+    """The centres make_cache_device draws first from its generator (float32 [clusters][d])."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    return _device_centres(g, clusters, d, device)
+
+
+def make_cache_device(n, d, clusters, sigma, seed, device, chunk=1 << 20):
+    """The same cluster recipe drawn with torch's seeded generator on `device`, for caches
+    too large to generate on the host (10M x 768).  Returns a torch.bfloat16 [n][d]
+    tensor (round to nearest even); values depend only on (seed, n, d, clusters, sigma,
+    chunk) and the device type."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    mu = _device_centres(g, clusters, d, device)
+    out = torch.empty((n, d), dtype=torch.bfloat16, device=device)
+    for start in range(0, n, chunk):
+        rows = min(chunk, n - start)
+        cid = torch.randint(0, clusters, (rows,), generator=g, device=device)
+        x = torch.randn(rows, d, generator=g, device=device, dtype=torch.float32)
+        x.mul_(sigma).add_(mu[cid])
+        x /= x.norm(dim=1, keepdim=True)
+        out[start:start + rows] = x.to(torch.bfloat16)
+    return out

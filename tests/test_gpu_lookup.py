@@ -1,9 +1,10 @@
 """GPU parity of the cache lookup and state fetch against the oracle.
 
 Bar: idx, sim and K bit-identical to the oracle (Sec. 4.3 Alg. 1 search +
-Sec. 5.3.1 selector), at small sizes spanning several 256-row tiles with
-ragged tails, on the edge cases (ties, overflowing candidate lists, empty
-cache, threshold boundaries) and at the workloads' full sizes.
+Sec. 5.3.1 selector), at small sizes spanning several 128- and 256-row tiles
+with ragged tails and several 16-query blocks, on the edge cases (ties,
+overflowing candidate lists, empty cache, threshold boundaries) and at the
+workloads' full sizes (exact for sampled queries, properties for the rest).
 """
 import numpy as np
 import pytest
@@ -65,7 +66,8 @@ def test_tiny_workload():
 
 
 @pytest.mark.parametrize("n,d,m", [(1, 64, 1), (255, 64, 3), (257, 768, 8), (5000, 768, 17),
-                                   (1500, 40, 40), (777, 2048, 2)])
+                                   (1500, 40, 40), (777, 2048, 2), (129, 768, 33),
+                                   (300, 1024, 20)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_random_caches(n, d, m, dtype):
     print(f"lookup random n={n} d={d} m={m} {dtype}", flush=True)
@@ -84,6 +86,11 @@ def test_overflowing_candidate_lists():
     q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, [1234]), [0.97], 4)
     gi, _, gk = _check(q, cache)
     assert gi[0] == 50 and gk[0] == 25
+    # the same cache with 20 queries (two query blocks), all near the duplicated row
+    q20 = synth.make_queries_at_sims(synth.cache_rows_f32(cache, [1234] * 20),
+                                     np.linspace(0.99, 0.9, 20), 6)
+    gi, _, _ = _check(q20, cache)
+    assert np.all(gi == 50)
     same = np.repeat(_rand(1, 64, 2, "bf16"), 700 * 256 + 3, axis=0)  # > 512 overflowing tiles
     q = synth.make_queries_at_sims(synth.cache_rows_f32(same, [0]), [0.9], 5)
     gi, _, _ = _check(q, same)
@@ -138,6 +145,70 @@ def test_sd15_b8_cache_full_size_sampled():
         assert gi[j] == i and gs[j] == np.float32(v)
         assert gk[j] == LK.select_k(np.float32(v), TP, KP)
         print(f"  q{j}: idx {i} sim {v:.6f} K {gk[j]}", flush=True)
+
+
+def test_256_queries_against_oracle():
+    """The retrieval-heavy query shape (256 queries, half within cosine 0.95 of a cached
+    row) on a 20k-row cache the oracle scans whole."""
+    print("lookup 20k x 768 bf16, 256 queries", flush=True)
+    cache = synth.make_cache(20_000, 768, 100, 0.05, 41)
+    rng = np.random.default_rng(42)
+    near = synth.make_queries_at_sims(synth.cache_rows_f32(cache, rng.choice(20_000, 128)),
+                                      rng.uniform(0.95, 0.995, 128), 43)
+    far = synth.make_cluster_queries(128, 768, 100, 0.05, 41, 44)
+    gi, _, gk = _check(np.concatenate([near, far]), cache)
+    assert np.all(gk[:128] >= 20)
+
+
+def test_retrieval_heavy_full_size_sampled():
+    """10M x 768 bf16 cache drawn on the device, 256 queries.  Exact against the oracle
+    for one query (every row rescored canonically); for all 256: the returned row's
+    canonical score gives sim and K, it dominates the planted row and a row sample."""
+    import paper_2312_04429_amd as P
+    w = synth.WORKLOADS["retrieval_heavy"]
+    n, d = w["n_cache"], w["d"]
+    print("lookup retrieval-heavy: drawing 10M x 768 on the device", flush=True)
+    cache = synth.make_cache_device(n, d, w["clusters"], w["sigma"], w["cache_seed"], "cuda")
+    mu = synth.cluster_centres_device(w["clusters"], d, w["cache_seed"], "cuda").cpu().numpy()
+    rng = np.random.default_rng(w["query_seed"])
+    half = w["n_queries"] // 2
+    planted = rng.choice(n, half, replace=False)
+    rows = cache[torch.from_numpy(planted).cuda()].view(torch.int16).cpu().numpy().view(np.uint16)
+    near = synth.make_queries_at_sims(synth.from_bf16_bits(rows), rng.uniform(0.95, 0.995, half),
+                                      w["query_seed"])
+    far = synth.cluster_queries_from(mu, half, w["sigma"], w["query_seed"] + 1)
+    q = np.concatenate([near, far])
+    print("  lookup 256 queries", flush=True)
+    idx, sim, kk = P.nv_cache_lookup(torch.from_numpy(q).cuda(), cache, TP, KP)
+    gi, gs, gk = idx.cpu().numpy(), sim.cpu().numpy(), kk.cpu().numpy()
+
+    def host_rows(r):
+        t = cache[torch.from_numpy(np.asarray(r, dtype=np.int64)).cuda()]
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+    best = host_rows(gi)
+    sample = rng.choice(n, 4096, replace=False)
+    samp = host_rows(sample)
+    print("  properties for 256 queries", flush=True)
+    for j in range(len(q)):
+        sj = LK.canonical_scores(q[j], best[j:j + 1])[0]
+        assert gs[j] == np.float32(sj) and gk[j] == LK.select_k(np.float32(sj), TP, KP)
+        if j < half:
+            sp = LK.canonical_scores(q[j], rows[j:j + 1])[0]
+            assert sj > sp or (sj == sp and gi[j] <= planted[j])
+        ss = LK.canonical_scores(q[j], samp)
+        assert np.all((ss < sj) | ((ss == sj) & (sample >= gi[j])))
+    assert np.all(gk[:half] >= 20)
+    j = half  # a far query: every row through the oracle, 1M rows at a time
+    print("  exact scan of one query over 10M rows (oracle)", flush=True)
+    bi, bs = -1, -np.inf
+    for start in range(0, n, 1 << 20):
+        blk = cache[start:start + (1 << 20)].view(torch.int16).cpu().numpy().view(np.uint16)
+        i, v = LK.top1_fast(LK.canonical_scores(q[j], blk))
+        if v > bs:
+            bi, bs = start + i, v
+    print(f"  q{j}: oracle idx {bi} sim {bs:.6f}; gpu idx {gi[j]} sim {gs[j]:.6f}", flush=True)
+    assert gi[j] == bi and gs[j] == np.float32(bs)
 
 
 def test_gather_states():
