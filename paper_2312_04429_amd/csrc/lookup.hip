@@ -10,8 +10,9 @@
 //      accumulation error of any summation order, plus the float64 canonical
 //      sum's own error).  Per tile (128 rows for bf16 with d <= 768, else
 //      256) the kernel keeps the best lower bound L_t, the best upper bound
-//      U_t and the rows whose upper bound reaches L_t (at most CAP, in row
-//      order; more sets an overflow count).
+//      U_t (float32 bounds widened to cover their own rounding) and the rows
+//      whose upper bound reaches L_t (at most CAP, in row order; more sets an
+//      overflow count).
 //   2. select: per query, L = max_t L_t; every row whose upper bound can reach
 //      L lives in a tile with U_t >= L and is listed there (or the tile
 //      overflowed and is rescanned whole).  Those rows are rescored with the
@@ -97,6 +98,7 @@ __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int 
     red[2][threadIdx.x >> 6] = nq;
   }
   __syncthreads();
+  if (threadIdx.x == 0 && j >= m) E[j] = 0.0;  // padding rows of the last query block
   if (threadIdx.x == 0 && j < m) {
     e = red[0][0] + red[0][1] + red[0][2] + red[0][3];
     nb = red[1][0] + red[1][1] + red[1][2] + red[1][3];
@@ -107,14 +109,28 @@ __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int 
   }
 }
 
+// Rigorous float32 bounds s~ +- dd.  dd = nr * e with nr >= |c_i| and
+// e >= E_q (both rounded up beforehand), so |s~ - s64| <= dd.  t = s~ +- dd
+// is off from the exact sum by at most 2^-24 |t| (one rounding, or none more
+// if contracted into an fma), and the final step rounds once more; the slack
+// |t| 2^-20 + 2^-100 covers both with room, including subnormal products.
+__device__ inline float upper_bound(float sc, float dd) {
+  const float t = sc + dd;
+  return t + fmaf(fabsf(t), 0x1p-20f, 0x1p-100f);
+}
+__device__ inline float lower_bound(float sc, float dd) {
+  const float t = sc - dd;
+  return t - fmaf(fabsf(t), 0x1p-20f, 0x1p-100f);
+}
+
 // Shared tail of the scans: the block's scores sS[q][r] (row stride TR + TPQ)
 // and row norms sN[r] are in LDS; Eq is the margin factor of the calling
-// thread's query (threadIdx.x / (NT / QB)).  NT / QB consecutive threads own one query;
-// each covers TR / (NT / QB) rows of the tile, forms their bounds, and the
-// group maxima come from lane shuffles.  Rows whose upper bound reaches the
-// group's best lower bound are listed in row order through a wave ballot, so
-// the list is deterministic.  No barrier inside: the scans double-buffer sS
-// and sN.
+// thread's query (threadIdx.x / (NT / QB)).  NT / QB consecutive threads own
+// one query; each covers TR / (NT / QB) rows of the tile, forms their bounds,
+// and the group maxima come from lane shuffles.  Rows whose upper bound
+// reaches the group's best lower bound are listed in row order through a wave
+// ballot, so the list is deterministic.  No barrier inside: the scans
+// double-buffer sS.
 template <int NT, int TR>
 __device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_t n, int q0,
                               int qcount, int T, double Eq, LookupWs ws) {
@@ -123,21 +139,23 @@ __device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_
   const int t = threadIdx.x, q = t / TPQ, sub = t % TPQ, lane = t & 63;
   const int64_t row0 = (int64_t)tile * TR;
   const bool act = q < qcount;
+  const bool full = row0 + TR <= n;  // uniform: every row of the tile exists
+  // e >= Eq: (1 + 2^-22) absorbs the rounding to float32
+  const float e = act ? (float)(Eq * (1.0 + 0x1p-22)) : 0.f;
   const float* sq = sS + q * SS;
-  double L = -INFINITY, U = -INFINITY;
+  float L = -INFINITY, U = -INFINITY;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
     const int r = sub + j * TPQ;
-    if (act && row0 + r < n) {
-      const double sc = (double)sq[r], dd = (double)sN[r] * Eq;
-      L = fmax(L, sc - dd);
-      U = fmax(U, sc + dd);
-    }
+    const float sc = sq[r], dd = sN[r] * e;
+    const bool ok = act && (full || row0 + r < n);
+    L = ok ? fmaxf(L, lower_bound(sc, dd)) : L;
+    U = ok ? fmaxf(U, upper_bound(sc, dd)) : U;
   }
 #pragma unroll
   for (int o = TPQ / 2; o > 0; o >>= 1) {
-    L = fmax(L, __shfl_xor(L, o, 64));
-    U = fmax(U, __shfl_xor(U, o, 64));
+    L = fmaxf(L, __shfl_xor(L, o, 64));
+    U = fmaxf(U, __shfl_xor(U, o, 64));
   }
   const int gbase = lane & ~(TPQ - 1);
   const uint64_t gmask = (TPQ == 64 ? ~0ull : ((1ull << (TPQ & 63)) - 1)) << gbase;
@@ -147,11 +165,8 @@ __device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
     const int r = sub + j * TPQ;
-    bool p = false;
-    if (act && row0 + r < n) {
-      const double sc = (double)sq[r], dd = (double)sN[r] * Eq;
-      p = sc + dd >= L;
-    }
+    const float sc = sq[r], dd = sN[r] * e;
+    const bool p = act && (full || row0 + r < n) && upper_bound(sc, dd) >= L;
     const uint64_t bal = __ballot(p);
     if (p) {
       const int pos = cnt + __popcll(bal & gmask & below);
@@ -160,8 +175,8 @@ __device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_
     cnt += __popcll(bal & gmask);
   }
   if (act && sub == 0) {
-    ws.tileL[(int64_t)(q0 + q) * T + tile] = L;
-    ws.tileU[(int64_t)(q0 + q) * T + tile] = U;
+    ws.tileL[(int64_t)(q0 + q) * T + tile] = (double)L;
+    ws.tileU[(int64_t)(q0 + q) * T + tile] = (double)U;
     ws.cnt[(int64_t)(q0 + q) * T + tile] = cnt;
   }
 }
@@ -174,6 +189,26 @@ constexpr int SS_RR = RR_TILE + 16;
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+typedef __attribute__((address_space(1))) const void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+// Request one 16-query block of bf16 queries and its 16 margin factors
+// straight into LDS (global -> LDS 16-byte loads, no registers): in each
+// round, wave w moves the 64 chunks starting at chunk (round * 4 + w) * 64;
+// lane l's chunk lands 16 l bytes past the wave's LDS base.  Complete after
+// the issuing wave's vmcnt reaches 0.
+__device__ inline void dma_queries(uint16_t* sQ, double* sE, const LookupWs& ws, int q0, int d) {
+  const int nc = QB * d / 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const char* src = (const char*)(ws.qbf + (int64_t)q0 * d);
+  for (int base = wave * 64; base < nc; base += 256)
+    if (base + lane < nc)
+      __builtin_amdgcn_global_load_lds((gptr_t)(src + (size_t)(base + lane) * 16),
+                                       (lptr_t)((char*)sQ + (size_t)base * 16), 16, 0, 0);
+  if (wave == 0 && lane < QB / 2)
+    __builtin_amdgcn_global_load_lds((gptr_t)(ws.E + q0 + 2 * lane), (lptr_t)sE, 16, 0, 0);
 }
 
 // Stage one 16-query block of bf16 queries into LDS.
@@ -274,18 +309,37 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
   }
 }
 
+// 16 rows x 16 queries x (KS * 32) k for both row blocks of a wave; Q is the
+// query block in LDS (its own buffer: __restrict__ lets the compiler tell
+// these reads from global -> LDS loads in flight into the other buffer).
+__device__ __forceinline__ void rr_block(const uint16_t* __restrict__ Q, const u32x4 (&a)[KS][2],
+                                         int d, int li, int kc, floatx4& acc0, floatx4& acc1) {
+#pragma unroll
+  for (int j = 0; j < KS; ++j) {
+    const int k = j * 32 + kc * 8;
+    uint4 qv = make_uint4(0, 0, 0, 0);
+    if (k < d) qv = *(const uint4*)(Q + li * d + k);
+    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(bf16x8*)&qv, acc0, 0,
+                                                   0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(bf16x8*)&qv, acc1, 0,
+                                                   0, 0);
+  }
+}
+
 // bf16 cache with d <= 768, any m: 4 waves, each holding its 32
 // cache rows (two 16-row blocks, the whole k range) in registers for the
 // entire query range, so the cache is read from HBM once; 16-query blocks
 // stream through a double-buffered LDS and each query fragment read feeds both
-// row blocks.  128-row tiles let two workgroups share a CU, so one loads while
-// the other multiplies.
+// row blocks.  Query blocks move global -> LDS without registers, a block
+// ahead.  128-row tiles let two workgroups share a CU, so one loads while the
+// other multiplies.
 __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restrict__ cache,
                                                           int64_t n, int d, int m, int T,
                                                           LookupWs ws) {
   extern __shared__ __align__(16) unsigned char smem[];
-  uint16_t* sQ = (uint16_t*)smem;                       // [2][QB][d]
-  float* sS = (float*)(smem + 2 * QB * d * 2);          // [2][QB][SS_RR]
+  double* sE = (double*)smem;                           // [3][QB] margin factors
+  uint16_t* sQ = (uint16_t*)(smem + 3 * QB * 8);        // [2][QB][d]
+  float* sS = (float*)((char*)sQ + 2 * QB * d * 2);     // [2][QB][SS_RR]
   float* sN = sS + 2 * QB * SS_RR;                      // [RR_TILE]
   const int tile = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -304,25 +358,11 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
       a[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     }
   }
-  // next query block travels through registers: QB * d / 8 chunks of 16 bytes
-  const int nqc = QB * d / 8;
-  constexpr int QPT = (QB * 32 * KS / 8 + 255) / 256;
-  uint4 qr[QPT];
-  auto qfetch = [&](int q0) {
-#pragma unroll
-    for (int i = 0; i < QPT; ++i) {
-      const int c = tid + i * 256;
-      if (c < nqc) qr[i] = ((const uint4*)(ws.qbf + (int64_t)q0 * d))[c];
-    }
-  };
-  auto qstash = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < QPT; ++i) {
-      const int c = tid + i * 256;
-      if (c < nqc) ((uint4*)(sQ + buf * QB * d))[c] = qr[i];
-    }
-  };
-  stage_queries(sQ, ws.qbf, 0, d);
+  // Query blocks 0 and 1 with their margin factors; block i + 2 is requested
+  // right after the barrier of block i (its buffers were last read by block
+  // i's multiplies and block i - 1's tail).
+  dma_queries(sQ, sE, ws, 0, d);
+  if (QB < m) dma_queries(sQ + QB * d, sE + QB, ws, QB, d);
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     float nn = 0.f;
@@ -337,37 +377,24 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
     nn += __shfl_xor(nn, 32, 64);
     if (kc == 0) sN[wave * 32 + b * 16 + li] = sqrtf(nn * 1.001f);
   }
-  // Query block i + 1 (registers) and the margin factors of block i + 1 are
-  // requested a whole block ahead: after the barrier of block i - 1.
-  if (QB < m) qfetch(QB);
-  double Ecur = query_margin<256>(ws.E, 0, m), Enext = query_margin<256>(ws.E, QB, m);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  const int qg = tid / (256 / QB);  // this thread's query within a block (tile tail)
   for (int q0 = 0, i = 0; q0 < m; q0 += QB, ++i) {
     const uint16_t* Q = sQ + (i & 1) * QB * d;
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < KS; ++j) {
-      const int k = j * 32 + kc * 8;
-      uint4 qv = make_uint4(0, 0, 0, 0);
-      if (k < d) qv = *(const uint4*)(Q + li * d + k);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(bf16x8*)&qv, acc0,
-                                                     0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(bf16x8*)&qv, acc1,
-                                                     0, 0, 0);
-    }
+    rr_block(Q, a, d, li, kc, acc0, acc1);
     float* S = sS + (i & 1) * QB * SS_RR;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       S[li * SS_RR + wave * 32 + kc * 4 + r] = acc0[r];
       S[li * SS_RR + wave * 32 + 16 + kc * 4 + r] = acc1[r];
     }
-    // block i + 1 -> the other LDS buffer, last read by block i - 1's multiplies
-    if (q0 + QB < m) qstash((i + 1) & 1);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of block i + 1 has landed
     __syncthreads();
-    if (q0 + 2 * QB < m) qfetch(q0 + 2 * QB);
-    const double Eq = Ecur;
-    Ecur = Enext;
-    Enext = query_margin<256>(ws.E, q0 + 2 * QB, m);
+    if (q0 + 2 * QB < m)
+      dma_queries(sQ + (i & 1) * QB * d, sE + ((i + 2) % 3) * QB, ws, q0 + 2 * QB, d);
+    const double Eq = q0 + qg < m ? sE[(i % 3) * QB + qg] : 0.0;
     tile_finalize<256, RR_TILE>(S, sN, tile, n, q0, min(QB, m - q0), T, Eq, ws);
   }
 }
@@ -546,7 +573,7 @@ WsPlan plan_ws(int32_t m, int64_t n, int32_t d, int tr) {
   const int64_t mq = ceil_div(m, QB) * QB;
   size_t o = 0;
   p.off_qbf = o;  o = align_up(o + (size_t)mq * d * 2, 256);
-  p.off_E = o;    o = align_up(o + (size_t)m * 8, 256);
+  p.off_E = o;    o = align_up(o + (size_t)mq * 8, 256);
   p.off_L = o;    o = align_up(o + (size_t)m * T * 8, 256);
   p.off_U = o;    o = align_up(o + (size_t)m * T * 8, 256);
   p.off_cnt = o;  o = align_up(o + (size_t)m * T * 4, 256);
@@ -612,7 +639,8 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
   NV_LAUNCH_CHECK("lk_prep");
   if (T > 0) {
     if (rr) {
-      const size_t lds = (size_t)2 * QB * d * 2 + (size_t)2 * QB * SS_RR * 4 + RR_TILE * 4;
+      const size_t lds =
+          (size_t)3 * QB * 8 + (size_t)2 * QB * d * 2 + (size_t)2 * QB * SS_RR * 4 + RR_TILE * 4;
       NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
       trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
