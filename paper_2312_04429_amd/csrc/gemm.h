@@ -37,6 +37,7 @@ struct GemmArgs {
   // filled by gemm_launch: byte extents of src1 / src2
   uint64_t bytes1, bytes2;
   int n_major;  // tile order: weight columns outermost (filled by gemm_launch)
+  int vec_ok;   // epilogue quads may use vector loads / stores (filled by gemm_launch)
 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);

@@ -37,6 +37,17 @@ constexpr int ROW = BK + 8;  // halfs per LDS row
 
 constexpr uint32_t OOB = 0x80000000u;  // offset past every descriptor's range
 
+// ring depth of the streamed kernel per tile shape (LDS: depth x (BM + BN) x 128 bytes)
+#ifndef GEMM_S128
+#define GEMM_S128 2
+#endif
+#ifndef GEMM_S12864
+#define GEMM_S12864 3
+#endif
+#ifndef GEMM_S64
+#define GEMM_S64 4
+#endif
+
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
@@ -48,26 +59,80 @@ __device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
 __device__ inline float silu(float x) { return x / (1.0f + __expf(-x)); }
 
-// Element epilogue (non-GEGLU).
-__device__ inline void store_out(const GemmArgs& g, int64_t m, int n, float v) {
-  if (g.bias) v += g.bias[n];
-  if (g.rowvec) v += g.rowvec[(m / g.rows_div) * (int64_t)g.ld_rowvec + n];
-  if (g.silu) v = silu(v);
-  if (g.residual) v += (float)g.residual[m * g.ld_res + n];
-  if (g.out_f32)
-    ((float*)g.out)[m * g.ldo + n] = v;
-  else
-    ((_Float16*)g.out)[m * g.ldo + n] = (_Float16)v;
+// Epilogue of 4 consecutive columns n..n+3 of row m (non-GEGLU): + bias,
+// + rowvec, SiLU, + residual, then float16 or float32 out.  vec: the quad is
+// inside N and every row stride keeps it 8-byte (float16) / 16-byte (float32)
+// aligned, so it moves as one vector; otherwise element by element.
+__device__ inline void store_out4(const GemmArgs& g, int64_t m, int n, float (&v)[4], bool vec) {
+  const int nn = vec ? 4 : max(0, min(4, g.N - n));
+  if (g.bias) {
+    if (vec) {
+      const float4 b = *(const float4*)(g.bias + n);
+      v[0] += b.x; v[1] += b.y; v[2] += b.z; v[3] += b.w;
+    } else {
+      for (int r = 0; r < nn; ++r) v[r] += g.bias[n + r];
+    }
+  }
+  if (g.rowvec) {
+    const float* rv = g.rowvec + (m / g.rows_div) * (int64_t)g.ld_rowvec + n;
+    for (int r = 0; r < nn; ++r) v[r] += rv[r];
+  }
+  if (g.silu)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = silu(v[r]);
+  if (g.residual) {
+    const _Float16* rp = g.residual + m * g.ld_res + n;
+    if (vec) {
+      const half4 h = *(const half4*)rp;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] += (float)h[r];
+    } else {
+      for (int r = 0; r < nn; ++r) v[r] += (float)rp[r];
+    }
+  }
+  if (g.out_f32) {
+    float* o = (float*)g.out + m * g.ldo + n;
+    if (vec)
+      *(float4*)o = make_float4(v[0], v[1], v[2], v[3]);
+    else
+      for (int r = 0; r < nn; ++r) o[r] = v[r];
+  } else {
+    _Float16* o = (_Float16*)g.out + m * g.ldo + n;
+    if (vec) {
+      half4 h;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h[r] = (_Float16)v[r];
+      *(half4*)o = h;
+    } else {
+      for (int r = 0; r < nn; ++r) o[r] = (_Float16)v[r];
+    }
+  }
 }
 
-__device__ inline void store_geglu(const GemmArgs& g, int64_t m, int na, float a, float gt) {
-  // na: packed column of the "a" value (its gate sits 16 columns later)
-  if (g.bias) {
-    a += g.bias[na];
-    gt += g.bias[na + 16];
+// GEGLU quad: na is the packed column of the first "a" value (gates sit 16
+// columns later); output columns oc..oc+3 with oc = (na / 32) * 16 + na % 32.
+__device__ inline void store_geglu4(const GemmArgs& g, int64_t m, int na, const float (&a)[4],
+                                    const float (&gt)[4], bool vec) {
+  float y[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float av = a[r], gv = gt[r];
+    if (g.bias) {
+      av += g.bias[na + r];
+      gv += g.bias[na + 16 + r];
+    }
+    y[r] = av * gelu_erf(gv);
   }
   const int oc = (na >> 5) * 16 + (na & 15);
-  ((_Float16*)g.out)[m * g.ldo + oc] = (_Float16)(a * gelu_erf(gt));
+  _Float16* o = (_Float16*)g.out + m * g.ldo + oc;
+  if (vec) {
+    half4 h;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) h[r] = (_Float16)y[r];
+    *(half4*)o = h;
+  } else {
+    for (int r = 0; r < 4; ++r) o[r] = (_Float16)y[r];
+  }
 }
 
 template <int MODE, int BM, int BN, bool DUAL>
@@ -317,7 +382,7 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -349,77 +414,361 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
   }
   if (kt < kt1) compute(0);
 
-  // Lane holds rows 4*(lane/16)+r, column lane%16 of each 16x16 block.
+  // Operands are swapped in the multiply (weights as the row operand), so lane
+  // (li, kc) of block (i, j) holds row m = ... + i * 16 + li and the four
+  // consecutive columns n = ... + j * 16 + kc * 4 + r.
   if (gridDim.z > 1) {
     float* part = g.partial + (int64_t)blockIdx.z * g.M * g.N;
+    const bool pv = (g.N & 3) == 0;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i) {
+      const int64_t m = m0 + wm * WM + i * 16 + li;
+      if (m >= g.M) continue;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int n = n0 + wn * WN + j * 16 + li;
+        const int n = n0 + wn * WN + j * 16 + kc * 4;
         if (n >= g.N) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
-          if (m < g.M) part[m * g.N + n] = acc[i][j][r];
-        }
+        float* pp = part + m * g.N + n;
+        if (pv)
+          *(float4*)pp = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        else
+          for (int r = 0; r < 4 && n + r < g.N; ++r) pp[r] = acc[i][j][r];
       }
+    }
     return;
   }
+  const bool vec = g.vec_ok;
   if (g.geglu) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int64_t m = m0 + wm * WM + i * 16 + li;
+      if (m >= g.M) continue;
+#pragma unroll
+      for (int jj = 0; jj < FN / 2; ++jj) {
+        const int na = n0 + wn * WN + 2 * jj * 16 + kc * 4;
+        if (na + 16 >= g.N) continue;
+        float a[4], gt[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          a[r] = acc[i][2 * jj][r];
+          gt[r] = acc[i][2 * jj + 1][r];
+        }
+        store_geglu4(g, m, na, a, gt, vec);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int64_t m = m0 + wm * WM + i * 16 + li;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + kc * 4;
+      if (n >= g.N) continue;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      store_out4(g, m, n, v, vec && n + 4 <= g.N);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Streamed variant for shapes whose every 64-deep k tile lies inside one
+// source and one tap (dense: C1 and K multiples of 64; conv: C1 and C2
+// multiples of 64).  Tiles move global -> LDS with 16-byte buffer loads that
+// write LDS directly (no registers, no LDS store instructions) into a ring of
+// STAGES buffers; a wave waits for its own loads of the tile it is about to
+// multiply (vmcnt), one barrier per tile publishes everyone's, and the tile
+// STAGES - 1 ahead is requested right after it.  Rows are 128 bytes with the
+// 16-byte chunk c of row r stored at chunk c ^ (r & 7): the 16 rows a quarter
+// wave reads at one k offset hit distinct bank groups.  Out-of-range rows and
+// padding taps use an offset past the descriptor's range and land as zeros.
+__device__ inline void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t off, void* lds_wave_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_wave_base,
+                                           16, off, 0, 0, 0);
+}
+
+// s_waitcnt with only vmcnt limited (expcnt, lgkmcnt at their maxima; gfx9 encoding).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier for the ring: each wave has already waited (vmcnt) for its
+// own loads of the tile about to be read, so the barrier alone publishes the
+// tile; no memory fence, which would also wait for the loads still in flight
+// into the other buffers.  The empty asm statements keep the compiler from
+// moving LDS accesses across it.
+__device__ inline void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One 64-deep k tile: wave tile (FM x 16) rows by (FN x 16) columns.  The
+// tile's LDS buffers are read through restrict-qualified pointers: while this
+// runs, only other ring buffers are being written (by loads in flight).
+template <int FM, int FN>
+__device__ __forceinline__ void mma_tile(const _Float16* __restrict__ a,
+                                         const _Float16* __restrict__ b, int arow0, int brow0,
+                                         int li, int kc, floatx4 (&acc)[FM][FN]) {
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    const int c = sub * 4 + kc;
+    half8 fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r = arow0 + i * 16 + li;
+      fa[i] = *(const half8*)(a + r * 64 + ((c ^ (r & 7)) << 3));
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int r = brow0 + j * 16 + li;
+      fb[j] = *(const half8*)(b + r * 64 + ((c ^ (r & 7)) << 3));
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int jj = 0; jj < FN / 2; ++jj) {
-        const int na = n0 + wn * WN + 2 * jj * 16 + li;
-        if (na + 16 >= g.N) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
-          if (m < g.M) store_geglu(g, m, na, acc[i][2 * jj][r], acc[i][2 * jj + 1][r]);
-        }
-      }
-    return;
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[j], fa[i], acc[i][j], 0, 0, 0);
   }
+}
+
+template <int MODE, int BM, int BN, int STAGES>
+__global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int AJ = BM / 32, BJ = BN / 32;  // 8-row groups per wave per tile (A, B)
+  constexpr int OPS = AJ + BJ;               // loads per wave per tile
+  constexpr int TILE_H = (BM + BN) * 64;     // halfs per ring buffer
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* ring = (_Float16*)smem;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 15, kc = lane >> 4;
+  const int ntn = (g.N + BN - 1) / BN;
+  const int mtn = (int)((g.M + BM - 1) / BM);
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t m0 = (int64_t)(g.n_major ? tile % mtn : tile / ntn) * BM;
+  const int n0 = (g.n_major ? tile / mtn : tile % ntn) * BN;
+  const int nk = g.K / 64;
+  const int kt0 = blockIdx.z * kt_per_split;
+  const int kt1 = min(nk, kt0 + kt_per_split);
+  // loader geometry: group j of this wave covers rows (j * 4 + wave) * 8 ..+8;
+  // lane l loads row +l/8, chunk slot l%8, i.e. k chunk (l%8) ^ (l/8)
+  const int lrow = lane >> 3;
+  const int cch = (lane & 7) ^ lrow;
+  const __amdgpu_buffer_rsrc_t rs1 = make_rsrc(g.src1, g.bytes1);
+  const __amdgpu_buffer_rsrc_t rs2 = make_rsrc(g.src2 ? g.src2 : g.src1, g.src2 ? g.bytes2 : 0);
+  const __amdgpu_buffer_rsrc_t rsw = make_rsrc(g.w, (uint32_t)((int64_t)g.N * g.ldw * 2));
+
+  int64_t a_m[AJ];
+  int a_b[AJ], a_oy[AJ], a_ox[AJ];
+#pragma unroll
+  for (int j = 0; j < AJ; ++j) {
+    a_m[j] = m0 + (j * 4 + wave) * 8 + lrow;
+    a_b[j] = a_oy[j] = a_ox[j] = 0;
+    if (MODE == 1 && a_m[j] < g.M) {
+      const int hw = g.Ho * g.Wo;
+      a_b[j] = (int)(a_m[j] / hw);
+      const int p = (int)(a_m[j] - (int64_t)a_b[j] * hw);
+      a_oy[j] = p / g.Wo;
+      a_ox[j] = p - a_oy[j] * g.Wo;
+    }
+  }
+  const int cin = g.C1 + g.C2;
+  int t_k0 = kt0 * 64, t_tap = 0, t_ci = 0;
+  bool t_first = true;
+  if (MODE == 1) {
+    t_tap = t_k0 / cin;
+    t_ci = t_k0 - t_tap * cin;
+  }
+  uint32_t aoff[AJ], boff[BJ];
+  auto a_offsets = [&]() {
+    if (MODE == 0) {
+      t_first = t_k0 < g.C1;
+#pragma unroll
+      for (int j = 0; j < AJ; ++j) {
+        const bool ok = a_m[j] < g.M && t_k0 < g.K;
+        aoff[j] = !ok ? OOB
+                : t_first ? (uint32_t)((a_m[j] * g.lda1 + t_k0 + cch * 8) * 2)
+                          : (uint32_t)((a_m[j] * g.lda2 + (t_k0 - g.C1) + cch * 8) * 2);
+      }
+    } else {
+      t_first = t_ci < g.C1;
+      const int ky = (t_tap * 11) >> 5, kx = t_tap - 3 * ((t_tap * 11) >> 5);
+      const int ld = t_first ? g.C1 : g.C2;
+      const int cs = (t_first ? t_ci : t_ci - g.C1) + cch * 8;
+#pragma unroll
+      for (int j = 0; j < AJ; ++j) {
+        int iy, ix;
+        bool in;
+        if (g.upsample) {
+          const int uy = a_oy[j] + ky - 1, ux = a_ox[j] + kx - 1;
+          in = uy >= 0 && ux >= 0 && uy < 2 * g.Hin && ux < 2 * g.Win;
+          iy = uy >> 1;
+          ix = ux >> 1;
+        } else {
+          iy = a_oy[j] * g.stride + ky - 1;
+          ix = a_ox[j] * g.stride + kx - 1;
+          in = iy >= 0 && ix >= 0 && iy < g.Hin && ix < g.Win;
+        }
+        const bool ok = a_m[j] < g.M && in && t_tap < 9;
+        const int64_t pix = ((int64_t)a_b[j] * g.Hin + iy) * g.Win + ix;
+        aoff[j] = ok ? (uint32_t)((pix * ld + cs) * 2) : OOB;
+      }
+    }
+  };
+  a_offsets();
+#pragma unroll
+  for (int j = 0; j < BJ; ++j) {
+    const int n = n0 + (j * 4 + wave) * 8 + lrow;
+    boff[j] = (n < g.N) ? (uint32_t)(((int64_t)n * g.ldw + t_k0 + cch * 8) * 2) : OOB;
+  }
+  // request the next tile in k order into ring buffer `buf`, then advance
+  auto issue = [&](int buf) {
+    _Float16* A = ring + buf * TILE_H;
+    _Float16* Bt = A + BM * 64;
+    const __amdgpu_buffer_rsrc_t rsa = t_first ? rs1 : rs2;
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) lds_dma16(rsa, aoff[j], A + (j * 4 + wave) * 512);
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) lds_dma16(rsw, boff[j], Bt + (j * 4 + wave) * 512);
+    t_k0 += 64;
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) boff[j] += 128;
+    bool fresh;
+    if (MODE == 0) {
+      fresh = t_k0 == g.C1 || t_k0 >= g.K;
+    } else {
+      t_ci += 64;
+      fresh = false;
+      if (t_ci >= cin) {
+        t_ci -= cin;
+        ++t_tap;
+        fresh = true;
+      }
+      if (t_ci == g.C1) fresh = true;
+    }
+    if (fresh) {
+      a_offsets();
+    } else {
+#pragma unroll
+      for (int j = 0; j < AJ; ++j) aoff[j] += 128;
+    }
+  };
+
+  floatx4 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + li;
-      if (n >= g.N) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t m = m0 + wm * WM + i * 16 + kc * 4 + r;
-        if (m < g.M) store_out(g, m, n, acc[i][j][r]);
-      }
-    }
-}
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-// Sum split-K partials in split order and apply the epilogue.
-__global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
-  const int64_t MN = g.M * (int64_t)g.N;
-  if (g.geglu) {
-    const int64_t total = g.M * (int64_t)(g.N / 2);
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * 256) {
-      const int64_t m = e / (g.N / 2);
-      const int oc = (int)(e - m * (g.N / 2));
-      const int na = (oc >> 4) * 32 + (oc & 15);
-      float a = 0.f, gt = 0.f;
-      for (int s = 0; s < splits; ++s) {
-        a += g.partial[s * MN + m * g.N + na];
-        gt += g.partial[s * MN + m * g.N + na + 16];
+  // Prologue: tiles kt0 .. kt0 + STAGES - 2.  Requests past kt1 fetch tiles
+  // that are never multiplied (in range or zero-filled), which keeps the
+  // per-wave count of loads in flight fixed for the waits below.
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s) issue(s);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    wait_vmcnt<(STAGES - 2) * OPS>();  // this wave's loads of tile kt have landed
+    ring_barrier();                    // everyone's have; buffer (kt - 1) is free
+    issue((kt - kt0 + STAGES - 1) % STAGES);
+    const _Float16* A = ring + ((kt - kt0) % STAGES) * TILE_H;
+    mma_tile<FM, FN>(A, A + BM * 64, wm * WM, wn * WN, li, kc, acc);
+  }
+  wait_vmcnt<0>();  // drain the requests past the last tile before the workgroup ends
+
+  // Operands are swapped in the multiply (weights as the row operand), so lane
+  // (li, kc) of block (i, j) holds row m = ... + i * 16 + li and the four
+  // consecutive columns n = ... + j * 16 + kc * 4 + r.
+  if (gridDim.z > 1) {
+    float* part = g.partial + (int64_t)blockIdx.z * g.M * g.N;
+    const bool pv = (g.N & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int64_t m = m0 + wm * WM + i * 16 + li;
+      if (m >= g.M) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int n = n0 + wn * WN + j * 16 + kc * 4;
+        if (n >= g.N) continue;
+        float* pp = part + m * g.N + n;
+        if (pv)
+          *(float4*)pp = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        else
+          for (int r = 0; r < 4 && n + r < g.N; ++r) pp[r] = acc[i][j][r];
       }
-      store_geglu(g, m, na, a, gt);
     }
     return;
   }
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < MN;
+  const bool vec = g.vec_ok;
+  if (g.geglu) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int64_t m = m0 + wm * WM + i * 16 + li;
+      if (m >= g.M) continue;
+#pragma unroll
+      for (int jj = 0; jj < FN / 2; ++jj) {
+        const int na = n0 + wn * WN + 2 * jj * 16 + kc * 4;
+        if (na + 16 >= g.N) continue;
+        float a[4], gt[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          a[r] = acc[i][2 * jj][r];
+          gt[r] = acc[i][2 * jj + 1][r];
+        }
+        store_geglu4(g, m, na, a, gt, vec);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int64_t m = m0 + wm * WM + i * 16 + li;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + kc * 4;
+      if (n >= g.N) continue;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      store_out4(g, m, n, v, vec && n + 4 <= g.N);
+    }
+  }
+}
+
+// Sum split-K partials in split order and apply the epilogue, four
+// consecutive columns per thread (N % 4 == 0, checked by the launcher).
+__global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
+  const int64_t MN = g.M * (int64_t)g.N;
+  const int nq = g.N / 4;
+  const int64_t total = g.geglu ? g.M * (int64_t)(g.N / 32) * 4 : g.M * (int64_t)nq;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * 256) {
-    float v = 0.f;
-    for (int s = 0; s < splits; ++s) v += g.partial[s * MN + e];
-    const int64_t m = e / g.N;
-    store_out(g, m, (int)(e - m * g.N), v);
+    if (g.geglu) {  // e -> (row, 32-column group, quad of the 16 "a" columns)
+      const int per_row = (g.N / 32) * 4;
+      const int64_t m = e / per_row;
+      const int rem = (int)(e - m * per_row);
+      const int na = (rem >> 2) * 32 + (rem & 3) * 4;
+      float a[4] = {0.f, 0.f, 0.f, 0.f}, gt[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < splits; ++s) {
+        const float4 pa = *(const float4*)(g.partial + s * MN + m * g.N + na);
+        const float4 pg = *(const float4*)(g.partial + s * MN + m * g.N + na + 16);
+        a[0] += pa.x; a[1] += pa.y; a[2] += pa.z; a[3] += pa.w;
+        gt[0] += pg.x; gt[1] += pg.y; gt[2] += pg.z; gt[3] += pg.w;
+      }
+      store_geglu4(g, m, na, a, gt, g.vec_ok);
+    } else {
+      const int64_t m = e / nq;
+      const int n = (int)(e - m * nq) * 4;
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < splits; ++s) {
+        const float4 p = *(const float4*)(g.partial + s * MN + m * g.N + n);
+        v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+      }
+      store_out4(g, m, n, v, g.vec_ok);
+    }
   }
 }
 
@@ -448,15 +797,56 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   hipLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), lds, s, g, kps);
   trace_post(fam, s);
   if (splits > 1) {
-    const int64_t total = g.geglu ? g.M * (int64_t)(g.N / 2) : g.M * (int64_t)g.N;
+    const int64_t total = g.M * (int64_t)(g.N / 4);
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
     hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
   }
   return hipGetLastError();
 }
 
+template <int MODE, int BM, int BN, int STAGES>
+hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
+  const size_t lds = (size_t)STAGES * (BM + BN) * 64 * 2;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int nk = g.K / 64;
+  const int kps = (nk + splits - 1) / splits;
+  splits = (nk + kps - 1) / kps;
+  dim3 grid((unsigned)(ceil_div(g.M, BM) * ceil_div(g.N, BN)), 1, (unsigned)splits);
+  const int fam = MODE == 1 ? NV_FAM_CONV : NV_FAM_LINEAR;
+  const double flops = 2.0 * (double)g.M * g.N * g.K;
+  const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
+                       (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
+  trace_pre(fam, flops, bytes, s);
+  hipLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES>), grid, dim3(256), lds, s, g, kps);
+  trace_post(fam, s);
+  if (splits > 1) {
+    const int64_t total = g.M * (int64_t)(g.N / 4);
+    const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+    hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
+  }
+  return hipGetLastError();
+}
+
+// Streamed kernel when every 64-deep k tile lies inside one source and tap.
+template <int MODE>
+bool streamable(const GemmArgs& g) {
+  if (g.C1 % 64 != 0) return false;
+  return MODE == 0 ? (g.K % 64 == 0) : ((g.C1 + g.C2) % 64 == 0);
+}
+
 template <int MODE, int BM, int BN>
 hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
+  if (streamable<MODE>(g)) {
+    if (BM == 128 && BN == 128) return launch_s<MODE, 128, 128, GEMM_S128>(g, splits, s);
+    if (BM == 128 && BN == 64) return launch_s<MODE, 128, 64, GEMM_S12864>(g, splits, s);
+    return launch_s<MODE, 64, 64, GEMM_S64>(g, splits, s);
+  }
   // the incremental single-source path needs every 64-deep tile inside one
   // source and inside K: C1 and K (dense) or C1 and Cin (conv) multiples of 64
   const bool dual = (g.C1 % BK) != 0 || (MODE == 0 && (g.K % BK) != 0) ||
@@ -481,7 +871,7 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
   const bool n_fits_128 = g.N % 128 == 0 || g.N > 512;
   auto split_for = [&](int64_t tiles, int min_kt) {
     int sp = 1;
-    if (!g.partial) return 1;
+    if (!g.partial || (g.N & 3) != 0) return 1;
     while (tiles * sp < TARGET && nk / (sp + 1) >= min_kt &&
            (size_t)(sp + 1) * g.M * g.N * 4 <= g.partial_bytes)
       ++sp;
@@ -507,6 +897,12 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
     g.bytes2 = g.src2 ? (uint64_t)(((g.M - 1) * g.lda2 + g.C2) * 2) : 0;
   }
   g.n_major = (int64_t)g.N >= g.M;  // weights at least as large as the activation rows
+  // quads of 4 output columns move as vectors when every row stride and base
+  // keeps them aligned (8 bytes float16, 16 bytes float32 / bias)
+  auto al = [](const void* p, int a) { return ((uintptr_t)p & (a - 1)) == 0; };
+  g.vec_ok = (g.N % 4 == 0) && (g.ldo % 4 == 0) && al(g.out, g.out_f32 ? 16 : 8) &&
+             (!g.bias || al(g.bias, 16)) &&
+             (!g.residual || ((g.ld_res % 4 == 0) && al(g.residual, 8)));
   return g.conv ? dispatch<1>(g, s) : dispatch<0>(g, s);
 }
 

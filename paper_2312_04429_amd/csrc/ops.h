@@ -25,8 +25,8 @@ struct GnArgs {
   const float* gamma;
   const float* beta;
   int silu;
-  float* part;           // [rows][ceil(HW/32)][G][2] chunk partials (scratch)
-  float* stats;          // [rows][G][2] (mean, rstd) scratch
+  float* part;           // [rows][part_chunks][G][2] chunk partials (scratch)
+  int part_chunks;       // chunk capacity per row of part (at least ceil(HW / 8))
   _Float16* out;         // [rows][HW][C1 + C2]
 };
 

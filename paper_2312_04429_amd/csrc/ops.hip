@@ -2,6 +2,7 @@
 // GroupNorm (+SiLU), LayerNorm, the sinusoidal time embedding, conv_in on the
 // float32 latent, classifier-free guidance + DDIM update, the DDIM schedule
 // tables, and layout/permutation helpers.
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -25,70 +26,97 @@ __device__ inline float load_cat(const _Float16* s1, int C1, const _Float16* s2,
   return c < C1 ? (float)s1[pix * C1 + c] : (float)s2[pix * C2 + (c - C1)];
 }
 
-// GroupNorm statistics, deterministic and two-pass at every level:
-//   gn_partial_k: one workgroup per (row, chunk of GN_CHUNK pixels).  Threads
-//     own 8-channel vectors (16-byte loads) for a phase of the chunk's pixels
-//     and keep per-channel sums in registers; LDS folds phases, then channels
-//     into groups, in a fixed order.  A second sweep (cache-resident) sums
-//     squared deviations from the chunk's group mean.  Output per (row,
-//     chunk, group): mean and sum of squared deviations.
-//   gn_finalize_k: one wave per (row, group) merges the chunks with the
-//     pairwise (Chan) update over a fixed tree and writes (mean, rstd).
-constexpr int GN_CHUNK = 32;
+// GroupNorm, deterministic and two-pass at every level, in two launches:
+//   gn_stats_k: one workgroup per (row, chunk of P pixels).  Threads own
+//     8-channel vectors (16-byte loads) of a phase of the chunk's pixels, held
+//     in registers for both passes (one sweep over memory); LDS folds phases,
+//     then channels into groups, in a fixed order.  Output per (row, chunk,
+//     group): mean and sum of squared deviations from it.
+//   gn_apply_k: one workgroup per (row, block of Q pixels).  It first merges
+//     the chunk partials of every group of its row with the pairwise (Chan)
+//     update over a fixed tree (every workgroup of the row gets identical
+//     statistics), builds per-channel scale and shift in LDS, then normalises,
+//     applies the affine map and the optional SiLU, 8 channels per thread.
 constexpr int GN_MAXC = 4096;
+constexpr int GN_VPT = 16;  // 16-byte vectors per thread and vector slot in gn_stats_k
+
+struct GnShape {
+  int nv, PP, nown, P;
+};
+__host__ __device__ inline GnShape gn_shape(int C) {
+  GnShape g;
+  g.nv = C / 8;
+  g.PP = g.nv <= 256 ? 256 / g.nv : 1;  // pixel phases
+  g.nown = (g.nv + 255) / 256;         // vector slots per thread (1 or 2)
+  g.P = GN_VPT * g.PP;                 // pixels per chunk
+  return g;
+}
 
 __device__ inline half8 load_vec(const GnArgs& a, int64_t pix, int c0) {
   return c0 < a.C1 ? *(const half8*)(a.src1 + pix * a.C1 + c0)
                    : *(const half8*)(a.src2 + pix * a.C2 + (c0 - a.C1));
 }
 
-__global__ void __launch_bounds__(256) gn_partial_k(GnArgs a, int nchunks) {
-  __shared__ float red[GN_MAXC];     // [phases][C] partials (phases * C <= max(2048, C))
+template <int NOWN>
+__global__ void __launch_bounds__(256) gn_stats_k(GnArgs a, int nchunks) {
+  __shared__ float red[GN_MAXC];     // [phase][C] per-thread partials (PP * C <= max(2048, C))
   __shared__ float chsum[GN_MAXC];   // per-channel sums
-  __shared__ float gsum[256];
+  __shared__ float gmean[256];
   const int row = blockIdx.x / nchunks, chunk = blockIdx.x % nchunks;
-  const int C = a.C1 + a.C2, cg = C / a.G, nv = C / 8;
-  const int p0 = chunk * GN_CHUNK;
-  const int np = min(GN_CHUNK, a.HW - p0);
+  const int C = a.C1 + a.C2, cg = C / a.G;
+  const GnShape sh = gn_shape(C);
+  const int p0 = chunk * sh.P;
+  const int np = min(sh.P, a.HW - p0);
   const int64_t pix0 = (int64_t)row * a.HW + p0;
   const int t = threadIdx.x;
-  // mapping: nv <= 256 -> PP phases of nv vectors; else each thread owns up to 2 vectors
-  const int PP = nv <= 256 ? 256 / nv : 1;
-  const int nown = nv <= 256 ? 1 : 2;
+  const int phase = sh.nv <= 256 ? t / sh.nv : 0;
+  half8 x[NOWN][GN_VPT];
+#pragma unroll
+  for (int o = 0; o < NOWN; ++o) {
+    const int v = sh.nv <= 256 ? t % sh.nv : t + 256 * o;
+#pragma unroll
+    for (int i = 0; i < GN_VPT; ++i) {
+      const int p = phase + i * sh.PP;
+      if (phase < sh.PP && v < sh.nv && p < np)
+        x[o][i] = load_vec(a, pix0 + p, v * 8);
+      else
+        x[o][i] = half8{};  // zero: adds nothing to sums, excluded from deviations below
+    }
+  }
   for (int pass = 0; pass < 2; ++pass) {
-    float acc[2][8];
+    float acc[NOWN][8];
 #pragma unroll
-    for (int o = 0; o < 2; ++o)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[o][e] = 0.f;
-    const int phase = nv <= 256 ? t / nv : 0;
-    for (int o = 0; o < nown; ++o) {
-      const int v = nv <= 256 ? t % nv : t + 256 * o;
-      if (phase >= PP || v >= nv) continue;
+    for (int o = 0; o < NOWN; ++o) {
+      const int v = sh.nv <= 256 ? t % sh.nv : t + 256 * o;
       float mu[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) mu[e] = pass ? gsum[(v * 8 + e) / cg] : 0.f;
-      for (int p = phase; p < np; p += PP) {
-        const half8 x = load_vec(a, pix0 + p, v * 8);
+      for (int e = 0; e < 8; ++e) {
+        acc[o][e] = 0.f;
+        mu[e] = (pass && v < sh.nv) ? gmean[(v * 8 + e) / cg] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < GN_VPT; ++i) {
+        const int p = phase + i * sh.PP;
+        if (p >= np) continue;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float d = (float)x[e] - mu[e];
+          const float d = (float)x[o][i][e] - mu[e];
           acc[o][e] += pass ? d * d : d;
         }
       }
     }
     __syncthreads();
-    // per-thread partials -> red[phase][channel]
-    for (int o = 0; o < nown; ++o) {
-      const int v = nv <= 256 ? t % nv : t + 256 * o;
-      if (phase < PP && v < nv)
+#pragma unroll
+    for (int o = 0; o < NOWN; ++o) {
+      const int v = sh.nv <= 256 ? t % sh.nv : t + 256 * o;
+      if (phase < sh.PP && v < sh.nv)
 #pragma unroll
         for (int e = 0; e < 8; ++e) red[phase * C + v * 8 + e] = acc[o][e];
     }
     __syncthreads();
     for (int c = t; c < C; c += 256) {
       float s = 0.f;
-      for (int ph = 0; ph < PP; ++ph) s += red[ph * C + c];
+      for (int ph = 0; ph < sh.PP; ++ph) s += red[ph * C + c];
       chsum[c] = s;
     }
     __syncthreads();
@@ -96,10 +124,10 @@ __global__ void __launch_bounds__(256) gn_partial_k(GnArgs a, int nchunks) {
       float s = 0.f;
       for (int c = 0; c < cg; ++c) s += chsum[t * cg + c];
       if (pass == 0) {
-        gsum[t] = s / (float)(np * cg);  // chunk mean of the group
+        gmean[t] = s / (float)(np * cg);  // chunk mean of the group
       } else {
         float* out = a.part + ((int64_t)(row * nchunks + chunk) * a.G + t) * 2;
-        out[0] = gsum[t];
+        out[0] = gmean[t];
         out[1] = s;
       }
     }
@@ -117,22 +145,29 @@ __device__ inline void chan_merge(double& n, double& mean, double& m2, double nb
   n = nn;
 }
 
-__global__ void __launch_bounds__(64) gn_finalize_k(GnArgs a, int nchunks) {
-  const int i = blockIdx.x;  // (row, group)
-  const int row = i / a.G, g = i % a.G, lane = threadIdx.x;
-  const int cg = (a.C1 + a.C2) / a.G;
+__global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int nchunks, int Q) {
+  __shared__ float sc[GN_MAXC], sf[GN_MAXC];  // per-channel scale and shift
+  __shared__ float gm[256], gr[256];          // per-group mean, rstd
+  const int C = a.C1 + a.C2, cg = C / a.G;
+  const GnShape sh = gn_shape(C);
+  const int qblocks = (a.HW + Q - 1) / Q;
+  const int row = blockIdx.x / qblocks, qb = blockIdx.x % qblocks;
+  const int t = threadIdx.x;
+  // 1. merge: TPG threads per group, chunks strided over them, then a fixed tree
+  const int TPG = 256 / a.G;  // G is a power of two in [4, 256]
+  const int g = t / TPG, s = t % TPG;
   double n = 0.0, mean = 0.0, m2 = 0.0;
-  for (int c = lane; c < nchunks; c += 64) {
+  for (int c = s; c < nchunks; c += TPG) {
     const float* pp = a.part + ((int64_t)(row * nchunks + c) * a.G + g) * 2;
-    chan_merge(n, mean, m2, (double)(min(GN_CHUNK, a.HW - c * GN_CHUNK) * cg), (double)pp[0],
+    chan_merge(n, mean, m2, (double)(min(sh.P, a.HW - c * sh.P) * cg), (double)pp[0],
                (double)pp[1]);
   }
-  for (int o = 1; o < 64; o <<= 1) {
+  for (int o = 1; o < TPG; o <<= 1) {
     const double nb = __shfl_xor(n, o, 64), mb = __shfl_xor(mean, o, 64),
                  m2b = __shfl_xor(m2, o, 64);
     // both partners merge (lower, upper) in the same order -> identical results
     double n1 = n, mean1 = mean, m21 = m2;
-    if (lane & o) {
+    if (s & o) {
       n1 = nb; mean1 = mb; m21 = m2b;
       chan_merge(n1, mean1, m21, n, mean, m2);
     } else {
@@ -140,33 +175,34 @@ __global__ void __launch_bounds__(64) gn_finalize_k(GnArgs a, int nchunks) {
     }
     n = n1; mean = mean1; m2 = m21;
   }
-  if (lane == 0) {
-    a.stats[2 * i] = (float)mean;
-    a.stats[2 * i + 1] = rsqrtf((float)(m2 / n) + a.eps);
+  if (s == 0) {
+    gm[g] = (float)mean;
+    gr[g] = rsqrtf((float)(m2 / n) + a.eps);
   }
-}
-
-// Normalise, affine, optional SiLU; 8 channels per thread; output [rows][HW][C].
-__global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int64_t total8) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total8) return;
-  const int C = a.C1 + a.C2, cg = C / a.G;
-  const int64_t e = i * 8;
-  const int64_t pix = e / C;
-  const int c0 = (int)(e - pix * C);
-  const int row = (int)(pix / a.HW);
-  half8 x = c0 < a.C1 ? *(const half8*)(a.src1 + pix * a.C1 + c0)
-                      : *(const half8*)(a.src2 + pix * a.C2 + (c0 - a.C1));
-  half8 y;
+  __syncthreads();
+  for (int c = t; c < C; c += 256) {
+    const int gg = c / cg;
+    const float k = gr[gg] * a.gamma[c];
+    sc[c] = k;
+    sf[c] = a.beta[c] - gm[gg] * k;
+  }
+  __syncthreads();
+  // 2. apply to pixels [qb * Q, qb * Q + Q) of this row
+  const int p0 = qb * Q, np = min(Q, a.HW - p0);
+  const int64_t pix0 = (int64_t)row * a.HW + p0;
+  for (int i = t; i < np * sh.nv; i += 256) {
+    const int p = i / sh.nv, v = i - p * sh.nv;
+    const half8 xv = load_vec(a, pix0 + p, v * 8);
+    half8 y;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int c = c0 + j, g = c / cg;
-    const float mean = a.stats[2 * (row * a.G + g)], rstd = a.stats[2 * (row * a.G + g) + 1];
-    float v = ((float)x[j] - mean) * rstd * a.gamma[c] + a.beta[c];
-    if (a.silu) v = silu(v);
-    y[j] = (_Float16)v;
+    for (int e = 0; e < 8; ++e) {
+      const int c = v * 8 + e;
+      float r = fmaf((float)xv[e], sc[c], sf[c]);
+      if (a.silu) r = silu(r);
+      y[e] = (_Float16)r;
+    }
+    *(half8*)(a.out + (pix0 + p) * C + v * 8) = y;
   }
-  *(half8*)(a.out + e) = y;
 }
 
 // One wave per token; C <= 2048, C % 8 == 0.
@@ -375,12 +411,19 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
 
 hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
   const int C = a.C1 + a.C2;
-  if (a.G < 1 || a.G > 256 || C % a.G || C % 8 || C > GN_MAXC) return hipErrorInvalidValue;
-  const int nchunks = (int)ceil_div(a.HW, GN_CHUNK);
-  hipLaunchKernelGGL(gn_partial_k, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
-  hipLaunchKernelGGL(gn_finalize_k, dim3(rows * a.G), dim3(64), 0, s, a, nchunks);
-  const int64_t total8 = (int64_t)rows * a.HW * (a.C1 + a.C2) / 8;
-  hipLaunchKernelGGL(gn_apply_k, dim3(blocks_for(total8)), dim3(256), 0, s, a, total8);
+  if (a.G < 4 || a.G > 256 || (a.G & (a.G - 1)) || C % a.G || C % 8 || C > GN_MAXC)
+    return hipErrorInvalidValue;
+  const GnShape sh = gn_shape(C);
+  const int nchunks = (int)ceil_div(a.HW, sh.P);
+  if (nchunks > a.part_chunks) return hipErrorInvalidValue;  // partial scratch too small
+  if (sh.nown == 1)
+    hipLaunchKernelGGL(gn_stats_k<1>, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
+  else
+    hipLaunchKernelGGL(gn_stats_k<2>, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
+  // about 4 vectors per thread in the apply pass
+  const int Q = std::max(1, std::min(a.HW, 1024 / sh.nv));
+  const int qblocks = (int)ceil_div(a.HW, Q);
+  hipLaunchKernelGGL(gn_apply_k, dim3(rows * qblocks), dim3(256), 0, s, a, nchunks, Q);
   return hipGetLastError();
 }
 

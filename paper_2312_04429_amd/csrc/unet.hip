@@ -276,7 +276,7 @@ struct Plan {
   std::vector<Op> step;  // one UNet evaluation
   size_t bytes = 0;
   // fixed regions
-  size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0, stats = 0;
+  size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0;
   size_t gnpart = 0, splitk = 0;
 };
 
@@ -369,8 +369,9 @@ void emit_gn(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2, con
   const auto& cfg = B.net_->cfg;
   const float* g = B.W32(n + ".g");
   const float* b = B.W32(n + ".b");
-  const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off, st = B.P->stats;
+  const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off;
   const size_t gp = B.P->gnpart;
+  const int part_chunks = (int)ceil_div(B.net_->cfg.H * B.net_->cfg.W, 8);
   const int C1 = x1.C, C2 = x2 ? x2->C : 0, HW = x1.HW, G = cfg.gn_groups;
   const float eps = cfg.gn_eps;
   const bool has2 = x2 != nullptr;
@@ -386,8 +387,8 @@ void emit_gn(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2, con
     a.gamma = g;
     a.beta = b;
     a.silu = silu;
-    a.stats = F32(c, st);
     a.part = F32(c, gp);
+    a.part_chunks = part_chunks;
     a.out = H16(c, oo);
     return gn_launch(a, c.R, c.s);
   });
@@ -640,8 +641,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
   P->pooled = B.fixed((size_t)Bs * std::max(c.pooled_dim, 1) * 4);
   P->tproj = B.fixed((size_t)Rmax * net->temb_total * 4);
   int maxG = c.gn_groups;
-  P->stats = B.fixed((size_t)Rmax * maxG * 2 * 4);
-  P->gnpart = B.fixed((size_t)Rmax * ceil_div(HW0, 32) * maxG * 2 * 4);
+  P->gnpart = B.fixed((size_t)Rmax * ceil_div(HW0, 8) * maxG * 2 * 4);
   P->splitk = B.fixed(SPLITK_BYTES);
   // per-call context K|V regions, one per transformer block
   std::map<std::string, size_t> kv_regions;
