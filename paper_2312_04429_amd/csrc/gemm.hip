@@ -41,11 +41,8 @@ constexpr uint32_t OOB = 0x80000000u;  // offset past every descriptor's range
 #ifndef GEMM_S128
 #define GEMM_S128 2
 #endif
-#ifndef GEMM_S12864
-#define GEMM_S12864 3
-#endif
 #ifndef GEMM_S64
-#define GEMM_S64 4
+#define GEMM_S64 2
 #endif
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -842,11 +839,6 @@ bool streamable(const GemmArgs& g) {
 
 template <int MODE, int BM, int BN>
 hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
-  if (streamable<MODE>(g)) {
-    if (BM == 128 && BN == 128) return launch_s<MODE, 128, 128, GEMM_S128>(g, splits, s);
-    if (BM == 128 && BN == 64) return launch_s<MODE, 128, 64, GEMM_S12864>(g, splits, s);
-    return launch_s<MODE, 64, 64, GEMM_S64>(g, splits, s);
-  }
   // the incremental single-source path needs every 64-deep tile inside one
   // source and inside K: C1 and K (dense) or C1 and Cin (conv) multiples of 64
   const bool dual = (g.C1 % BK) != 0 || (MODE == 0 && (g.K % BK) != 0) ||
@@ -855,8 +847,36 @@ hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
               : launch_t<MODE, BM, BN, false>(g, splits, s);
 }
 
+// Tile choice for the streamed kernel (measured on the UNet's shapes): at
+// these sizes a CU is fed best by several small workgroups at once (latency is
+// hidden across workgroups rather than by a deeper ring), so 64 x 64 tiles
+// with a two-deep ring are the default and K is split only while the grid is
+// small and every split keeps at least MIN_KT tiles.  Larger tiles pay off
+// when the grid is already large, or K is very long (fewer bytes per flop).
+template <int MODE>
+hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
+  constexpr int MIN_KT = 16;
+  const int nk = g.K / 64;
+  const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128);
+  const int64_t t64 = ceil_div(g.M, 64) * ceil_div(g.N, 64);
+  auto split_to = [&](int64_t tiles, int64_t target) {
+    int sp = 1;
+    if (!g.partial || (g.N & 3) != 0) return 1;
+    while (tiles * (sp + 1) <= target && nk / (sp + 1) >= MIN_KT &&
+           (size_t)(sp + 1) * g.M * g.N * 4 <= g.partial_bytes)
+      ++sp;
+    return sp;
+  };
+  if (t128 >= 512) return launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s);
+  if (t128 >= 128 && nk >= 128)
+    return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 512), s);
+  if (t64 >= 1024) return launch_s<MODE, 64, 128, 2>(g, 1, s);
+  return launch_s<MODE, 64, 64, GEMM_S64>(g, split_to(t64, 768), s);
+}
+
 template <int MODE>
 hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
+  if (streamable<MODE>(g)) return dispatch_streamed<MODE>(g, s);
   // Larger tiles move fewer bytes per flop (64, 43 and 32 flop per byte of
   // L2 traffic for 128x128, 128x64, 64x64).  At these problem sizes a
   // workgroup is bound by load latency (about one wave per SIMD), so K is
