@@ -847,15 +847,16 @@ hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
               : launch_t<MODE, BM, BN, false>(g, splits, s);
 }
 
-// Tile choice for the streamed kernel (measured on the UNet's shapes): at
-// these sizes a CU is fed best by several small workgroups at once (latency is
-// hidden across workgroups rather than by a deeper ring), so 64 x 64 tiles
-// with a two-deep ring are the default and K is split only while the grid is
-// small and every split keeps at least MIN_KT tiles.  Larger tiles pay off
-// when the grid is already large, or K is very long (fewer bytes per flop).
+// Tile choice for the streamed kernel (GPU time measured on the UNet's
+// shapes).  A workgroup here is bound by the latency of its k-tile loads
+// (about 0.4 us per tile), so small tiles and many resident workgroups win:
+// 64 x 64 tiles with a two-deep ring by default; K is split when it is long
+// (>= 40 tiles) or the grid is tiny, keeping >= MIN_KT tiles per split and
+// about 700 workgroups at most.  Large grids take 64 x 128 (wide N) or
+// 128 x 128 tiles; a long K over a mid-sized grid takes split 128 x 128.
 template <int MODE>
 hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
-  constexpr int MIN_KT = 16;
+  constexpr int MIN_KT = 10;
   const int nk = g.K / 64;
   const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128);
   const int64_t t64 = ceil_div(g.M, 64) * ceil_div(g.N, 64);
@@ -867,11 +868,13 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
       ++sp;
     return sp;
   };
-  if (t128 >= 512) return launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s);
+  if (t64 >= 1024)
+    return g.N >= 1024 ? launch_s<MODE, 64, 128, 2>(g, 1, s)
+                       : launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s);
   if (t128 >= 128 && nk >= 128)
     return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 512), s);
-  if (t64 >= 1024) return launch_s<MODE, 64, 128, 2>(g, 1, s);
-  return launch_s<MODE, 64, 64, GEMM_S64>(g, split_to(t64, 768), s);
+  const bool split = nk >= 40 || t64 < 128;
+  return launch_s<MODE, 64, 64, GEMM_S64>(g, split ? split_to(t64, 700) : 1, s);
 }
 
 template <int MODE>

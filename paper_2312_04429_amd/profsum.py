@@ -8,6 +8,7 @@ import argparse
 import sqlite3
 
 FAMILIES = [("conv3x3_igemm", "gemm_f16<1"), ("linear_gemm", "gemm_f16<0"),
+            ("conv3x3_igemm", "gemm_s<1"), ("linear_gemm", "gemm_s<0"),
             ("attention", "attn_f16"), ("cache_scan", "lk_scan"), ("splitk_reduce", "splitk_reduce"),
             ("groupnorm", "gn_"), ("layernorm", "layernorm"), ("other", "")]
 
