@@ -219,10 +219,23 @@ int32_t nv_op_conv3x3(const void* x, const void* x2, const void* w, const float*
                       int32_t stride, int32_t upsample, void* workspace, size_t workspace_bytes,
                       void* stream);
 
+/* nv_op_attention: multi-head softmax(q k^T * scale) v per row, float16 in and
+ * out, float32 softmax (Sec. 2.1: the UNet's self- and cross-attention).
+ *   q [rows][S][ldq] and k [rows][L][ldk] with head h in columns
+ *   [h*dh, (h+1)*dh); v given TRANSPOSED: channel c of key j of row r at
+ *   vt[c * vt_ld + r * vt_row + j], with vt_row >= L, vt_row % 8 == 0 and
+ *   vt_ld >= rows * vt_row, vt_ld % 8 == 0 (keys L..vt_row-1 are never used);
+ *   out [rows][S][ldo].  dh in {16, 32, 40, 64, 80, 128, 160}; ldq, ldk, ldo
+ *   % 8 == 0.  No workspace. */
+int32_t nv_op_attention(const void* q, const void* k, const void* vt, void* out, int32_t rows,
+                        int32_t S, int32_t L, int32_t heads, int32_t dh, int32_t ldq, int32_t ldk,
+                        int32_t ldo, int64_t vt_ld, int64_t vt_row, float scale, void* stream);
+
 /* ------------------------------------------------------------------------ *
- * Launch tracing for measurement.  While enabled, the library records a
- * pair of HIP events on the launch stream around every kernel launch of the
- * families in family_mask (the first max_launches launches are kept); each
+ * Launch tracing for measurement.  While enabled, every kernel launch of the
+ * families in family_mask carries a pair of HIP events that the dispatch
+ * timestamps at the kernel's start and end (the first max_launches launches
+ * are kept), i.e. the kernel's execution time alone; each
  * record carries the launch's algorithmic FLOPs (2 M N K for matrix
  * products) and bytes.  nv_trace_read waits for the recorded events and
  * returns the sums over the launches of `family` (a mask).  Enabling again

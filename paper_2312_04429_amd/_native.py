@@ -59,6 +59,8 @@ _sigs = {
     "nv_op_linear": (I32, [VP, VP, VP, VP, VP, VP, I64, I32, I32, I32, VP, SZ, VP]),
     "nv_op_conv3x3": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, I32, VP, SZ,
                             VP]),
+    "nv_op_attention": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, I32, I64, I64,
+                              F32, VP]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(lib, _name)

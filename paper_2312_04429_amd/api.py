@@ -211,6 +211,23 @@ def nv_op_conv3x3(x, w, bias=None, stride=1, upsample=False, out=None, x2=None):
     N.check(st, "nv_op_conv3x3")
     return out
 
+def nv_op_attention(q, k, vt, heads, scale, L=None, vt_row=None, out=None):
+    """Multi-head attention of q [rows][S][C] over keys k [rows][L][C] and values
+    given transposed, vt [C][rows * vt_row] (key j of row r in column r * vt_row + j);
+    float16 in and out."""
+    _need_cuda(q, k, vt)
+    rows, S, C = q.shape
+    L = k.shape[1] if L is None else L
+    vt_row = vt.shape[1] // rows if vt_row is None else vt_row
+    if out is None:
+        out = torch.empty((rows, S, C), dtype=torch.float16, device=q.device)
+    st = N.lib.nv_op_attention(_p(q), _p(k), _p(vt), _p(out), rows, S, L, heads, C // heads,
+                               q.stride(1), k.stride(1), out.stride(1), vt.stride(0), vt_row,
+                               float(scale), _stream())
+    N.check(st, "nv_op_attention")
+    return out
+
+
 def nv_trace_enable(family_mask, max_launches=65536):
     N.check(N.lib.nv_trace_enable(family_mask, max_launches), "nv_trace_enable")
 

@@ -7,11 +7,12 @@
 namespace nv {
 
 struct AttnArgs {
-  const _Float16* q;  // [rows][S][ldq], head h at column h*dh
-  const _Float16* k;  // [rows][L][ldk]
-  const _Float16* v;  // [rows][L][ldv]
-  _Float16* o;        // [rows][S][ldo]
-  int ldq, ldk, ldv, ldo;
+  const _Float16* q;   // [rows][S][ldq], head h at column h*dh
+  const _Float16* k;   // [rows][L][ldk]
+  const _Float16* vt;  // V transposed: element (row, key j, channel c) at c*vt_ld + row*vt_row + j
+  _Float16* o;         // [rows][S][ldo]
+  int ldq, ldk, ldo;
+  int64_t vt_ld, vt_row;  // vt_row >= L, vt_row % 8 == 0; keys in [L, vt_row) are never used
   int rows, S, L, heads, dh;
   float scale;
 };

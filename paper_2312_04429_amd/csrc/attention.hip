@@ -12,7 +12,9 @@
 // output rescale are per-lane scalars, and the probabilities P^T are already
 // in the B-operand layout of O^T = V^T P^T (the 8 keys a lane contributes to
 // one 32-key MFMA step are the 2 x 4 keys it holds; V^T supplies the same 8
-// keys for its row d).
+// keys for its row d).  V arrives transposed from its projection, so both
+// tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps
+// (dims past d read as zero) plus, for d % 32 == 16, one 16-wide step.
 #include "common.h"
 #include "attention.h"
 #include "trace.h"
@@ -22,18 +24,24 @@ namespace {
 
 constexpr int QB = 2;    // 16-query column blocks per wave
 constexpr int KB = 64;   // keys per block
+constexpr int VROW = KB + 8;  // halfs per LDS V^T row
 constexpr float LOG2E = 1.4426950408889634f;
 
-template <int DP, int DV>
+template <int DH>
 __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
-  constexpr int KROW = DP + 8;          // halfs per LDS key row (16-byte slots 4k+1 apart)
-  constexpr int VROW = KB + 8;          // halfs per LDS V^T row
-  constexpr int KCH = KB * (DP / 8);    // 16-byte chunks of a K block
-  constexpr int VCH = KB * (DV / 8);
-  constexpr int KPT = (KCH + 255) / 256;  // chunks per thread
-  constexpr int VPT = (VCH + 255) / 256;
+  // 32-wide head-dim steps (a remainder of 8 runs as a zero-masked 32-wide
+  // step), then one 16-wide step for a remainder of 16
+  constexpr int N32 = DH % 32 == 8 ? DH / 32 + 1 : DH / 32;
+  constexpr int REM = DH % 32 == 8 ? 0 : DH % 32;
+  constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
+  constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
+  constexpr int KST = KCH % 2 ? KCH : KCH + 1; // odd chunk stride: conflict-free row reads
+  constexpr int KROW = KST * 8;                // halfs per LDS key row
+  constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
+  constexpr int KPT = (KCN + 255) / 256, VPT = (VCN + 255) / 256;
+  static_assert(DH % 8 == 0 && (REM == 0 || REM == 16), "head dim");
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                      // [2]
+  _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                       // [2]
   _Float16 (*sVt)[DV * VROW] = (_Float16 (*)[DV * VROW])(smem + 2 * KB * KROW * 2);  // [2]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -43,23 +51,21 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   const int nqb = (a.S + 64 * QB - 1) / (64 * QB);
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int qblk = id % nqb, head = (id / nqb) % a.heads, row = id / (nqb * a.heads);
-  const int dh = a.dh;
   const int q0 = qblk * (64 * QB) + wave * (16 * QB);
 
-  // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8.
-  half8 fq[QB][DP / 32];
+  // Q^T fragments (B operand): query q0 + qb*16 + li; 32-wide steps take dims
+  // ks*32 + kc*8 .. +8, the 16-wide step dims N32*32 + kc*4 .. +4; zero past DH.
+  half8 fq[QB][N32 > 0 ? N32 : 1];
+  half4 fq16[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int q = q0 + qb * 16 + li;
-    const _Float16* qrow = a.q + ((int64_t)row * a.S + (q < a.S ? q : 0)) * a.ldq + head * dh;
+    const _Float16* qrow = a.q + ((int64_t)row * a.S + (q < a.S ? q : 0)) * a.ldq + head * DH;
 #pragma unroll
-    for (int ks = 0; ks < DP / 32; ++ks) {
-      const int d0 = ks * 32 + kc * 8;
-      if (q < a.S && d0 < dh)
-        fq[qb][ks] = *(const half8*)(qrow + d0);
-      else
-        fq[qb][ks] = half8{0, 0, 0, 0, 0, 0, 0, 0};
-    }
+    for (int ks = 0; ks < N32; ++ks)
+      fq[qb][ks] = (q < a.S && ks * 32 + kc * 8 < DH) ? *(const half8*)(qrow + ks * 32 + kc * 8) : half8{};
+    fq16[qb] = half4{};
+    if (REM && q < a.S && N32 * 32 + kc * 4 < DH) fq16[qb] = *(const half4*)(qrow + N32 * 32 + kc * 4);
   }
 
   floatx4 acc[QB][DV / 16];
@@ -75,8 +81,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
   const float sc = a.scale * LOG2E;
 
-  const _Float16* kbase = a.k + (int64_t)row * a.L * a.ldk + head * dh;
-  const _Float16* vbase = a.v + (int64_t)row * a.L * a.ldv + head * dh;
+  const _Float16* kbase = a.k + (int64_t)row * a.L * a.ldk + head * DH;
+  const _Float16* vtbase = a.vt + (int64_t)head * DH * a.vt_ld + (int64_t)row * a.vt_row;
   const int nkb = (a.L + KB - 1) / KB;
 
   uint4 rk[KPT], rv[VPT];
@@ -84,43 +90,43 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * 256;
-      const int kr = c / (DP / 8), d0 = (c % (DP / 8)) * 8;
+      const int kr = c / KCH, ch = c % KCH;
       const int j = kb * KB + kr;
-      rk[i] = (c < KCH && j < a.L && d0 < dh) ? *(const uint4*)(kbase + (int64_t)j * a.ldk + d0)
-                                             : make_uint4(0, 0, 0, 0);
+      rk[i] = (c < KCN && j < a.L) ? *(const uint4*)(kbase + (int64_t)j * a.ldk + ch * 8)
+                                   : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + i * 256;
-      const int kr = c / (DV / 8), d0 = (c % (DV / 8)) * 8;
-      const int j = kb * KB + kr;
-      rv[i] = (c < VCH && j < a.L && d0 < dh) ? *(const uint4*)(vbase + (int64_t)j * a.ldv + d0)
-                                             : make_uint4(0, 0, 0, 0);
+      const int d = c / (KB / 8), j0 = kb * KB + (c % (KB / 8)) * 8;
+      rv[i] = (c < VCN && j0 < a.L) ? *(const uint4*)(vtbase + (int64_t)d * a.vt_ld + j0)
+                                    : make_uint4(0, 0, 0, 0);
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, int kb) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * 256;
-      if (c < KCH) {
-        const int kr = c / (DP / 8), d0 = (c % (DP / 8)) * 8;
-        *(uint4*)&sK[buf][kr * KROW + d0] = rk[i];
-      }
+      if (c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + i * 256;
-      if (c < VCH) {
-        const int kr = c / (DV / 8), d0 = (c % (DV / 8)) * 8;
-        const half8 v = *(const half8*)&rv[i];
+      if (c < VCN) {
+        const int d = c / (KB / 8), k8 = (c % (KB / 8)) * 8;
+        half8 v = *(const half8*)&rv[i];
+        const int past = kb * KB + k8 + 8 - a.L;  // keys of this chunk at or past L
+        if (past > 0)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sVt[buf][(d0 + e) * VROW + kr] = v[e];
+          for (int e = 0; e < 8; ++e)
+            if (e >= 8 - past) v[e] = (_Float16)0.0f;
+        *(half8*)&sVt[buf][d * VROW + k8] = v;
       }
     }
   };
 
   fetch(0);
-  stash(0);
+  stash(0, 0);
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
     const int cur = kb & 1;
@@ -132,16 +138,19 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     floatx4 s[QB][4];
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      half8 fk[DP / 32];
+      const _Float16* kr = &K_[(h * 16 + li) * KROW];
+      half8 fk[N32 > 0 ? N32 : 1];
 #pragma unroll
-      for (int ks = 0; ks < DP / 32; ++ks)
-        fk[ks] = *(const half8*)&K_[(h * 16 + li) * KROW + ks * 32 + kc * 8];
+      for (int ks = 0; ks < N32; ++ks) fk[ks] = ks * 32 + kc * 8 < DH ? *(const half8*)(kr + ks * 32 + kc * 8) : half8{};
+      half4 fk16 = half4{};
+      if (REM && N32 * 32 + kc * 4 < DH) fk16 = *(const half4*)(kr + N32 * 32 + kc * 4);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         s[qb][h] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < DP / 32; ++ks)
+        for (int ks = 0; ks < N32; ++ks)
           s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
+        if (REM) s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x16f16(fk16, fq16[qb], s[qb][h], 0, 0, 0);
       }
     }
     const bool tail = (kb + 1) * KB > a.L;
@@ -176,7 +185,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
     }
-    // O^T += V^T P^T over two 32-key steps
+    // O^T += V^T P^T over two 32-key steps (rows d >= DH of the tile are never
+    // written; they only feed output rows that are not stored)
 #pragma unroll
     for (int j = 0; j < DV / 16; ++j) {
 #pragma unroll
@@ -192,7 +202,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
           acc[qb][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp[qb][st], acc[qb][j], 0, 0, 0);
       }
     }
-    if (more) stash(cur ^ 1);
+    if (more) stash(cur ^ 1, kb + 1);
     __syncthreads();
   }
 #pragma unroll
@@ -203,11 +213,11 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     const int q = q0 + qb * 16 + li;
     if (q >= a.S) continue;
     const float inv = 1.0f / l;
-    _Float16* orow = a.o + ((int64_t)row * a.S + q) * a.ldo + head * dh;
+    _Float16* orow = a.o + ((int64_t)row * a.S + q) * a.ldo + head * DH;
 #pragma unroll
     for (int j = 0; j < DV / 16; ++j) {
       const int d0 = j * 16 + kc * 4;
-      if (d0 < dh) {
+      if (d0 < DH) {
         half4 o;
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[r] = (_Float16)(acc[qb][j][r] * inv);
@@ -217,22 +227,24 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
 }
 
-template <int DP, int DV>
+template <int DH>
 hipError_t launch(const AttnArgs& a, hipStream_t s) {
-  const size_t lds = (size_t)2 * (KB * (DP + 8) + DV * (KB + 8)) * 2;
+  constexpr int KCH = DH / 8, KST = KCH % 2 ? KCH : KCH + 1, DV = (DH + 15) / 16 * 16;
+  const size_t lds = (size_t)2 * (KB * KST * 8 + DV * VROW) * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DP, DV>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
+  if (a.vt_row < a.L || a.vt_row % 8 || a.vt_ld % 8 || a.vt_ld < (int64_t)a.rows * a.vt_row)
+    return hipErrorInvalidValue;
   dim3 grid((unsigned)(ceil_div(a.S, 64 * QB) * a.heads * a.rows));
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
-  trace_pre(NV_FAM_ATTN, flops, bytes, s);
-  hipLaunchKernelGGL((attn_f16<DP, DV>), grid, dim3(256), lds, s, a);
-  trace_post(NV_FAM_ATTN, s);
+  const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes);
+  hipExtLaunchKernelGGL((attn_f16<DH>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u, a);
   return hipGetLastError();
 }
 
@@ -241,13 +253,13 @@ hipError_t launch(const AttnArgs& a, hipStream_t s) {
 hipError_t attn_launch(const AttnArgs& a, hipStream_t s) {
   // head dims: 16 (tiny), 40 / 80 / 160 (SD-1.5 levels), 64 (SDXL)
   switch (a.dh) {
-    case 16: return launch<32, 16>(a, s);
-    case 32: return launch<32, 32>(a, s);
-    case 40: return launch<64, 48>(a, s);
-    case 64: return launch<64, 64>(a, s);
-    case 80: return launch<96, 80>(a, s);
-    case 128: return launch<128, 128>(a, s);
-    case 160: return launch<160, 160>(a, s);
+    case 16: return launch<16>(a, s);
+    case 32: return launch<32>(a, s);
+    case 40: return launch<40>(a, s);
+    case 64: return launch<64>(a, s);
+    case 80: return launch<80>(a, s);
+    case 128: return launch<128>(a, s);
+    case 160: return launch<160>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

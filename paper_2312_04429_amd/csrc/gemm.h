@@ -31,6 +31,12 @@ struct GemmArgs {
   void* out;
   int ldo;
   int out_f32;
+  // columns n >= vt_col0 go transposed to vt instead of out:
+  // vt[(n - vt_col0) * vt_ld + (m / vt_div) * vt_stride + m % vt_div]
+  _Float16* vt;
+  int vt_col0;
+  int64_t vt_ld;
+  int64_t vt_div, vt_stride;
   // split-K scratch (float32 partials), optional
   float* partial;
   size_t partial_bytes;

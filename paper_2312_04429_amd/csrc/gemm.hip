@@ -77,6 +77,12 @@ __device__ inline void store_out4(const GemmArgs& g, int64_t m, int n, float (&v
   if (g.silu)
 #pragma unroll
     for (int r = 0; r < 4; ++r) v[r] = silu(v[r]);
+  if (g.vt && n >= g.vt_col0) {  // transposed columns (no residual on these)
+    _Float16* o = g.vt + (int64_t)(n - g.vt_col0) * g.vt_ld + (m / g.vt_div) * g.vt_stride +
+                  m % g.vt_div;
+    for (int r = 0; r < nn; ++r) o[(int64_t)r * g.vt_ld] = (_Float16)v[r];
+    return;
+  }
   if (g.residual) {
     const _Float16* rp = g.residual + m * g.ld_res + n;
     if (vec) {
@@ -790,9 +796,9 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   const double flops = 2.0 * (double)g.M * g.N * g.K;
   const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
-  trace_pre(fam, flops, bytes, s);
-  hipLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), lds, s, g, kps);
-  trace_post(fam, s);
+  const TraceEv ev = trace_begin(fam, flops, bytes);
+  hipExtLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), (uint32_t)lds, s, ev.a,
+                        ev.b, 0u, g, kps);
   if (splits > 1) {
     const int64_t total = g.M * (int64_t)(g.N / 4);
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
@@ -819,9 +825,9 @@ hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
   const double flops = 2.0 * (double)g.M * g.N * g.K;
   const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
-  trace_pre(fam, flops, bytes, s);
-  hipLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES>), grid, dim3(256), lds, s, g, kps);
-  trace_post(fam, s);
+  const TraceEv ev = trace_begin(fam, flops, bytes);
+  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES>), grid, dim3(256), (uint32_t)lds, s, ev.a,
+                        ev.b, 0u, g, kps);
   if (splits > 1) {
     const int64_t total = g.M * (int64_t)(g.N / 4);
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);

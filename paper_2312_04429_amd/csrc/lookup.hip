@@ -643,25 +643,22 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
           (size_t)3 * QB * 8 + (size_t)2 * QB * d * 2 + (size_t)2 * QB * SS_RR * 4 + RR_TILE * 4;
       NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
-      hipLaunchKernelGGL(lk_scan_bf16, dim3(T), dim3(256), lds, s, (const uint16_t*)cache, n, d,
-                         m, T, ws);
-      trace_post(NV_FAM_SCAN, s);
+      const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d);
+      hipExtLaunchKernelGGL(lk_scan_bf16, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
+                            (const uint16_t*)cache, n, (int)d, (int)m, T, ws);
       NV_LAUNCH_CHECK("lk_scan_bf16");
     } else if (bf) {
       const size_t lds = (size_t)QB * d * 2 + (size_t)2 * QB * SS_WIDE * 4 + TILE * 4;
       NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16_wide,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d, s);
-      hipLaunchKernelGGL(lk_scan_bf16_wide, dim3(T), dim3(256), lds, s, (const uint16_t*)cache, n, d, m,
-                         T, ws);
-      trace_post(NV_FAM_SCAN, s);
+      const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d);
+      hipExtLaunchKernelGGL(lk_scan_bf16_wide, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b,
+                            0u, (const uint16_t*)cache, n, (int)d, (int)m, T, ws);
       NV_LAUNCH_CHECK("lk_scan_bf16_wide");
     } else {
-      trace_pre(NV_FAM_SCAN, 2.0 * m * (double)n * d, 4.0 * (double)n * d, s);
-      hipLaunchKernelGGL(lk_scan_f32, dim3(T), dim3(256), 0, s, (const float*)cache, n, d,
-                         queries, m, T, ws);
-      trace_post(NV_FAM_SCAN, s);
+      const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 4.0 * (double)n * d);
+      hipExtLaunchKernelGGL(lk_scan_f32, dim3(T), dim3(256), 0u, s, ev.a, ev.b, 0u,
+                            (const float*)cache, n, (int)d, queries, (int)m, T, ws);
       NV_LAUNCH_CHECK("lk_scan_f32");
     }
   }

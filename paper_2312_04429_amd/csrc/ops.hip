@@ -145,6 +145,8 @@ __device__ inline void chan_merge(double& n, double& mean, double& m2, double nb
   n = nn;
 }
 
+constexpr int GN_APT = 4;  // 16-byte vectors per thread in gn_apply_k (Q * nv <= 1024)
+
 __global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int nchunks, int Q) {
   __shared__ float sc[GN_MAXC], sf[GN_MAXC];  // per-channel scale and shift
   __shared__ float gm[256], gr[256];          // per-group mean, rstd
@@ -153,6 +155,26 @@ __global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int nchunks, int Q) 
   const int qblocks = (a.HW + Q - 1) / Q;
   const int row = blockIdx.x / qblocks, qb = blockIdx.x % qblocks;
   const int t = threadIdx.x;
+  // 0. issue this thread's input vectors first: their latency overlaps the merge
+  const int p0 = qb * Q, np = min(Q, a.HW - p0);
+  const int64_t pix0 = (int64_t)row * a.HW + p0;
+  half8 xv[GN_APT];
+#pragma unroll
+  for (int j = 0; j < GN_APT; ++j) {
+    const int i = t + j * 256;
+    if (i < np * sh.nv) {
+      const int p = i / sh.nv, v = i - p * sh.nv;
+      xv[j] = load_vec(a, pix0 + p, v * 8);
+    }
+  }
+  // and the affine parameters of the channels this thread tabulates
+  float gam[GN_MAXC / 256], bet[GN_MAXC / 256];
+#pragma unroll
+  for (int j = 0; j < GN_MAXC / 256; ++j) {
+    const int c = t + j * 256;
+    gam[j] = c < C ? a.gamma[c] : 0.f;
+    bet[j] = c < C ? a.beta[c] : 0.f;
+  }
   // 1. merge: TPG threads per group, chunks strided over them, then a fixed tree
   const int TPG = 256 / a.G;  // G is a power of two in [4, 256]
   const int g = t / TPG, s = t % TPG;
@@ -180,24 +202,28 @@ __global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int nchunks, int Q) 
     gr[g] = rsqrtf((float)(m2 / n) + a.eps);
   }
   __syncthreads();
-  for (int c = t; c < C; c += 256) {
-    const int gg = c / cg;
-    const float k = gr[gg] * a.gamma[c];
-    sc[c] = k;
-    sf[c] = a.beta[c] - gm[gg] * k;
+#pragma unroll
+  for (int j = 0; j < GN_MAXC / 256; ++j) {
+    const int c = t + j * 256;
+    if (c < C) {
+      const int gg = c / cg;
+      const float k = gr[gg] * gam[j];
+      sc[c] = k;
+      sf[c] = bet[j] - gm[gg] * k;
+    }
   }
   __syncthreads();
   // 2. apply to pixels [qb * Q, qb * Q + Q) of this row
-  const int p0 = qb * Q, np = min(Q, a.HW - p0);
-  const int64_t pix0 = (int64_t)row * a.HW + p0;
-  for (int i = t; i < np * sh.nv; i += 256) {
+#pragma unroll
+  for (int j = 0; j < GN_APT; ++j) {
+    const int i = t + j * 256;
+    if (i >= np * sh.nv) continue;
     const int p = i / sh.nv, v = i - p * sh.nv;
-    const half8 xv = load_vec(a, pix0 + p, v * 8);
     half8 y;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int c = v * 8 + e;
-      float r = fmaf((float)xv[e], sc[c], sf[c]);
+      float r = fmaf((float)xv[j][e], sc[c], sf[c]);
       if (a.silu) r = silu(r);
       y[e] = (_Float16)r;
     }
@@ -420,8 +446,8 @@ hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
     hipLaunchKernelGGL(gn_stats_k<1>, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
   else
     hipLaunchKernelGGL(gn_stats_k<2>, dim3(rows * nchunks), dim3(256), 0, s, a, nchunks);
-  // about 4 vectors per thread in the apply pass
-  const int Q = std::max(1, std::min(a.HW, 1024 / sh.nv));
+  // at most GN_APT vectors per thread in the apply pass
+  const int Q = std::max(1, std::min(a.HW, GN_APT * 256 / sh.nv));
   const int qblocks = (int)ceil_div(a.HW, Q);
   hipLaunchKernelGGL(gn_apply_k, dim3(rows * qblocks), dim3(256), 0, s, a, nchunks, Q);
   return hipGetLastError();

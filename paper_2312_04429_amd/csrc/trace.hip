@@ -1,5 +1,6 @@
-// Launch tracing for measurement: HIP events recorded on the launch stream
-// around every kernel launch of the selected families, summed on read.
+// Launch tracing for measurement: for every kernel launch of the selected
+// families, a pair of HIP events that the dispatch timestamps at the kernel's
+// start and end (hipExtLaunchKernel), summed on read.
 #include <mutex>
 #include <vector>
 
@@ -21,27 +22,20 @@ struct Tracer {
   size_t cap = 0;
   std::vector<hipEvent_t> pool;
   std::vector<Rec> recs;
-  Rec* open = nullptr;
 } T;
 
 }  // namespace
 
-void trace_pre(int family, double flops, double bytes, hipStream_t s) {
-  if (!(T.mask & family)) return;
+TraceEv trace_begin(int family, double flops, double bytes) {
+  TraceEv ev;
+  if (!(T.mask & family)) return ev;
   std::lock_guard<std::mutex> lk(T.mu);
-  if (T.recs.size() >= T.cap) return;
+  if (T.recs.size() >= T.cap) return ev;
   Rec r{T.pool[2 * T.recs.size()], T.pool[2 * T.recs.size() + 1], family, flops, bytes};
-  (void)hipEventRecord(r.a, s);
   T.recs.push_back(r);
-  T.open = &T.recs.back();
-}
-
-void trace_post(int family, hipStream_t s) {
-  if (!(T.mask & family)) return;
-  std::lock_guard<std::mutex> lk(T.mu);
-  if (!T.open || T.open->family != family) return;
-  (void)hipEventRecord(T.open->b, s);
-  T.open = nullptr;
+  ev.a = r.a;
+  ev.b = r.b;
+  return ev;
 }
 
 }  // namespace nv
@@ -56,7 +50,6 @@ extern "C" int32_t nv_trace_enable(int32_t family_mask, int32_t max_launches) {
   for (auto e : T.pool) (void)hipEventDestroy(e);
   T.pool.clear();
   T.recs.clear();
-  T.open = nullptr;
   T.pool.resize(2 * (size_t)max_launches);
   for (auto& e : T.pool) NV_HIP_TRY(hipEventCreate(&e));
   T.recs.reserve(max_launches);

@@ -533,20 +533,43 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
         return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
       });
     }
-    Ten qkv = B.alloc(HW, 3 * C);
-    emit_linear(B, ops, t, nullptr, B.W16(b + ".attn1.qkv.w"), nullptr, 3 * C, qkv, nullptr);
+    // Q|K as token rows, V written transposed (channel rows, Rmax*HW tokens
+    // each) so the attention kernel reads both K and V^T tiles as rows
+    Ten qk = B.alloc(HW, 2 * C);
+    Ten vt = B.alloc(HW, C);
+    {
+      const _Float16* w = B.W16(b + ".attn1.qkv.w");
+      const size_t xi = t.off, qko = qk.off, vto = vt.off;
+      const int64_t vld = (int64_t)B.Rmax_ * HW;
+      ops.push_back([=](const RunCtx& c) {
+        GemmArgs g = dense_args(3 * C, C, w, nullptr);
+        g.M = (int64_t)c.R * HW;
+        g.src1 = H16(c, xi);
+        g.out = H16(c, qko);
+        g.ldo = 2 * C;
+        g.vt = H16(c, vto);
+        g.vt_col0 = 2 * C;
+        g.vt_ld = vld;
+        g.vt_div = HW;
+        g.vt_stride = HW;
+        return gemm_run(g, c);
+      });
+    }
     B.drop(t);
     Ten a = B.alloc(HW, C);
     {
-      const size_t qo = qkv.off, ao = a.off;
+      const size_t qo = qk.off, vto = vt.off, ao = a.off;
+      const int64_t vld = (int64_t)B.Rmax_ * HW;
       ops.push_back([=](const RunCtx& c) {
         AttnArgs at{};
         at.q = H16(c, qo);
         at.k = H16(c, qo) + C;
-        at.v = H16(c, qo) + 2 * C;
+        at.vt = H16(c, vto);
         at.o = H16(c, ao);
-        at.ldq = at.ldk = at.ldv = 3 * C;
+        at.ldq = at.ldk = 2 * C;
         at.ldo = C;
+        at.vt_ld = vld;
+        at.vt_row = HW;
         at.rows = c.R;
         at.S = HW;
         at.L = HW;
@@ -556,7 +579,8 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
         return attn_launch(at, c.s);
       });
     }
-    B.drop(qkv);
+    B.drop(qk);
+    B.drop(vt);
     emit_linear(B, ops, a, nullptr, B.W16(b + ".attn1.o.w"), B.W32(b + ".attn1.o.b"), C, h, &h);
     B.drop(a);
     // cross-attention
@@ -576,18 +600,23 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
     // context K|V of this block: computed once per call into a region reserved
     // before any per-step buffer, so no step op can overwrite it
     const size_t kvoff = kv_regions.at(b);
+    const int Lp = (Lc + 7) / 8 * 8;
+    const size_t vtoff = kvoff + align_up((size_t)B.Rmax_ * Lc * C * 2, 256);
     a = B.alloc(HW, C);
     {
       const size_t qo = qc.off, ao = a.off;
+      const int64_t vld = (int64_t)B.Rmax_ * Lp;
       ops.push_back([=](const RunCtx& c) {
         AttnArgs at{};
         at.q = H16(c, qo);
         at.k = H16(c, kvoff);
-        at.v = H16(c, kvoff) + C;
+        at.vt = H16(c, vtoff);
         at.o = H16(c, ao);
         at.ldq = C;
-        at.ldk = at.ldv = 2 * C;
+        at.ldk = C;
         at.ldo = C;
+        at.vt_ld = vld;
+        at.vt_row = Lp;
         at.rows = c.R;
         at.S = HW;
         at.L = Lc;
@@ -652,7 +681,10 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
     if (n.size() > suf.size() && n.compare(n.size() - suf.size(), suf.size(), suf) == 0) {
       const std::string b = n.substr(0, n.size() - suf.size());
       kv_width[b] = (int)p.shape[0];
-      kv_regions[b] = B.fixed((size_t)Rmax * c.ctx_len * 2 * p.shape[0] * 2);
+      // K rows [Rmax * Lc][C], then V^T [C][Rmax * Lp] (Lp = Lc rounded up to 8)
+      const size_t Lp = (c.ctx_len + 7) / 8 * 8;
+      kv_regions[b] = B.fixed(align_up((size_t)Rmax * c.ctx_len * p.shape[0] * 2, 256) +
+                              (size_t)p.shape[0] * Rmax * Lp * 2);
     }
   }
   auto& ops = P->step;
@@ -817,12 +849,19 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
     const _Float16* w = B.W16(b + ".attn2.kv.w");
     const int Lc = c.ctx_len, D = c.ctx_dim;
     const int C = kv_width.at(b);
+    const int Lp = (Lc + 7) / 8 * 8;
+    const size_t vtoff = kvoff + align_up((size_t)Rmax * Lc * C * 2, 256);
     P->pre.push_back([=](const RunCtx& x) {
       GemmArgs g = dense_args(2 * C, D, w, nullptr);
       g.M = (int64_t)x.R * Lc;
       g.src1 = H16(x, ctxo);
       g.out = x.ws + kvoff;
-      g.ldo = 2 * C;
+      g.ldo = C;
+      g.vt = H16(x, vtoff);
+      g.vt_col0 = C;
+      g.vt_ld = (int64_t)Rmax * Lp;
+      g.vt_div = Lc;
+      g.vt_stride = Lp;
       return gemm_run(g, x);
     });
   }
@@ -1269,5 +1308,42 @@ extern "C" int32_t nv_op_conv3x3(const void* x, const void* x2, const void* w, c
   g.partial = (float*)workspace;
   g.partial_bytes = workspace_bytes;
   NV_HIP_TRY(gemm_launch(g, (hipStream_t)stream));
+  return NV_OK;
+}
+
+extern "C" int32_t nv_op_attention(const void* q, const void* k, const void* vt, void* out,
+                                   int32_t rows, int32_t S, int32_t L, int32_t heads, int32_t dh,
+                                   int32_t ldq, int32_t ldk, int32_t ldo, int64_t vt_ld,
+                                   int64_t vt_row, float scale, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(q && k && vt && out, "null pointer argument");
+  NV_CHECK_ARG(rows >= 1 && S >= 1 && L >= 1 && heads >= 1, "sizes must be >= 1");
+  NV_CHECK_ARG(ldq >= heads * dh && ldk >= heads * dh && ldo >= heads * dh,
+               "row strides smaller than heads * dh");
+  NV_CHECK_ARG(ldq % 8 == 0 && ldk % 8 == 0 && ldo % 8 == 0, "row strides must be multiples of 8");
+  NV_CHECK_ARG(vt_row >= L && vt_row % 8 == 0 && vt_ld % 8 == 0 && vt_ld >= rows * vt_row,
+               "bad transposed-V layout");
+  NV_CHECK_ARG(std::isfinite(scale), "scale must be finite");
+  if (!attn_supported(dh)) {
+    set_error("head dim must be one of 16, 32, 40, 64, 80, 128, 160");
+    return NV_ERR_UNSUPPORTED;
+  }
+  AttnArgs a{};
+  a.q = (const _Float16*)q;
+  a.k = (const _Float16*)k;
+  a.vt = (const _Float16*)vt;
+  a.o = (_Float16*)out;
+  a.ldq = ldq;
+  a.ldk = ldk;
+  a.ldo = ldo;
+  a.vt_ld = vt_ld;
+  a.vt_row = vt_row;
+  a.rows = rows;
+  a.S = S;
+  a.L = L;
+  a.heads = heads;
+  a.dh = dh;
+  a.scale = scale;
+  NV_HIP_TRY(attn_launch(a, (hipStream_t)stream));
   return NV_OK;
 }
