@@ -16,10 +16,10 @@ import json
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-FAMS = {"conv3x3_igemm": ("gemm_f16<1", ["gemm.hip", "gemm.h"]),
-        "linear_gemm": ("gemm_f16<0", ["gemm.hip", "gemm.h"]),
-        "attention": ("attn_f16", ["attention.hip"]),
-        "cache_scan": ("lk_scan", ["lookup.hip"])}
+FAMS = {"conv3x3_igemm": (("gemm_f16<1", "gemm_s<1"), ["gemm.hip", "gemm.h"]),
+        "linear_gemm": (("gemm_f16<0", "gemm_s<0"), ["gemm.hip", "gemm.h"]),
+        "attention": (("attn_f16",), ["attention.hip"]),
+        "cache_scan": (("lk_scan",), ["lookup.hip"])}
 CALIB_BYTES = float(1 << 30)
 
 
@@ -55,9 +55,9 @@ def main():
         raise SystemExit("calibration dispatch not found")
     kib_f = max(cf) * 1024.0 / CALIB_BYTES   # counter bytes per true byte
     kib_w = max(cw) * 1024.0 / CALIB_BYTES
-    for fam, (key, files) in FAMS.items():
-        f = [v for (d, n), v in fetch.items() if key in n]
-        w = [v for (d, n), v in write.items() if key in n]
+    for fam, (keys, files) in FAMS.items():
+        f = [v for (d, n), v in fetch.items() if any(k in n for k in keys)]
+        w = [v for (d, n), v in write.items() if any(k in n for k in keys)]
         if not f or not w:
             continue
         fb = sum(f) / len(f) * 1024.0 / kib_f
