@@ -4,17 +4,17 @@
 // conditioning enters the UNet through cross-attention).
 //
 // Work split: one workgroup = 128 queries of one (row, head); each wave owns
-// 32 queries (two 16-query column blocks).  Keys stream in blocks of 64:
-// the next block is fetched into registers while the current one is used
-// from LDS (double buffer, one barrier per block).  The kernel computes the
+// 32 queries (two 16-query column blocks).  Keys stream in blocks of 64
+// through two register sets (fetched two blocks ahead) and a double-buffered
+// LDS, one barrier per block.  The kernel computes the
 // transposed score block S^T = K Q^T so that every accumulator entry of a
 // lane belongs to one query (column l % 16): the running max / sum and the
 // output rescale are per-lane scalars, and the probabilities P^T are already
 // in the B-operand layout of O^T = V^T P^T (the 8 keys a lane contributes to
 // one 32-key MFMA step are the 2 x 4 keys it holds; V^T supplies the same 8
 // keys for its row d).  V arrives transposed from its projection, so both
-// tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps
-// (dims past d read as zero) plus, for d % 32 == 16, one 16-wide step.
+// tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps,
+// dims past d read as zero (d = 40 -> 64, 80 -> 96 for Q K^T).
 #include "common.h"
 #include "attention.h"
 #include "trace.h"
@@ -29,17 +29,14 @@ constexpr float LOG2E = 1.4426950408889634f;
 
 template <int DH>
 __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
-  // 32-wide head-dim steps (a remainder of 8 runs as a zero-masked 32-wide
-  // step), then one 16-wide step for a remainder of 16
-  constexpr int N32 = DH % 32 == 8 ? DH / 32 + 1 : DH / 32;
-  constexpr int REM = DH % 32 == 8 ? 0 : DH % 32;
+  constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
   constexpr int KST = KCH % 2 ? KCH : KCH + 1; // odd chunk stride: conflict-free row reads
   constexpr int KROW = KST * 8;                // halfs per LDS key row
   constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
   constexpr int KPT = (KCN + 255) / 256, VPT = (VCN + 255) / 256;
-  static_assert(DH % 8 == 0 && (REM == 0 || REM == 16), "head dim");
+  static_assert(DH % 8 == 0, "head dim");
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                       // [2]
   _Float16 (*sVt)[DV * VROW] = (_Float16 (*)[DV * VROW])(smem + 2 * KB * KROW * 2);  // [2]
@@ -53,19 +50,17 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   const int qblk = id % nqb, head = (id / nqb) % a.heads, row = id / (nqb * a.heads);
   const int q0 = qblk * (64 * QB) + wave * (16 * QB);
 
-  // Q^T fragments (B operand): query q0 + qb*16 + li; 32-wide steps take dims
-  // ks*32 + kc*8 .. +8, the 16-wide step dims N32*32 + kc*4 .. +4; zero past DH.
-  half8 fq[QB][N32 > 0 ? N32 : 1];
-  half4 fq16[QB];
+  // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8,
+  // zero past DH.
+  half8 fq[QB][N32];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int q = q0 + qb * 16 + li;
     const _Float16* qrow = a.q + ((int64_t)row * a.S + (q < a.S ? q : 0)) * a.ldq + head * DH;
 #pragma unroll
     for (int ks = 0; ks < N32; ++ks)
-      fq[qb][ks] = (q < a.S && ks * 32 + kc * 8 < DH) ? *(const half8*)(qrow + ks * 32 + kc * 8) : half8{};
-    fq16[qb] = half4{};
-    if (REM && q < a.S && N32 * 32 + kc * 4 < DH) fq16[qb] = *(const half4*)(qrow + N32 * 32 + kc * 4);
+      fq[qb][ks] = (q < a.S && ks * 32 + kc * 8 < DH) ? *(const half8*)(qrow + ks * 32 + kc * 8)
+                                                      : half8{};
   }
 
   floatx4 acc[QB][DV / 16];
@@ -85,8 +80,10 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   const _Float16* vtbase = a.vt + (int64_t)head * DH * a.vt_ld + (int64_t)row * a.vt_row;
   const int nkb = (a.L + KB - 1) / KB;
 
-  uint4 rk[KPT], rv[VPT];
-  auto fetch = [&](int kb) {
+  // Two register sets: block kb + 2 is requested while block kb is multiplied
+  // and block kb + 1 waits in the other set (two blocks of latency hiding).
+  uint4 rkA[KPT], rvA[VPT], rkB[KPT], rvB[VPT];
+  auto fetch = [&](int kb, uint4(&rk)[KPT], uint4(&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * 256;
@@ -103,7 +100,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
                                     : make_uint4(0, 0, 0, 0);
     }
   };
-  auto stash = [&](int buf, int kb) {
+  auto stash = [&](int buf, int kb, const uint4(&rk)[KPT], const uint4(&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * 256;
@@ -125,13 +122,12 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     }
   };
 
-  fetch(0);
-  stash(0, 0);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
+  // one key block: request block kb + 2 into F (free: it held block kb, already
+  // in LDS), multiply block kb from LDS, then move block kb + 1 from S to LDS
+  auto body = [&](int kb, uint4(&Fk)[KPT], uint4(&Fv)[VPT], const uint4(&Sk)[KPT],
+                  const uint4(&Sv)[VPT]) {
     const int cur = kb & 1;
-    const bool more = kb + 1 < nkb;
-    if (more) fetch(kb + 1);
+    if (kb + 2 < nkb) fetch(kb + 2, Fk, Fv);
     const _Float16* K_ = sK[cur];
     const _Float16* V_ = sVt[cur];
     // S^T for 4 key quarters x QB query blocks; lane holds keys h*16 + 4*kc + r.
@@ -139,18 +135,16 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const _Float16* kr = &K_[(h * 16 + li) * KROW];
-      half8 fk[N32 > 0 ? N32 : 1];
+      half8 fk[N32];
 #pragma unroll
-      for (int ks = 0; ks < N32; ++ks) fk[ks] = ks * 32 + kc * 8 < DH ? *(const half8*)(kr + ks * 32 + kc * 8) : half8{};
-      half4 fk16 = half4{};
-      if (REM && N32 * 32 + kc * 4 < DH) fk16 = *(const half4*)(kr + N32 * 32 + kc * 4);
+      for (int ks = 0; ks < N32; ++ks)
+        fk[ks] = ks * 32 + kc * 8 < DH ? *(const half8*)(kr + ks * 32 + kc * 8) : half8{};
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         s[qb][h] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < N32; ++ks)
           s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
-        if (REM) s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x16f16(fk16, fq16[qb], s[qb][h], 0, 0, 0);
       }
     }
     const bool tail = (kb + 1) * KB > a.L;
@@ -202,8 +196,16 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
           acc[qb][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp[qb][st], acc[qb][j], 0, 0, 0);
       }
     }
-    if (more) stash(cur ^ 1, kb + 1);
+    if (kb + 1 < nkb) stash(cur ^ 1, kb + 1, Sk, Sv);
     __syncthreads();
+  };
+  fetch(0, rkA, rvA);
+  if (1 < nkb) fetch(1, rkB, rvB);
+  stash(0, 0, rkA, rvA);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; kb += 2) {  // unrolled by two: the register sets stay static
+    body(kb, rkA, rvA, rkB, rvB);
+    if (kb + 1 < nkb) body(kb + 1, rkB, rvB, rkA, rvA);
   }
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {

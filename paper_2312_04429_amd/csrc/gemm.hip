@@ -42,7 +42,7 @@ constexpr uint32_t OOB = 0x80000000u;  // offset past every descriptor's range
 #define GEMM_S128 2
 #endif
 #ifndef GEMM_S64
-#define GEMM_S64 2
+#define GEMM_S64 3
 #endif
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -856,7 +856,8 @@ hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
 // Tile choice for the streamed kernel (GPU time measured on the UNet's
 // shapes).  A workgroup here is bound by the latency of its k-tile loads
 // (about 0.4 us per tile), so small tiles and many resident workgroups win:
-// 64 x 64 tiles with a two-deep ring by default; K is split when it is long
+// 64 x 64 tiles with a three-deep ring by default (inside the network the
+// weights arrive cold from HBM, where the third buffer pays); K is split when it is long
 // (>= 40 tiles) or the grid is tiny, keeping >= MIN_KT tiles per split and
 // about 700 workgroups at most.  Large grids take 64 x 128 (wide N) or
 // 128 x 128 tiles; a long K over a mid-sized grid takes split 128 x 128.

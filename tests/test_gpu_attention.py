@@ -14,6 +14,7 @@ pytestmark = pytest.mark.gpu
 
 @pytest.mark.parametrize("rows,S,L,heads,dh", [(2, 300, 77, 8, 40), (2, 256, 256, 8, 40),
                                                (1, 200, 130, 8, 80), (2, 64, 77, 8, 160),
+                                               (1, 128, 256, 4, 80), (2, 70, 200, 2, 16),
                                                (2, 130, 8, 4, 16), (1, 128, 77, 10, 64),
                                                (1, 96, 100, 2, 32), (1, 64, 64, 2, 128)])
 def test_attention(rows, S, L, heads, dh):
