@@ -31,7 +31,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="sd15_b1")
+    ap.add_argument("--workload", default="sd15_b1",
+                    help="sd15_b1 (default), sd15_b8_mixed, sdxl_b2, retrieval_heavy")
+    ap.add_argument("--k", type=int, default=None,
+                    help="sd15_b1: place the query in this K's similarity band; "
+                         "sdxl_b2: the skip count (default: first of the workload's K values)")
+    ap.add_argument("--scan-only", action="store_true",
+                    help="time the lookup alone, warm (back to back) and cold (a 2 GiB write "
+                         "between repetitions evicts the cache from the Infinity Cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the event tracing of kernel launches (for counter passes)")
@@ -50,6 +57,7 @@ def unet_flops_per_row(cfg):
     td = 4 * c0
     H, W = cfg["H"], cfg["W"]
     fl += 2 * c0 * td + 2 * td * td                       # time MLP
+    fl += 2 * cfg.get("pooled_dim", 0) * td                 # pooled vector -> time embedding
     fl += 2 * H * W * c0 * 9 * cfg["in_ch"]                 # conv_in
     specs = synth.param_specs(cfg)
     # walk the topology with spatial sizes
@@ -124,9 +132,11 @@ def traffic_for(family):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc):
-    """The oracle on this host's cores: one guided UNet step (2 rows) and the
-    lookup over the same cache, extrapolated to images/s at the same K."""
+def cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc, d_cache, pooled):
+    """The oracle on this host's cores, on a bounded sample of the workload: one
+    guided UNet step (2 rows) and the lookup over a slice of queries x cache
+    rows, extrapolated to images/s at the same K values (lookup time scaled by
+    queries x rows, denoise time by the number of UNet steps)."""
     import synth
     from oracle import lookup as LK
     from oracle import unet as U
@@ -135,22 +145,77 @@ def cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count()
+    ks = K if isinstance(K, list) else [K]
+    notes = []
+    t_lookup = 0.0
+    if "n_cache" in wl:
+        n, m = wl["n_cache"], q.shape[0]
+        n_s = min(n, 1_000_000)
+        m_s = max(1, min(m, 2_000_000 // n_s))
+        if cache is None:
+            sample = d_cache[:n_s].view(dtype=__import__("torch").int16).cpu().numpy().view(np.uint16)
+        else:
+            sample = cache[:n_s]
+        t0 = time.perf_counter()
+        LK.lookup(q[:m_s], sample, [t for t, _ in wl["thresholds"]],
+                  [k for _, k in wl["thresholds"]])
+        t_s = time.perf_counter() - t0
+        t_lookup = t_s * (m * n) / (m_s * n_s)
+        notes.append(f"lookup of {m_s} of {m} queries over {n_s} of {n} cache rows "
+                     f"({t_s:.2f} s, scaled x{(m * n) / (m_s * n_s):g})")
     net = U.UNet(cfg, weights)
-    x = synth.make_latents(1, 4, cfg["H"], cfg["W"], 2000)[0]
+    x = synth.make_latents(1, cfg["in_ch"], cfg["H"], cfg["W"], 2000)[0]
+    pl = None if pooled is None else pooled[0]
     t0 = time.perf_counter()
-    LK.lookup(q, cache, [t for t, _ in wl["thresholds"]], [k for _, k in wl["thresholds"]])
-    t_lookup = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    net(x, 481, unc[0])
-    net(x, 481, cond[0])
+    net(x, 481, unc[0], pooled=pl)
+    net(x, 481, cond[0], pooled=pl)
     t_step = time.perf_counter() - t0
-    t_img = t_lookup + (wl["N"] - K) * t_step
-    return {"value": 1.0 / t_img, "unit": "images/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"oracle (NumPy fp32/fp64) on this host: 1 lookup over the "
-                       f"{cache.shape[0]}x{cache.shape[1]} cache ({t_lookup:.2f} s) + 1 guided "
-                       f"UNet step = 2 rows ({t_step:.2f} s), extrapolated to {wl['N'] - K} "
-                       f"steps per image"),
+    steps = sum(wl["N"] - k for k in ks)
+    notes.append(f"1 guided UNet step = 2 rows ({t_step:.2f} s) x {steps} steps for "
+                 f"{len(ks)} image{'s' if len(ks) > 1 else ''}")
+    t_batch = t_lookup + steps * t_step
+    return {"value": len(ks) / t_batch, "unit": "images/s", "cores": int(cores), "kind": "oracle",
+            "sample": "oracle (NumPy fp32 UNet, fp64 lookup) on this host: " + "; ".join(notes),
             "unet_step_s": t_step, "lookup_s": t_lookup}
+
+
+BAND = {25: 0.97, 20: 0.925, 15: 0.875, 10: 0.80, 5: 0.70, 0: 0.5}  # similarity inside each K's band
+
+
+def build_lookup_inputs(wl, B, args, dev, torch, synth):
+    """Cache, queries and the indices of the queries that feed the denoise."""
+    n, d = wl["n_cache"], wl["d"]
+    if n > 2_000_000:  # too large for the host generator: drawn on the device, same recipe
+        d_cache = synth.make_cache_device(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"], dev)
+        cache = None
+        host_rows = lambda r: d_cache[torch.from_numpy(np.asarray(r, dtype=np.int64)).to(dev)] \
+            .view(torch.int16).cpu().numpy().view(np.uint16)
+    else:
+        cache = synth.make_cache(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"])
+        d_cache = torch.from_numpy(cache.view(np.int16)).to(dev)
+        host_rows = lambda r: cache[np.asarray(r)]
+    if "n_queries" in wl:  # retrieval-heavy: half planted (s in [0.95, 0.999]), half fresh draws
+        m = wl["n_queries"]
+        rng = np.random.default_rng(wl["query_seed"])
+        planted = rng.choice(n, m // 2, replace=False)
+        near = synth.make_queries_at_sims(synth.from_bf16_bits(host_rows(planted)),
+                                          rng.uniform(0.95, 0.999, m // 2), wl["query_seed"])
+        mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev).cpu().numpy()
+        far = synth.cluster_queries_from(mu, m - m // 2, wl["sigma"], wl["query_seed"] + 1)
+        q = np.empty((m, d), dtype=np.float32)
+        q[0::2], q[1::2] = near, far
+        return d_cache, cache, q, list(range(B))
+    target = [(31337 + 7919 * b) % n for b in range(B)]
+    if args.k is not None:
+        sims = [BAND[args.k]] * B
+    elif "query_sims" in wl:
+        sims = list(wl["query_sims"])
+    else:  # each sample's K drawn from the selector's K values, similarity inside its band
+        ks = synth.make_k_values(B, sorted(k for k in BAND if k), wl["k_seed"])
+        sims = [BAND[int(k)] for k in ks]
+    rows = host_rows(target)
+    q = synth.make_queries_at_sims(synth.from_bf16_bits(rows), sims, wl["query_seed"])
+    return d_cache, cache, q, list(range(B))
 
 
 def main():
@@ -168,43 +233,60 @@ def main():
     cfg = synth.unet_config(wl["unet"])
     S = synth.SCHEDULE_SD
     sched = (S["T"], wl["N"], S["beta_start"], S["beta_end"])
-    thr = [t for t, _ in wl["thresholds"]]
-    kv = [k for _, k in wl["thresholds"]]
     B = wl["batch"]
     dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    has_cache = "n_cache" in wl
     print(f"[bench] generating {args.workload} inputs", file=sys.stderr, flush=True)
+    if has_cache:
+        thr = [t_ for t_, _ in wl["thresholds"]]
+        kv = [k for _, k in wl["thresholds"]]
+        d_cache, cache, q, feed = build_lookup_inputs(wl, B, args, dev, torch, synth)
+        d_q = t(q)
+        lws_bytes = P.nv_cache_lookup_workspace(q.shape[0], wl["n_cache"], wl["d"])
+        lws_own, lws_addr = P.workspace(lws_bytes, dev)
+        lws = (lws_own, lws_addr, lws_bytes)
+    if args.scan_only:
+        if not has_cache:
+            sys.exit(f"--scan-only needs a workload with a cache ({args.workload} has none)")
+        return scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, q.shape[0])
     weights = synth.make_weights(cfg, wl["weight_seed"])
     net = P.NvUNet(cfg, weights)
-    cache = synth.make_cache(wl["n_cache"], wl["d"], wl["clusters"], wl["sigma"], wl["cache_seed"])
-    target = [31337 % wl["n_cache"]]
-    q = synth.make_queries_at_sims(synth.cache_rows_f32(cache, target), wl["query_sims"],
-                                   wl["query_seed"])
     cond = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["cond_seed"])
     unc = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["uncond_seed"])
-    slots = [5, 10, 15, 20, 25]
-    pool = 64
-    rng = np.random.default_rng(77)
-    store = rng.standard_normal((pool, len(slots), cfg["in_ch"], cfg["H"], cfg["W"]),
-                                dtype=np.float32)
-    payload = (np.arange(wl["n_cache"]) % pool).astype(np.int32)
+    d_cond, d_unc = t(cond), t(unc)
+    d_pooled = t(synth.make_pooled(B, cfg["pooled_dim"], wl["pooled_seed"])) \
+        if cfg.get("pooled_dim") else None
     noise = synth.make_latents(B, cfg["in_ch"], cfg["H"], cfg["W"], 2000)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    d_cache = t(cache.view(np.int16))
-    d_q, d_store, d_payload = t(q), t(store), t(payload)
-    d_cond, d_unc, d_noise = t(cond), t(unc), t(noise)
-    lws_bytes = P.nv_cache_lookup_workspace(q.shape[0], cache.shape[0], cache.shape[1])
-    lws_own, lws_addr = P.workspace(lws_bytes, dev)
-    lws = (lws_own, lws_addr, lws_bytes)
+    d_noise = t(noise)
     x = torch.empty_like(d_noise)
-
     ks_seen = []
+    if has_cache:
+        slots = [5, 10, 15, 20, 25]
+        pool = 64
+        rng = np.random.default_rng(77)
+        store = rng.standard_normal((pool, len(slots), cfg["in_ch"], cfg["H"], cfg["W"]),
+                                    dtype=np.float32)
+        payload = (np.arange(wl["n_cache"]) % pool).astype(np.int32)
+        d_store, d_payload = t(store), t(payload)
+        nf = len(feed)
 
-    def step():
-        idx, sim, kk = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
-        P.nv_gather_states(d_store, slots, d_payload, wl["n_cache"], idx, kk, d_noise, out=x)
-        k_host = kk.cpu().tolist()          # the one device -> host crossing per batch
-        ks_seen.append(k_host)
-        net.nv_denoise(x, k_host, d_cond, d_unc, guidance=wl["guidance"], sched=sched)
+        def step():
+            idx, sim, kk = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+            idx, kk = idx[:nf], kk[:nf]  # the queries that feed this batch
+            P.nv_gather_states(d_store, slots, d_payload, wl["n_cache"], idx, kk, d_noise, out=x)
+            k_host = kk.cpu().tolist()          # the one device -> host crossing per batch
+            ks_seen.append(k_host)
+            net.nv_denoise(x, k_host, d_cond, d_unc, pooled=d_pooled, guidance=wl["guidance"],
+                           sched=sched)
+    else:  # denoise-only workload (no cache in its recipe): a fixed skip count
+        kfix = args.k if args.k is not None else wl["k_sweep"][0]
+
+        def step():
+            x.copy_(d_noise)  # stands in for the fetched state (contents do not affect timing)
+            ks_seen.append([kfix] * B)
+            net.nv_denoise(x, [kfix] * B, d_cond, d_unc, pooled=d_pooled,
+                           guidance=wl["guidance"], sched=sched)
 
     print("[bench] warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -238,21 +320,27 @@ def main():
                               "tflops": kfl / (kms * 1e-3) / 1e12 if kms else None,
                               "gbps": kby / (kms * 1e-3) / 1e9 if kms else None}
     ms = dt * 1e3 / args.steps
-    K = ks_seen[-1][0]
+    ks_last = ks_seen[-1]
+    K = ks_last[0] if len(ks_last) == 1 else ks_last
     images = args.steps * B
     unet_steps = sum(wl["N"] - k for ks in ks_seen[-args.steps:] for k in ks)
     fl_row = unet_flops_per_row(cfg)
     fl_step = 2 * fl_row
     ups = unet_steps / dt
+    desc = {"sd15": "SD-1.5-shaped (859.5M params, random-init)",
+            "sdxl": "SDXL-shaped (2.56B params, random-init)",
+            "tiny": "tiny (random-init)"}[wl["unet"]]
+    config = {"workload": args.workload, "unet": desc,
+              "latent": [cfg["in_ch"], cfg["H"], cfg["W"]], "batch": B, "cfg_rows": 2 * B,
+              "N": wl["N"], "K": K, "guidance": wl["guidance"]}
+    if has_cache:
+        config["cache"] = f"{wl['n_cache']}x{wl['d']} bf16"
+        config["queries"] = int(q.shape[0])
     out = {
         "metric": "images/sec and UNet steps/sec at skip K (SD1.5-shape, 1 GPU); % MFMA peak",
         "value": images / dt, "unit": "images/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f16", "data": "synthetic",
-        "config": {"workload": args.workload, "unet": "SD-1.5-shaped (859.5M params, random-init)",
-                   "latent": [cfg["in_ch"], cfg["H"], cfg["W"]], "batch": B, "cfg_rows": 2 * B,
-                   "N": wl["N"], "K": K, "cache": f"{wl['n_cache']}x{wl['d']} bf16",
-                   "guidance": wl["guidance"]},
+        "vs_baseline": None, "dtype": "f16", "data": "synthetic", "config": config,
         "unet_steps_per_s": ups, "unet_step_ms": 1e3 / ups,
         "unet_step_tflop": fl_step / 1e12,
         "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16,
@@ -281,7 +369,55 @@ def main():
         del src, dst
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(cfg, weights, wl, K, cache, q, cond, unc)
+        out["cpu_baseline"] = cpu_baseline(
+            cfg, weights, wl, ks_last, cache if has_cache else None, q if has_cache else None,
+            cond, unc, d_cache if has_cache else None,
+            synth.make_pooled(B, cfg["pooled_dim"], wl["pooled_seed"]) if d_pooled is not None
+            else None)
+    print(json.dumps(out))
+
+
+def scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
+    """Lookup alone: warm (back to back) and cold (2 GiB written between repetitions)."""
+    nbytes = wl["n_cache"] * wl["d"] * 2
+    for _ in range(max(args.warmup, 1)):
+        P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+    e1.record()
+    torch.cuda.synchronize()
+    warm = e0.elapsed_time(e1) / args.steps
+    flush = torch.empty(1 << 29, dtype=torch.float32, device=dev)
+    cold = 0.0
+    for _ in range(args.steps):
+        flush.fill_(1.0)                 # 2 GiB of writes evicts the 256 MB Infinity Cache
+        e0.record()
+        P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+        e1.record()
+        torch.cuda.synchronize()
+        cold += e0.elapsed_time(e1)
+    cold /= args.steps
+    P.nv_trace_enable(P.FAM_SCAN, 4 * args.steps + 8)
+    for _ in range(args.steps):
+        P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+    torch.cuda.synchronize()
+    P.nv_trace_disable()
+    n, kms, _, kby = P.nv_trace_read(P.FAM_SCAN)
+    out = {"metric": "cache lookup (scan + rescore + selector), GB/s of cache read",
+           "value": nbytes / (warm * 1e-3) / 1e9, "unit": "GB/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+           "data": "synthetic",
+           "config": {"workload": args.workload, "cache": f"{wl['n_cache']}x{wl['d']} bf16",
+                      "queries": m},
+           "lookup_ms_warm": warm, "lookup_ms_cold": cold,
+           "gbps_cold": nbytes / (cold * 1e-3) / 1e9,
+           "scan_kernel_ms": kms / n, "scan_kernel_gbps": kby / (kms * 1e-3) / 1e9,
+           "hbm_frac_scan_kernel": kby / (kms * 1e-3) / HBM_PEAK,
+           "hbm_frac_lookup_warm": nbytes / (warm * 1e-3) / HBM_PEAK,
+           "hbm_frac_lookup_cold": nbytes / (cold * 1e-3) / HBM_PEAK}
     print(json.dumps(out))
 
 

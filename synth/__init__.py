@@ -9,7 +9,7 @@ from .configs import (UNET_TINY, UNET_SD15, UNET_SDXL, SCHEDULE_SD, THRESHOLDS_P
                       THRESHOLDS_TINY, WORKLOADS, unet_config)
 from .weights import param_specs, make_weights, param_count, bf16_round
 from .data import (make_cache, make_cache_device, cluster_centres_device, make_queries_at_sims,
-                   make_cluster_queries, cluster_queries_from, make_contexts, make_k_values,
+                   make_cluster_queries, cluster_queries_from, make_contexts, make_pooled, make_k_values,
                    cache_rows_f32, cluster_centres, make_latents, to_bf16_bits, from_bf16_bits)
 
 __all__ = [
@@ -17,5 +17,5 @@ __all__ = [
     "WORKLOADS", "unet_config", "param_specs", "make_weights", "param_count", "bf16_round",
     "make_cache", "make_queries_at_sims", "make_cluster_queries", "make_contexts", "make_latents",
     "to_bf16_bits", "from_bf16_bits", "make_k_values", "cache_rows_f32", "cluster_centres",
-    "make_cache_device", "cluster_centres_device", "cluster_queries_from",
+    "make_cache_device", "cluster_centres_device", "cluster_queries_from", "make_pooled",
 ]

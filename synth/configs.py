@@ -91,8 +91,12 @@ WORKLOADS = {
         unet="sdxl", N=50, guidance=7.5, weight_seed=0, batch=2, k_sweep=(10, 20),
         cond_seed=3, uncond_seed=4, pooled_seed=6,
     ),
+    # 256 queries (half planted within cosine 0.95 of cached rows, half fresh
+    # cluster draws, interleaved); the first 16 feed a batch-16 SD-1.5 denoise
+    # at their own K (misses start from noise, K = 0).
     "retrieval_heavy": dict(
-        n_cache=10_000_000, d=768, cache_dtype="bf16", clusters=10_000, sigma=0.05,
+        unet="sd15", n_cache=10_000_000, d=768, cache_dtype="bf16", clusters=10_000, sigma=0.05,
         cache_seed=31, query_seed=32, n_queries=256, thresholds=THRESHOLDS_PAPER,
+        N=50, guidance=7.5, weight_seed=0, batch=16, cond_seed=3, uncond_seed=4,
     ),
 }

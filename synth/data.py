@@ -119,6 +119,13 @@ def make_contexts(b, length, dim, seed):
     return from_bf16_bits(to_bf16_bits(x)).reshape(b, length, dim)
 
 
+def make_pooled(b, dim, seed):
+    """Pooled text-embedding stand-in (SDXL): N(0, 1), rounded to bfloat16 values."""
+    rng = np.random.default_rng([seed, 7])
+    x = rng.standard_normal((b, dim), dtype=np.float32)
+    return from_bf16_bits(to_bf16_bits(x)).reshape(b, dim)
+
+
 def make_latents(b, c, h, w, seed):
     """x_N ~ N(0, I) in float32 [b][c][h][w]."""
     rng = np.random.default_rng([seed, 5])
