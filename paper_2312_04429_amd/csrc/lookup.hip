@@ -9,15 +9,16 @@
 //      d 2^-52) |q~| (Cauchy-Schwarz on the rounding of q plus the worst-case
 //      accumulation error of any summation order, plus the float64 canonical
 //      sum's own error).  Per tile (128 rows for bf16 with d <= 768, else
-//      256) the kernel keeps the best lower bound L_t, the best upper bound
-//      U_t (float32 bounds widened to cover their own rounding) and the rows
-//      whose upper bound reaches L_t (at most CAP, in row order; more sets an
-//      overflow count).
-//   2. select: per query, L = max_t L_t; every row whose upper bound can reach
-//      L lives in a tile with U_t >= L and is listed there (or the tile
-//      overflowed and is rescanned whole).  Those rows are rescored with the
-//      canonical float64 left-to-right dot product; the maximum with the
-//      lowest index wins; its float32 rounding goes through the thresholds.
+//      256) the kernel writes, for every query, the largest scan score M_tq
+//      of the tile's rows, and once per tile an upper bound N_t on its row
+//      norms.  Nothing else leaves the scan.
+//   2. select: per query, L = max_t (M_tq - N_t E_q) is a lower bound on the
+//      best canonical score, and every row that can reach it lies in a tile
+//      with M_tq + N_t E_q >= L.  Those tiles are read again: a float64 dot
+//      with eight partial sums discards rows that provably cannot reach L;
+//      the rest are rescored with the canonical float64 left-to-right dot
+//      product; the maximum with the lowest index wins; its float32 rounding
+//      goes through the thresholds.
 #include <algorithm>
 #include <cmath>
 
@@ -29,8 +30,6 @@ namespace {
 
 constexpr int TILE = 256;    // cache rows per workgroup of the f32 and wide-d bf16 scans
 constexpr int QB = 16;       // queries per matrix-core column block
-constexpr int CAP = 16;      // listed candidates per (query, tile)
-constexpr int OVF_CAP = 512; // overflowed tiles handled per select pass
 constexpr int MAX_D = 2048;
 
 struct Thresholds {
@@ -40,13 +39,20 @@ struct Thresholds {
 };
 
 struct LookupWs {
-  uint16_t* qbf;  // [mq_pad][d] bf16 bits of the queries
-  double* E;      // [m] margin factor per query
-  double* tileL;  // [m][T]
-  double* tileU;  // [m][T]
-  int32_t* cnt;   // [m][T]
-  int32_t* cand;  // [m][T][CAP]
+  uint16_t* qbf;  // [mq][dp] bf16 bits of the queries, chunk-swizzled (see qpos)
+  double* E;      // [mq] margin factor per query
+  float* tmax;    // [T][mq] largest scan score of each tile, per query
+  float* nmax;    // [T] upper bound on the row norms of each tile
+  int mq;         // m rounded up to a whole query block
+  int dp;         // d rounded up to a multiple of 64 (query row length in qbf)
 };
+
+// Element offset of k (a multiple of 8) of query row r in a [rows][dp] query
+// block: the 16-byte chunk k / 8 sits at chunk (k / 8) ^ (r & 7) of its row.
+// Rows are dp = 64 j elements long, so the swap stays inside the row, and the
+// eight rows that one 16-byte LDS read by eight lanes touches (same k, rows
+// r..r+7) land on eight different 16-byte bank groups.
+__device__ inline int qpos(int r, int k, int dp) { return r * dp + ((((k >> 3) ^ (r & 7))) << 3); }
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -70,17 +76,26 @@ __device__ inline T block_max_256(T v, T* red) {
   return r;
 }
 
+__device__ inline double block_sum_256(double v, double* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
 // Per query: bf16 copy (padded rows are zero) and the margin factor E_q.
 __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int m, int mq_pad,
-                                               int d, int cache_bf16, uint16_t* __restrict__ qbf,
+                                               int d, int dp, int cache_bf16,
+                                               uint16_t* __restrict__ qbf,
                                                double* __restrict__ E) {
   __shared__ double red[3][4];
   const int j = blockIdx.x;
   double e = 0.0, nb = 0.0, nq = 0.0;
-  for (int k = threadIdx.x; k < d; k += 256) {
-    float v = j < m ? q[(int64_t)j * d + k] : 0.0f;
+  for (int k = threadIdx.x; k < dp; k += 256) {  // zero padding up to dp
+    float v = j < m && k < d ? q[(int64_t)j * d + k] : 0.0f;
     uint16_t b = f32_to_bf16_rne(v);
-    qbf[(int64_t)j * d + k] = b;
+    qbf[(int64_t)j * dp + ((((k >> 3) ^ (j & 7))) << 3) + (k & 7)] = b;
     double vb = (double)bf16_to_f32(b);
     double dv = (double)v;
     e += (dv - vb) * (dv - vb);
@@ -109,83 +124,43 @@ __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int 
   }
 }
 
-// Rigorous float32 bounds s~ +- dd.  dd = nr * e with nr >= |c_i| and
-// e >= E_q (both rounded up beforehand), so |s~ - s64| <= dd.  t = s~ +- dd
-// is off from the exact sum by at most 2^-24 |t| (one rounding, or none more
-// if contracted into an fma), and the final step rounds once more; the slack
-// |t| 2^-20 + 2^-100 covers both with room, including subnormal products.
-__device__ inline float upper_bound(float sc, float dd) {
-  const float t = sc + dd;
-  return t + fmaf(fabsf(t), 0x1p-20f, 0x1p-100f);
-}
-__device__ inline float lower_bound(float sc, float dd) {
-  const float t = sc - dd;
-  return t - fmaf(fabsf(t), 0x1p-20f, 0x1p-100f);
+// Largest score per query of a tile whose scores sS[q][r] (row stride SS) are
+// in LDS: 16 threads per query, rows past `rows` ignored.  Writes M_tq for
+// the 16 queries of the block at q0.
+template <int TR, int SS>
+__device__ inline void write_tile_max(const float* sS, int rows, int tile, int q0,
+                                      const LookupWs& ws) {
+  const int q = threadIdx.x >> 4, sub = threadIdx.x & 15;
+  float v = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < TR / 16; ++j) {
+    const int r = sub + 16 * j;
+    if (r < rows) v = fmaxf(v, sS[q * SS + r]);
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  if (sub == 0) ws.tmax[(int64_t)tile * ws.mq + q0 + q] = v;
 }
 
-// Shared tail of the scans: the block's scores sS[q][r] (row stride TR + TPQ)
-// and row norms sN[r] are in LDS; Eq is the margin factor of the calling
-// thread's query (threadIdx.x / (NT / QB)).  NT / QB consecutive threads own
-// one query; each covers TR / (NT / QB) rows of the tile, forms their bounds,
-// and the group maxima come from lane shuffles.  Rows whose upper bound
-// reaches the group's best lower bound are listed in row order through a wave
-// ballot, so the list is deterministic.  No barrier inside: the scans
-// double-buffer sS.
-template <int NT, int TR>
-__device__ void tile_finalize(const float* sS, const float* sN, int tile, int64_t n, int q0,
-                              int qcount, int T, double Eq, LookupWs ws) {
-  constexpr int TPQ = NT / QB, RPT = TR / TPQ, SS = TR + TPQ;
-  static_assert(TPQ <= 64 && (TPQ & (TPQ - 1)) == 0 && TR % TPQ == 0, "group shape");
-  const int t = threadIdx.x, q = t / TPQ, sub = t % TPQ, lane = t & 63;
-  const int64_t row0 = (int64_t)tile * TR;
-  const bool act = q < qcount;
-  const bool full = row0 + TR <= n;  // uniform: every row of the tile exists
-  // e >= Eq: (1 + 2^-22) absorbs the rounding to float32
-  const float e = act ? (float)(Eq * (1.0 + 0x1p-22)) : 0.f;
-  const float* sq = sS + q * SS;
-  float L = -INFINITY, U = -INFINITY;
+// N_t = the largest of the tile's row-norm bounds sN[0..rows) (first wave).
+template <int TR>
+__device__ inline void write_norm_max(const float* sN, int rows, int tile, const LookupWs& ws) {
+  if (threadIdx.x >= 64) return;
+  float v = 0.f;
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    const int r = sub + j * TPQ;
-    const float sc = sq[r], dd = sN[r] * e;
-    const bool ok = act && (full || row0 + r < n);
-    L = ok ? fmaxf(L, lower_bound(sc, dd)) : L;
-    U = ok ? fmaxf(U, upper_bound(sc, dd)) : U;
+  for (int j = 0; j < TR / 64; ++j) {
+    const int r = (int)threadIdx.x + 64 * j;
+    if (r < rows) v = fmaxf(v, sN[r]);
   }
 #pragma unroll
-  for (int o = TPQ / 2; o > 0; o >>= 1) {
-    L = fmaxf(L, __shfl_xor(L, o, 64));
-    U = fmaxf(U, __shfl_xor(U, o, 64));
-  }
-  const int gbase = lane & ~(TPQ - 1);
-  const uint64_t gmask = (TPQ == 64 ? ~0ull : ((1ull << (TPQ & 63)) - 1)) << gbase;
-  const uint64_t below = (1ull << lane) - 1;
-  int32_t* list = ws.cand + ((int64_t)(q0 + q) * T + tile) * CAP;
-  int cnt = 0;
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    const int r = sub + j * TPQ;
-    const float sc = sq[r], dd = sN[r] * e;
-    const bool p = act && (full || row0 + r < n) && upper_bound(sc, dd) >= L;
-    const uint64_t bal = __ballot(p);
-    if (p) {
-      const int pos = cnt + __popcll(bal & gmask & below);
-      if (pos < CAP) list[pos] = (int32_t)(row0 + r);
-    }
-    cnt += __popcll(bal & gmask);
-  }
-  if (act && sub == 0) {
-    ws.tileL[(int64_t)(q0 + q) * T + tile] = (double)L;
-    ws.tileU[(int64_t)(q0 + q) * T + tile] = (double)U;
-    ws.cnt[(int64_t)(q0 + q) * T + tile] = cnt;
-  }
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  if (threadIdx.x == 0) ws.nmax[tile] = v;
 }
 
 constexpr uint32_t OOB = 0x80000000u;  // offset past the tile descriptor's range
 constexpr int KS = 24;                 // 32-element k steps per register chunk (768 elements)
 constexpr int SS_WIDE = TILE + 16;    // score row stride, 256 threads x 256 rows
 constexpr int RR_TILE = 128;           // cache rows per many-query workgroup
-constexpr int SS_RR = RR_TILE + 16;
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -194,35 +169,25 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
-// Request one 16-query block of bf16 queries and its 16 margin factors
-// straight into LDS (global -> LDS 16-byte loads, no registers): in each
-// round, wave w moves the 64 chunks starting at chunk (round * 4 + w) * 64;
-// lane l's chunk lands 16 l bytes past the wave's LDS base.  Complete after
-// the issuing wave's vmcnt reaches 0.
-__device__ inline void dma_queries(uint16_t* sQ, double* sE, const LookupWs& ws, int q0, int d) {
-  const int nc = QB * d / 8;
+// Request one 16-query block of bf16 queries straight into LDS (global ->
+// LDS 16-byte loads, no registers): in each round, wave w moves the 64
+// chunks starting at chunk (round * 4 + w) * 64; lane l's chunk lands 16 l
+// bytes past the wave's LDS base.  Complete after the issuing wave's vmcnt
+// reaches 0.
+__device__ inline void dma_queries(uint16_t* sQ, const LookupWs& ws, int q0) {
+  const int nc = QB * ws.dp / 8;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const char* src = (const char*)(ws.qbf + (int64_t)q0 * d);
+  const char* src = (const char*)(ws.qbf + (int64_t)q0 * ws.dp);
   for (int base = wave * 64; base < nc; base += 256)
     if (base + lane < nc)
       __builtin_amdgcn_global_load_lds((gptr_t)(src + (size_t)(base + lane) * 16),
                                        (lptr_t)((char*)sQ + (size_t)base * 16), 16, 0, 0);
-  if (wave == 0 && lane < QB / 2)
-    __builtin_amdgcn_global_load_lds((gptr_t)(ws.E + q0 + 2 * lane), (lptr_t)sE, 16, 0, 0);
 }
 
 // Stage one 16-query block of bf16 queries into LDS.
-__device__ inline void stage_queries(uint16_t* sQ, const uint16_t* __restrict__ qbf, int q0, int d) {
-  for (int i = threadIdx.x; i < QB * d / 8; i += blockDim.x)
-    ((uint4*)sQ)[i] = ((const uint4*)(qbf + (int64_t)q0 * d))[i];
-}
-
-// Margin factor of this thread's query in the 16-query block at q0 (threads
-// NT / QB apart share a query), 0 past m.
-template <int NT>
-__device__ inline double query_margin(const double* __restrict__ E, int q0, int m) {
-  const int q = q0 + (int)threadIdx.x / (NT / QB);
-  return q < m ? E[q] : 0.0;
+__device__ inline void stage_queries(uint16_t* sQ, const uint16_t* __restrict__ qbf, int q0, int dp) {
+  for (int i = threadIdx.x; i < QB * dp / 8; i += blockDim.x)
+    ((uint4*)sQ)[i] = ((const uint4*)(qbf + (int64_t)q0 * dp))[i];
 }
 
 // bf16 cache with d > 768: 4 waves x 64 rows per 256-row tile; each wave runs
@@ -233,10 +198,11 @@ __device__ inline double query_margin(const double* __restrict__ E, int q0, int 
 // l, register r holds D[4 (l / 16) + r][l % 16].  Loads go through a
 // range-checked descriptor of the tile (rows past n read zero).
 __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restrict__ cache, int64_t n,
-                                                    int d, int m, int T, LookupWs ws) {
+                                                    int d, int m, LookupWs ws) {
   extern __shared__ __align__(16) unsigned char smem[];
-  uint16_t* sQ = (uint16_t*)smem;                       // [QB][d]
-  float* sS = (float*)(smem + QB * d * 2);              // [2][QB][SS_WIDE]
+  const int dp = ws.dp;
+  uint16_t* sQ = (uint16_t*)smem;                       // [QB][dp]
+  float* sS = (float*)(smem + QB * dp * 2);             // [2][QB][SS_WIDE]
   float* sN = sS + 2 * QB * SS_WIDE;                   // [TILE]
   const int tile = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -257,9 +223,8 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
     }
   };
   for (int q0 = 0, par = 0; q0 < m; q0 += QB, par ^= 1) {
-    const double Eq = query_margin<256>(ws.E, q0, m);
     __syncthreads();  // every wave is past the previous block's multiplies
-    stage_queries(sQ, ws.qbf, q0, d);
+    stage_queries(sQ, ws.qbf, q0, dp);
     __syncthreads();
     const bool norms = q0 == 0;  // row norms during the first query block
     float* S = sS + par * QB * SS_WIDE;
@@ -272,12 +237,13 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
       for (int j = 0; j < KS; ++j) {
         const int k = ch * 32 * KS + j * 32 + kc * 8;
         uint4 b = make_uint4(0, 0, 0, 0);
-        if (k < d) b = *(const uint4*)(sQ + li * d + k);
+        if (k < d) b = *(const uint4*)(sQ + qpos(li, k, dp));
         if (norms) {
           const u32x4 w = a[j];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const bf16x2 v = __builtin_bit_cast(bf16x2, w[e]);
+            const uint32_t we = w[e];  // via a scalar: a vector element cast directly
+            const bf16x2 v = __builtin_bit_cast(bf16x2, we);  // miscompiles to element 0
             nn = __builtin_amdgcn_fdot2_f32_bf16(v, v, nn, false);
           }
         }
@@ -305,20 +271,29 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
       consume(st + 1, a1);
     }
     __syncthreads();
-    tile_finalize<256, TILE>(S, sN, tile, n, q0, min(QB, m - q0), T, Eq, ws);
+    if (norms) write_norm_max<TILE>(sN, rows, tile, ws);
+    write_tile_max<TILE, SS_WIDE>(S, rows, tile, q0, ws);
   }
 }
 
-// 16 rows x 16 queries x (KS * 32) k for both row blocks of a wave; Q is the
+// 16 rows x 16 queries x (NS * 32) k for both row blocks of a wave; Q is the
 // query block in LDS (its own buffer: __restrict__ lets the compiler tell
 // these reads from global -> LDS loads in flight into the other buffer).
-__device__ __forceinline__ void rr_block(const uint16_t* __restrict__ Q, const u32x4 (&a)[KS][2],
-                                         int d, int li, int kc, floatx4& acc0, floatx4& acc1) {
+// NS = dp / 32 steps: the padded query row is zero past d, so every read is
+// unconditional and the compiler can run the LDS reads ahead of the multiplies.
+template <int NS>
+__device__ __forceinline__ void rr_block(const uint16_t* __restrict__ Q, const u32x4 (&a)[NS][2],
+                                         int li, int kc, floatx4& acc0, floatx4& acc1) {
+  constexpr int dp = NS * 32;
+  // qpos(li, 32 j + 8 kc, dp) = li dp + 8 (kc ^ (li & 3)) + 32 (j ^ ((li >> 2) & 1)):
+  // even j sit 32 x2 elements past 32 j, odd j 32 x2 before it (x2 = bit 2 of
+  // li), so two base addresses and immediate offsets cover every step.
+  const int x2 = (li >> 2) & 1;
+  const uint16_t* be = Q + li * dp + 8 * (kc ^ (li & 3)) + 32 * x2;
+  const uint16_t* bo = be - 64 * x2;
 #pragma unroll
-  for (int j = 0; j < KS; ++j) {
-    const int k = j * 32 + kc * 8;
-    uint4 qv = make_uint4(0, 0, 0, 0);
-    if (k < d) qv = *(const uint4*)(Q + li * d + k);
+  for (int j = 0; j < NS; ++j) {
+    const uint4 qv = *(const uint4*)((j & 1 ? bo : be) + 32 * j);
     acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(bf16x8*)&qv, acc0, 0,
                                                    0, 0);
     acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(bf16x8*)&qv, acc1, 0,
@@ -326,51 +301,54 @@ __device__ __forceinline__ void rr_block(const uint16_t* __restrict__ Q, const u
   }
 }
 
-// bf16 cache with d <= 768, any m: 4 waves, each holding its 32
-// cache rows (two 16-row blocks, the whole k range) in registers for the
-// entire query range, so the cache is read from HBM once; 16-query blocks
-// stream through a double-buffered LDS and each query fragment read feeds both
-// row blocks.  Query blocks move global -> LDS without registers, a block
-// ahead.  128-row tiles let two workgroups share a CU, so one loads while the
-// other multiplies.
+// bf16 cache with d <= 768, any m: 4 waves, each holding its 32 cache rows
+// (two 16-row blocks, the whole k range) in registers for the entire query
+// range, so the cache is read from HBM once; 16-query blocks stream through a
+// double-buffered LDS and each query fragment read feeds both row blocks.
+// Query blocks move global -> LDS without registers, a block ahead.  The
+// tile maximum per query comes straight from the accumulators (lane max,
+// two cross-lane steps, one LDS slot per wave), so a query block costs the
+// multiplies and a handful of VALU operations.  128-row tiles let two
+// workgroups share a CU, so one loads while the other multiplies.
+template <int NS>
 __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restrict__ cache,
-                                                          int64_t n, int d, int m, int T,
-                                                          LookupWs ws) {
+                                                          int64_t n, int d, int m, LookupWs ws) {
   extern __shared__ __align__(16) unsigned char smem[];
-  double* sE = (double*)smem;                           // [3][QB] margin factors
-  uint16_t* sQ = (uint16_t*)(smem + 3 * QB * 8);        // [2][QB][d]
-  float* sS = (float*)((char*)sQ + 2 * QB * d * 2);     // [2][QB][SS_RR]
-  float* sN = sS + 2 * QB * SS_RR;                      // [RR_TILE]
+  constexpr int dp = NS * 32;  // == ws.dp
+  uint16_t* sQ = (uint16_t*)smem;                       // [2][QB][dp]
+  float* sM = (float*)((char*)sQ + 2 * QB * dp * 2);    // [2][4 waves][QB]
+  float* sN = sM + 2 * 4 * QB;                          // [RR_TILE]
   const int tile = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, kc = lane >> 4;
   const int64_t row0 = (int64_t)tile * RR_TILE;
   const int rows = (int)min((int64_t)RR_TILE, n - row0);
+  const bool full = rows == RR_TILE;
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(cache + row0 * d, (uint32_t)rows * d * 2);
-  u32x4 a[KS][2];
+  u32x4 a[NS][2];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int rloc = wave * 32 + b * 16 + li;
 #pragma unroll
-    for (int j = 0; j < KS; ++j) {
+    for (int j = 0; j < NS; ++j) {
       const int k = j * 32 + kc * 8;
       const uint32_t off = (rloc < rows && k < d) ? (uint32_t)((rloc * d + k) * 2) : OOB;
       a[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     }
   }
-  // Query blocks 0 and 1 with their margin factors; block i + 2 is requested
-  // right after the barrier of block i (its buffers were last read by block
-  // i's multiplies and block i - 1's tail).
-  dma_queries(sQ, sE, ws, 0, d);
-  if (QB < m) dma_queries(sQ + QB * d, sE + QB, ws, QB, d);
+  // Query blocks 0 and 1; block i + 2 is requested right after the barrier of
+  // block i (its buffer was last read by block i's multiplies).
+  dma_queries(sQ, ws, 0);
+  if (QB < m) dma_queries(sQ + QB * dp, ws, QB);
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     float nn = 0.f;
 #pragma unroll
-    for (int j = 0; j < KS; ++j)
+    for (int j = 0; j < NS; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const bf16x2 v = __builtin_bit_cast(bf16x2, a[j][b][e]);
+        const uint32_t ae = a[j][b][e];  // via a scalar (see the wide scan)
+        const bf16x2 v = __builtin_bit_cast(bf16x2, ae);
         nn = __builtin_amdgcn_fdot2_f32_bf16(v, v, nn, false);
       }
     nn += __shfl_xor(nn, 16, 64);
@@ -379,36 +357,45 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  const int qg = tid / (256 / QB);  // this thread's query within a block (tile tail)
+  write_norm_max<RR_TILE>(sN, rows, tile, ws);
+  // rows of this lane's accumulator entries: wave * 32 + 4 kc + r (+ 16)
+  const int rl = wave * 32 + kc * 4;
   for (int q0 = 0, i = 0; q0 < m; q0 += QB, ++i) {
-    const uint16_t* Q = sQ + (i & 1) * QB * d;
+    const uint16_t* Q = sQ + (i & 1) * QB * dp;
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    rr_block(Q, a, d, li, kc, acc0, acc1);
-    float* S = sS + (i & 1) * QB * SS_RR;
+    rr_block<NS>(Q, a, li, kc, acc0, acc1);
+    float v = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      S[li * SS_RR + wave * 32 + kc * 4 + r] = acc0[r];
-      S[li * SS_RR + wave * 32 + 16 + kc * 4 + r] = acc1[r];
+      v = (full || rl + r < rows) ? fmaxf(v, acc0[r]) : v;
+      v = (full || rl + 16 + r < rows) ? fmaxf(v, acc1[r]) : v;
     }
+    v = fmaxf(v, __shfl_xor(v, 16, 64));
+    v = fmaxf(v, __shfl_xor(v, 32, 64));
+    float* M = sM + (i & 1) * 4 * QB;
+    if (kc == 0) M[wave * QB + li] = v;
     __builtin_amdgcn_s_waitcnt(0);  // this wave's part of block i + 1 has landed
     __syncthreads();
-    if (q0 + 2 * QB < m)
-      dma_queries(sQ + (i & 1) * QB * d, sE + ((i + 2) % 3) * QB, ws, q0 + 2 * QB, d);
-    const double Eq = q0 + qg < m ? sE[(i % 3) * QB + qg] : 0.0;
-    tile_finalize<256, RR_TILE>(S, sN, tile, n, q0, min(QB, m - q0), T, Eq, ws);
+    if (q0 + 2 * QB < m) dma_queries(sQ + (i & 1) * QB * dp, ws, q0 + 2 * QB);
+    // M[] of block i is rewritten by block i + 2, after the barrier of block
+    // i + 1, which these reads precede.
+    if (tid < QB)
+      ws.tmax[(int64_t)tile * ws.mq + q0 + tid] =
+          fmaxf(fmaxf(M[tid], M[QB + tid]), fmaxf(M[2 * QB + tid], M[3 * QB + tid]));
   }
 }
 
 // f32 cache: one thread per row, 16 queries at a time, d in chunks of 256.
 __global__ void __launch_bounds__(256) lk_scan_f32(const float* __restrict__ cache, int64_t n,
                                                    int d, const float* __restrict__ queries, int m,
-                                                   int T, LookupWs ws) {
+                                                   LookupWs ws) {
   __shared__ float sQ[QB * 256];
   __shared__ float sS[2][QB * SS_WIDE];
   __shared__ float sN[TILE];
   const int tile = blockIdx.x;
   const int r = threadIdx.x;
   const int64_t row = (int64_t)tile * TILE + r;
+  const int rows = (int)min((int64_t)TILE, n - (int64_t)tile * TILE);
   const bool rv = row < n;
   const float* crow = cache + (rv ? row : 0) * (int64_t)d;
   for (int q0 = 0; q0 < m; q0 += QB) {
@@ -437,20 +424,30 @@ __global__ void __launch_bounds__(256) lk_scan_f32(const float* __restrict__ cac
     for (int q = 0; q < QB; ++q) S[q * SS_WIDE + r] = acc[q];
     if (q0 == 0) sN[r] = sqrtf(nn * 1.001f);
     __syncthreads();
-    tile_finalize<256, TILE>(S, sN, tile, n, q0, qcount, T, query_margin<256>(ws.E, q0, m), ws);
+    if (q0 == 0) write_norm_max<TILE>(sN, rows, tile, ws);
+    write_tile_max<TILE, SS_WIDE>(S, rows, tile, q0, ws);
   }
 }
 
-// Canonical float64 left-to-right dot of one query (in LDS as double) with a row.
+// Canonical float64 left-to-right dot of one query (in LDS as double) with a
+// row.  Rows are read 64 elements (eight 16-byte loads) ahead of the sums.
 __device__ inline double canon_bf16(const double* qd, const uint16_t* __restrict__ row, int d) {
   double s = 0.0;
-  for (int k = 0; k < d; k += 8) {
-    const uint4 v = *(const uint4*)(row + k);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  for (int k0 = 0; k0 < d; k0 += 64) {
+    uint4 v[8];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      s = fma(qd[k + 2 * e], (double)__uint_as_float(w[e] << 16), s);
-      s = fma(qd[k + 2 * e + 1], (double)__uint_as_float(w[e] & 0xFFFF0000u), s);
+    for (int u = 0; u < 8; ++u)
+      if (k0 + 8 * u < d) v[u] = *(const uint4*)(row + k0 + 8 * u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (k0 + 8 * u >= d) break;
+      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      const int k = k0 + 8 * u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s = fma(qd[k + 2 * e], (double)__uint_as_float(w[e] << 16), s);
+        s = fma(qd[k + 2 * e + 1], (double)__uint_as_float(w[e] & 0xFFFF0000u), s);
+      }
     }
   }
   return s;
@@ -461,6 +458,37 @@ __device__ inline double canon_f32(const double* qd, const float* __restrict__ r
   return s;
 }
 
+// Float64 dot with eight partial sums (any order within 2 d 2^-53 sum|q_k c_k|
+// of the canonical value), used only to rule rows out.
+__device__ inline double fast_bf16(const double* qd, const uint16_t* __restrict__ row, int d) {
+  double p[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int k0 = 0; k0 < d; k0 += 64) {
+    uint4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = k0 + 8 * u < d ? *(const uint4*)(row + k0 + 8 * u) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int k = min(k0 + 8 * u, d - 8);  // past d the row chunk is zero
+      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[2 * e] = fma(qd[k + 2 * e], (double)__uint_as_float(w[e] << 16), p[2 * e]);
+        p[2 * e + 1] = fma(qd[k + 2 * e + 1], (double)__uint_as_float(w[e] & 0xFFFF0000u),
+                           p[2 * e + 1]);
+      }
+    }
+  }
+  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+}
+__device__ inline double fast_f32(const double* qd, const float* __restrict__ row, int d) {
+  double p[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int k = 0; k < d; k += 8)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) p[e] = fma(qd[k + e], (double)row[k + e], p[e]);
+  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+}
+
 __device__ inline void better(double& bs, int64_t& bi, double s, int64_t i) {
   if (s > bs || (s == bs && i < bi)) {
     bs = s;
@@ -468,6 +496,27 @@ __device__ inline void better(double& bs, int64_t& bi, double s, int64_t i) {
   }
 }
 
+// Bounds on the best canonical score of tile t for a query, from the tile's
+// largest scan score M and norm bound N: every row obeys |s~ - s64| <= N E,
+// so max s64 >= M - N E and no row exceeds M + N E.  Evaluated in float64
+// and widened by 2^-40 relative (plus 2^-1000) to cover their own rounding.
+__device__ inline double lower_d(float M, float N, double E) {
+  const double t = (double)M - (double)N * E * (1.0 + 0x1p-40);
+  return t - fma(fabs(t), 0x1p-40, 0x1p-1000);
+}
+__device__ inline double upper_d(float M, float N, double E) {
+  const double t = (double)M + (double)N * E * (1.0 + 0x1p-40);
+  return t + fma(fabs(t), 0x1p-40, 0x1p-1000);
+}
+
+// One workgroup per query.  Pass 1: L = max_t lower_d.  Pass 2, 2048 tiles at
+// a time: the tiles with upper_d >= L are listed in LDS and their rows split
+// over the threads; a row is rescored canonically unless its fast dot plus
+// 2^-40 |q| N_t (a bound on the difference of the two dots, with room)
+// stays below L.  (Max, lowest index) over the rescored rows is the result.
+// Both passes keep eight tile loads in flight per thread.
+constexpr int SEL_U = 8;
+constexpr int SEL_CHUNK = 256 * SEL_U;
 __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queries, int d,
                                                  const void* __restrict__ cache, int cache_bf16,
                                                  int64_t n, int T, int tr, Thresholds th,
@@ -476,55 +525,64 @@ __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queri
                                                  float* __restrict__ sim_out,
                                                  int32_t* __restrict__ k_out) {
   __shared__ double qd[MAX_D];
-  __shared__ double red[8];
-  __shared__ int ovf[OVF_CAP];
-  __shared__ int novf;
+  __shared__ double red[4];
+  __shared__ int list[SEL_CHUNK];
+  __shared__ int nlist;
   __shared__ double rs[4];
   __shared__ int64_t ri[4];
   const int q = blockIdx.x;
-  for (int k = threadIdx.x; k < d; k += 256) qd[k] = (double)queries[(int64_t)q * d + k];
-  if (threadIdx.x == 0) novf = 0;
+  double qq = 0.0;
+  for (int k = threadIdx.x; k < d; k += 256) {
+    const double v = (double)queries[(int64_t)q * d + k];
+    qd[k] = v;
+    qq += v * v;
+  }
+  const double qn = sqrt(block_sum_256(qq, red)) * (1.0 + 0x1p-40);
+  const double E = ws.E[q];
+  const float* tm = ws.tmax + q;
   double L = -INFINITY;
-  for (int t = threadIdx.x; t < T; t += 256) L = fmax(L, ws.tileL[(int64_t)q * T + t]);
+  for (int c0 = 0; c0 < T; c0 += SEL_CHUNK) {
+    float M[SEL_U], N[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int t = c0 + u * 256 + (int)threadIdx.x;
+      M[u] = t < T ? tm[(int64_t)t * ws.mq] : -INFINITY;
+      N[u] = t < T ? ws.nmax[t] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) L = fmax(L, lower_d(M[u], N[u], E));
+  }
   L = block_max_256(L, red);
   double bs = -INFINITY;
   int64_t bi = INT64_MAX;
-  bool full_scan = false;
-  for (int t = threadIdx.x; t < T; t += 256) {
-    if (!(ws.tileU[(int64_t)q * T + t] >= L)) continue;
-    const int c = ws.cnt[(int64_t)q * T + t];
-    if (c <= CAP) {
-      for (int j = 0; j < c; ++j) {
-        const int64_t row = ws.cand[((int64_t)q * T + t) * CAP + j];
-        const double s = cache_bf16
-                             ? canon_bf16(qd, (const uint16_t*)cache + row * (int64_t)d, d)
-                             : canon_f32(qd, (const float*)cache + row * (int64_t)d, d);
-        better(bs, bi, s, row);
-      }
-    } else {
-      const int p = atomicAdd(&novf, 1);
-      if (p < OVF_CAP) ovf[p] = t;
+  for (int c0 = 0; c0 < T; c0 += SEL_CHUNK) {
+    bool pass[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int t = c0 + u * 256 + (int)threadIdx.x;
+      pass[u] = t < T && upper_d(tm[(int64_t)t * ws.mq], ws.nmax[t], E) >= L;
     }
-  }
-  __syncthreads();
-  const int no = novf;
-  full_scan = no > OVF_CAP;
-  if (full_scan) {
-    for (int64_t row = threadIdx.x; row < n; row += 256) {
-      const double s = cache_bf16 ? canon_bf16(qd, (const uint16_t*)cache + row * (int64_t)d, d)
-                                  : canon_f32(qd, (const float*)cache + row * (int64_t)d, d);
-      better(bs, bi, s, row);
-    }
-  } else {
-    for (int o = 0; o < no; ++o) {
-      const int64_t row = (int64_t)ovf[o] * tr + threadIdx.x;
-      if ((int)threadIdx.x < tr && row < n) {
-        const double s = cache_bf16
-                             ? canon_bf16(qd, (const uint16_t*)cache + row * (int64_t)d, d)
-                             : canon_f32(qd, (const float*)cache + row * (int64_t)d, d);
-        better(bs, bi, s, row);
+    if (threadIdx.x == 0) nlist = 0;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u)  // order is irrelevant to (max, lowest index)
+      if (pass[u]) list[atomicAdd(&nlist, 1)] = c0 + u * 256 + (int)threadIdx.x;
+    __syncthreads();
+    const int cnt = nlist;
+    for (int i = threadIdx.x; i < cnt * tr; i += 256) {
+      const int tt = list[i / tr];
+      const int64_t row = (int64_t)tt * tr + i % tr;
+      if (row >= n) continue;
+      const double tol = 0x1p-40 * qn * (double)ws.nmax[tt] + 0x1p-1000;
+      if (cache_bf16) {
+        const uint16_t* c = (const uint16_t*)cache + row * (int64_t)d;
+        if (fast_bf16(qd, c, d) + tol >= L) better(bs, bi, canon_bf16(qd, c, d), row);
+      } else {
+        const float* c = (const float*)cache + row * (int64_t)d;
+        if (fast_f32(qd, c, d) + tol >= L) better(bs, bi, canon_f32(qd, c, d), row);
       }
     }
+    __syncthreads();  // list and nlist are rewritten by the next chunk
   }
   // (max score, lowest index) reduction
   for (int o = 32; o > 0; o >>= 1) {
@@ -561,23 +619,21 @@ __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queri
 }
 
 struct WsPlan {
-  size_t off_qbf, off_E, off_L, off_U, off_cnt, off_cand, total;
+  size_t off_qbf, off_E, off_tmax, off_nmax, total;
 };
 
 // bf16 scans with d <= 768 (register-resident rows) use 128-row tiles, the rest 256.
-inline bool rows_in_registers(int32_t m, int32_t d, bool bf16) { return bf16 && d <= 32 * KS; }
+inline bool rows_in_registers(int32_t d, bool bf16) { return bf16 && d <= 32 * KS; }
 
 WsPlan plan_ws(int32_t m, int64_t n, int32_t d, int tr) {
   WsPlan p{};
   const int64_t T = ceil_div(n, (int64_t)tr);
   const int64_t mq = ceil_div(m, QB) * QB;
   size_t o = 0;
-  p.off_qbf = o;  o = align_up(o + (size_t)mq * d * 2, 256);
+  p.off_qbf = o;  o = align_up(o + (size_t)mq * align_up(d, 64) * 2, 256);
   p.off_E = o;    o = align_up(o + (size_t)mq * 8, 256);
-  p.off_L = o;    o = align_up(o + (size_t)m * T * 8, 256);
-  p.off_U = o;    o = align_up(o + (size_t)m * T * 8, 256);
-  p.off_cnt = o;  o = align_up(o + (size_t)m * T * 4, 256);
-  p.off_cand = o; o = align_up(o + (size_t)m * T * CAP * 4, 256);
+  p.off_tmax = o; o = align_up(o + (size_t)T * mq * 4, 256);
+  p.off_nmax = o; o = align_up(o + (size_t)T * 4, 256);
   p.total = o;
   return p;
 }
@@ -589,8 +645,8 @@ using namespace nv;
 
 extern "C" size_t nv_cache_lookup_workspace(int32_t m, int64_t n, int32_t d) {
   if (m <= 0 || n < 0 || d <= 0) return 0;
-  const size_t small = plan_ws(m, n, d, TILE).total;
-  return rows_in_registers(m, d, true) ? std::max(small, plan_ws(m, n, d, RR_TILE).total) : small;
+  const size_t wide = plan_ws(m, n, d, TILE).total;
+  return rows_in_registers(d, true) ? std::max(wide, plan_ws(m, n, d, RR_TILE).total) : wide;
 }
 
 extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache,
@@ -621,7 +677,7 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
     return NV_ERR_UNSUPPORTED;
   }
   const int bf = c_dtype == NV_BF16;
-  const bool rr = rows_in_registers(m, d, bf);
+  const bool rr = rows_in_registers(d, bf);
   const int tr = rr ? RR_TILE : TILE;
   const WsPlan p = plan_ws(m, n, d, tr);
   if (!workspace || workspace_bytes < p.total || ((uintptr_t)workspace & 255)) {
@@ -630,35 +686,50 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
   }
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)workspace;
-  LookupWs ws{(uint16_t*)(w + p.off_qbf), (double*)(w + p.off_E),  (double*)(w + p.off_L),
-              (double*)(w + p.off_U),     (int32_t*)(w + p.off_cnt), (int32_t*)(w + p.off_cand)};
-  const int T = (int)ceil_div(n, (int64_t)tr);
   const int mq_pad = (int)ceil_div(m, QB) * QB;
-  hipLaunchKernelGGL(lk_prep, dim3(mq_pad), dim3(256), 0, s, queries, m, mq_pad, d, bf, ws.qbf,
+  const int dp = (int)align_up(d, 64);
+  LookupWs ws{(uint16_t*)(w + p.off_qbf), (double*)(w + p.off_E), (float*)(w + p.off_tmax),
+              (float*)(w + p.off_nmax), mq_pad, dp};
+  const int T = (int)ceil_div(n, (int64_t)tr);
+  hipLaunchKernelGGL(lk_prep, dim3(mq_pad), dim3(256), 0, s, queries, m, mq_pad, d, dp, bf, ws.qbf,
                      ws.E);
   NV_LAUNCH_CHECK("lk_prep");
   if (T > 0) {
     if (rr) {
-      const size_t lds =
-          (size_t)3 * QB * 8 + (size_t)2 * QB * d * 2 + (size_t)2 * QB * SS_RR * 4 + RR_TILE * 4;
-      NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      const size_t lds = (size_t)2 * QB * dp * 2 + (size_t)2 * 4 * QB * 4 + RR_TILE * 4;
+      const void* fn = nullptr;
+      switch (dp / 32) {
+#define NV_RR(ns) case ns: fn = (const void*)lk_scan_bf16<ns>; break;
+        NV_RR(2) NV_RR(4) NV_RR(6) NV_RR(8) NV_RR(10) NV_RR(12)
+        NV_RR(14) NV_RR(16) NV_RR(18) NV_RR(20) NV_RR(22) NV_RR(24)
+#undef NV_RR
+      }
+      NV_HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
       const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d);
-      hipExtLaunchKernelGGL(lk_scan_bf16, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
-                            (const uint16_t*)cache, n, (int)d, (int)m, T, ws);
+      const uint16_t* cb = (const uint16_t*)cache;
+      switch (dp / 32) {
+#define NV_RR(ns)                                                                          \
+  case ns:                                                                                 \
+    hipExtLaunchKernelGGL(lk_scan_bf16<ns>, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b, \
+                          0u, cb, n, (int)d, (int)m, ws);                                  \
+    break;
+        NV_RR(2) NV_RR(4) NV_RR(6) NV_RR(8) NV_RR(10) NV_RR(12)
+        NV_RR(14) NV_RR(16) NV_RR(18) NV_RR(20) NV_RR(22) NV_RR(24)
+#undef NV_RR
+      }
       NV_LAUNCH_CHECK("lk_scan_bf16");
     } else if (bf) {
-      const size_t lds = (size_t)QB * d * 2 + (size_t)2 * QB * SS_WIDE * 4 + TILE * 4;
+      const size_t lds = (size_t)QB * dp * 2 + (size_t)2 * QB * SS_WIDE * 4 + TILE * 4;
       NV_HIP_TRY(hipFuncSetAttribute((const void*)lk_scan_bf16_wide,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
       const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 2.0 * (double)n * d);
       hipExtLaunchKernelGGL(lk_scan_bf16_wide, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b,
-                            0u, (const uint16_t*)cache, n, (int)d, (int)m, T, ws);
+                            0u, (const uint16_t*)cache, n, (int)d, (int)m, ws);
       NV_LAUNCH_CHECK("lk_scan_bf16_wide");
     } else {
       const TraceEv ev = trace_begin(NV_FAM_SCAN, 2.0 * m * (double)n * d, 4.0 * (double)n * d);
       hipExtLaunchKernelGGL(lk_scan_f32, dim3(T), dim3(256), 0u, s, ev.a, ev.b, 0u,
-                            (const float*)cache, n, (int)d, queries, (int)m, T, ws);
+                            (const float*)cache, n, (int)d, queries, (int)m, ws);
       NV_LAUNCH_CHECK("lk_scan_f32");
     }
   }

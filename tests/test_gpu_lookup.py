@@ -97,6 +97,32 @@ def test_overflowing_candidate_lists():
     assert gi[0] == 0
 
 
+@pytest.mark.parametrize("d,dtype", [(768, "bf16"), (64, "bf16"), (1024, "bf16"), (768, "f32")])
+def test_scan_rounding_inversion(d, dtype):
+    """The bf16 scan orders two rows the wrong way round; the margins must keep
+    the true best.  Row 0 = 1.0 e_2 scores q_2 = 1.0038 canonically but 1.0 in
+    the scan (q_2 rounds down to bf16 1.0); row 300 = 0.70703125 (e_3 + e_4)
+    scores 1.0030 canonically but 1.0053 in the scan (q_3 = q_4 = 0.7093 round
+    up to 0.7109375).  The nonzeros sit at k % 8 in 2..4, so a row-norm bound
+    that read only part of each 8-element chunk would be 0 and the row-0 tile
+    would be dropped.  Every other row is zero."""
+    print(f"lookup rounding inversion d={d} {dtype}", flush=True)
+    q = np.zeros((1, d), dtype=np.float32)
+    q[0, 2], q[0, 3], q[0, 4] = 1.0038, 0.7093, 0.7093
+    c = np.zeros((400, d), dtype=np.float32)
+    c[0, 2] = 1.0
+    c[300, 3] = c[300, 4] = 0.70703125
+    cache = synth.to_bf16_bits(c) if dtype == "bf16" else c
+    gi, gs, gk = _check(q, cache)
+    assert gi[0] == 0 and gk[0] == 25
+    # the same pair in a cache of unit rows, several queries (m > 1 query block)
+    rng = _rand(4000, d, 17, "f32") * 0.2
+    rng[0], rng[3000] = c[0], c[300]
+    cache = synth.to_bf16_bits(rng) if dtype == "bf16" else rng
+    gi, _, _ = _check(np.repeat(q, 20, axis=0), cache)
+    assert np.all(gi == 0)
+
+
 def test_empty_cache_and_boundaries():
     print("lookup empty + boundaries", flush=True)
     q = _rand(3, 64, 1, "f32")
