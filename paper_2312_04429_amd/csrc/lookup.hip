@@ -13,12 +13,12 @@
 //      of the tile's rows, and once per tile an upper bound N_t on its row
 //      norms.  Nothing else leaves the scan.
 //   2. select: per query, L = max_t (M_tq - N_t E_q) is a lower bound on the
-//      best canonical score, and every row that can reach it lies in a tile
-//      with M_tq + N_t E_q >= L.  Those tiles are read again: a float64 dot
-//      with eight partial sums discards rows that provably cannot reach L;
-//      the rest are rescored with the canonical float64 left-to-right dot
-//      product; the maximum with the lowest index wins; its float32 rounding
-//      goes through the thresholds.
+//      best canonical score (lk_bound), and every row that can reach it lies
+//      in a tile with M_tq + N_t E_q >= L (listed by lk_mark).  Those tiles
+//      are read again (lk_select): a float64 dot in another summation order
+//      discards rows that provably cannot reach L; the rest are rescored with
+//      the canonical float64 left-to-right dot product; the maximum with the
+//      lowest index wins; its float32 rounding goes through the thresholds.
 #include <algorithm>
 #include <cmath>
 
@@ -39,20 +39,39 @@ struct Thresholds {
 };
 
 struct LookupWs {
-  uint16_t* qbf;  // [mq][dp] bf16 bits of the queries, chunk-swizzled (see qpos)
-  double* E;      // [mq] margin factor per query
-  float* tmax;    // [T][mq] largest scan score of each tile, per query
-  float* nmax;    // [T] upper bound on the row norms of each tile
-  int mq;         // m rounded up to a whole query block
-  int dp;         // d rounded up to a multiple of 64 (query row length in qbf)
+  uint16_t* qbf;   // [mq][dp] bf16 bits of the queries, chunk-swizzled (see qpos)
+  double* E;       // [mq] margin factor per query
+  float* tmax;     // [mq / QB][T][QB] largest scan score of each tile, per query
+  float* nmax;     // [T] upper bound on the row norms of each tile
+  uint64_t* Lkey;  // [mq] best lower bound per query, as an ordered key (dkey)
+  int32_t* cnt;    // [mq] tiles listed per query
+  int32_t* list;   // [m][T] tiles whose upper bound reaches the query's lower bound
+  int mq;          // m rounded up to a whole query block
+  int dp;          // d rounded up to a multiple of 128 (query row length in qbf)
+  int T;           // tiles
 };
 
+// Where the scan puts M_tq: query-block major, 16 queries of a tile adjacent.
+__device__ inline int64_t tmax_at(const LookupWs& ws, int q, int tile) {
+  return ((int64_t)(q / QB) * ws.T + tile) * QB + (q % QB);
+}
+
+// Doubles as unsigned keys with the same order (for atomicMax).
+__device__ inline uint64_t dkey(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x);
+  return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+__device__ inline double dkey_inv(uint64_t k) {
+  return __longlong_as_double((long long)((k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k));
+}
+
 // Element offset of k (a multiple of 8) of query row r in a [rows][dp] query
-// block: the 16-byte chunk k / 8 sits at chunk (k / 8) ^ (r & 7) of its row.
-// Rows are dp = 64 j elements long, so the swap stays inside the row, and the
-// eight rows that one 16-byte LDS read by eight lanes touches (same k, rows
-// r..r+7) land on eight different 16-byte bank groups.
-__device__ inline int qpos(int r, int k, int dp) { return r * dp + ((((k >> 3) ^ (r & 7))) << 3); }
+// block: the 16-byte chunk k / 8 sits at chunk (k / 8) ^ (r & 15) of its row.
+// Rows are dp = 128 j elements long, so the swap stays inside the row.  A
+// wave's 16-byte LDS read covers rows 0..15 at four chunk positions; the
+// swap spreads those 64 chunks evenly over the 16 16-byte bank groups of a
+// 256-byte bank line (4 each), which is what a conflict-free read needs.
+__device__ inline int qpos(int r, int k, int dp) { return r * dp + ((((k >> 3) ^ (r & 15))) << 3); }
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -88,14 +107,14 @@ __device__ inline double block_sum_256(double v, double* red) {
 __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int m, int mq_pad,
                                                int d, int dp, int cache_bf16,
                                                uint16_t* __restrict__ qbf,
-                                               double* __restrict__ E) {
+                                               double* __restrict__ E, LookupWs ws) {
   __shared__ double red[3][4];
   const int j = blockIdx.x;
   double e = 0.0, nb = 0.0, nq = 0.0;
   for (int k = threadIdx.x; k < dp; k += 256) {  // zero padding up to dp
     float v = j < m && k < d ? q[(int64_t)j * d + k] : 0.0f;
     uint16_t b = f32_to_bf16_rne(v);
-    qbf[(int64_t)j * dp + ((((k >> 3) ^ (j & 7))) << 3) + (k & 7)] = b;
+    qbf[(int64_t)j * dp + ((((k >> 3) ^ (j & 15))) << 3) + (k & 7)] = b;
     double vb = (double)bf16_to_f32(b);
     double dv = (double)v;
     e += (dv - vb) * (dv - vb);
@@ -113,6 +132,10 @@ __global__ void __launch_bounds__(256) lk_prep(const float* __restrict__ q, int 
     red[2][threadIdx.x >> 6] = nq;
   }
   __syncthreads();
+  if (threadIdx.x == 0) {
+    ws.Lkey[j] = dkey(-INFINITY);
+    ws.cnt[j] = 0;
+  }
   if (threadIdx.x == 0 && j >= m) E[j] = 0.0;  // padding rows of the last query block
   if (threadIdx.x == 0 && j < m) {
     e = red[0][0] + red[0][1] + red[0][2] + red[0][3];
@@ -139,7 +162,7 @@ __device__ inline void write_tile_max(const float* sS, int rows, int tile, int q
   }
 #pragma unroll
   for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  if (sub == 0) ws.tmax[(int64_t)tile * ws.mq + q0 + q] = v;
+  if (sub == 0) ws.tmax[tmax_at(ws, q0 + q, tile)] = v;
 }
 
 // N_t = the largest of the tile's row-norm bounds sN[0..rows) (first wave).
@@ -222,11 +245,13 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
       a[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     }
   };
-  for (int q0 = 0, par = 0; q0 < m; q0 += QB, par ^= 1) {
+  const int nb = (m + QB - 1) / QB, b0 = (tile >> 3) % nb;  // staggered, as in lk_scan_bf16
+  for (int i = 0, par = 0; i < nb; ++i, par ^= 1) {
+    const int q0 = (b0 + i < nb ? b0 + i : b0 + i - nb) * QB;
     __syncthreads();  // every wave is past the previous block's multiplies
     stage_queries(sQ, ws.qbf, q0, dp);
     __syncthreads();
-    const bool norms = q0 == 0;  // row norms during the first query block
+    const bool norms = i == 0;  // row norms during the first query block
     float* S = sS + par * QB * SS_WIDE;
     u32x4 a0[KS], a1[KS];
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -281,31 +306,57 @@ __global__ void __launch_bounds__(256) lk_scan_bf16_wide(const uint16_t* __restr
 // these reads from global -> LDS loads in flight into the other buffer).
 // NS = dp / 32 steps: the padded query row is zero past d, so every read is
 // unconditional and the compiler can run the LDS reads ahead of the multiplies.
+// Two accumulators per row block (even / odd steps) keep four independent
+// multiply chains in flight; the scan bound holds for any summation order.
 template <int NS>
 __device__ __forceinline__ void rr_block(const uint16_t* __restrict__ Q, const u32x4 (&a)[NS][2],
                                          int li, int kc, floatx4& acc0, floatx4& acc1) {
   constexpr int dp = NS * 32;
-  // qpos(li, 32 j + 8 kc, dp) = li dp + 8 (kc ^ (li & 3)) + 32 (j ^ ((li >> 2) & 1)):
-  // even j sit 32 x2 elements past 32 j, odd j 32 x2 before it (x2 = bit 2 of
-  // li), so two base addresses and immediate offsets cover every step.
-  const int x2 = (li >> 2) & 1;
-  const uint16_t* be = Q + li * dp + 8 * (kc ^ (li & 3)) + 32 * x2;
-  const uint16_t* bo = be - 64 * x2;
+  // qpos(li, 32 j + 8 kc, dp) = li dp + 8 (kc ^ (li & 3)) + 32 (j ^ (li >> 2)):
+  // for j = 4 i + r that is 32 j + 32 ((r ^ (li >> 2)) - r) past the row base,
+  // so four base addresses (one per j mod 4) and immediate offsets cover every
+  // step.
+  const int x2 = li >> 2;
+  const uint16_t* b0 = Q + li * dp + 8 * (kc ^ (li & 3));
+  const uint16_t* br[4] = {b0 + 32 * ((0 ^ x2) - 0), b0 + 32 * ((1 ^ x2) - 1),
+                           b0 + 32 * ((2 ^ x2) - 2), b0 + 32 * ((3 ^ x2) - 3)};
+  floatx4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < NS; ++j) {
-    const uint4 qv = *(const uint4*)((j & 1 ? bo : be) + 32 * j);
-    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(bf16x8*)&qv, acc0, 0,
-                                                   0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(bf16x8*)&qv, acc1, 0,
-                                                   0, 0);
+    const uint4 qv = *(const uint4*)(br[j & 3] + 32 * j);
+    floatx4& x0 = (j & 1) ? c0 : acc0;
+    floatx4& x1 = (j & 1) ? c1 : acc1;
+    x0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][0], *(const bf16x8*)&qv, x0,
+                                                 0, 0, 0);
+    x1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)&a[j][1], *(const bf16x8*)&qv, x1,
+                                                 0, 0, 0);
   }
+  acc0 += c0;
+  acc1 += c1;
+}
+
+// s_waitcnt with vmcnt <= N and lgkmcnt == 0 (gfx9 field layout).
+template <int N>
+__device__ inline void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// Barrier without the memory fence of __syncthreads (which would also wait
+// for the query blocks still in flight); callers have waited for what the
+// other waves must see.  The empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ inline void bare_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // bf16 cache with d <= 768, any m: 4 waves, each holding its 32 cache rows
 // (two 16-row blocks, the whole k range) in registers for the entire query
 // range, so the cache is read from HBM once; 16-query blocks stream through a
-// double-buffered LDS and each query fragment read feeds both row blocks.
-// Query blocks move global -> LDS without registers, a block ahead.  The
+// three-deep LDS ring and each query fragment read feeds both row blocks.
+// Query blocks move global -> LDS without registers, two blocks ahead.  The
 // tile maximum per query comes straight from the accumulators (lane max,
 // two cross-lane steps, one LDS slot per wave), so a query block costs the
 // multiplies and a handful of VALU operations.  128-row tiles let two
@@ -314,9 +365,10 @@ template <int NS>
 __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restrict__ cache,
                                                           int64_t n, int d, int m, LookupWs ws) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int dp = NS * 32;  // == ws.dp
-  uint16_t* sQ = (uint16_t*)smem;                       // [2][QB][dp]
-  float* sM = (float*)((char*)sQ + 2 * QB * dp * 2);    // [2][4 waves][QB]
+  constexpr int dp = NS * 32;      // == ws.dp
+  constexpr int DMA = NS / 4;      // global -> LDS requests per wave per query block
+  uint16_t* sQ = (uint16_t*)smem;                       // [3][QB][dp]
+  float* sM = (float*)((char*)sQ + 3 * QB * dp * 2);    // [2][4 waves][QB]
   float* sN = sM + 2 * 4 * QB;                          // [RR_TILE]
   const int tile = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -336,10 +388,19 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
       a[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     }
   }
-  // Query blocks 0 and 1; block i + 2 is requested right after the barrier of
-  // block i (its buffer was last read by block i's multiplies).
-  dma_queries(sQ, ws, 0);
-  if (QB < m) dma_queries(sQ + QB * dp, ws, QB);
+  // Workgroups start at different query blocks ((tile / 8) mod nb) and wrap
+  // around: all CUs reading the same block at once would hot-spot the few L2
+  // channels that hold it.  Iteration i handles block (b0 + i) mod nb; the
+  // blocks of iterations 0..2 go to ring slots 0..2, and the block of
+  // iteration i + 3 is requested right after the barrier of iteration i (its
+  // slot was last read by iteration i's multiplies).  Each wave's requests
+  // complete in issue order.
+  const int nb = (m + QB - 1) / QB;
+  const int b0 = (tile >> 3) % nb;  // tiles t, t + 8, ... share an XCD
+  auto blk = [&](int i) { const int b = b0 + i; return (b >= nb ? b - nb : b) * QB; };
+  dma_queries(sQ, ws, blk(0));
+  if (nb > 1) dma_queries(sQ + QB * dp, ws, blk(1));
+  if (nb > 2) dma_queries(sQ + 2 * QB * dp, ws, blk(2));
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     float nn = 0.f;
@@ -360,8 +421,9 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
   write_norm_max<RR_TILE>(sN, rows, tile, ws);
   // rows of this lane's accumulator entries: wave * 32 + 4 kc + r (+ 16)
   const int rl = wave * 32 + kc * 4;
-  for (int q0 = 0, i = 0; q0 < m; q0 += QB, ++i) {
-    const uint16_t* Q = sQ + (i & 1) * QB * dp;
+  for (int i = 0, slot = 0; i < nb; ++i, slot = slot == 2 ? 0 : slot + 1) {
+    const int q0 = blk(i);
+    const uint16_t* Q = sQ + slot * QB * dp;
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     rr_block<NS>(Q, a, li, kc, acc0, acc1);
     float v = -INFINITY;
@@ -374,15 +436,21 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
     v = fmaxf(v, __shfl_xor(v, 32, 64));
     float* M = sM + (i & 1) * 4 * QB;
     if (kc == 0) M[wave * QB + li] = v;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of block i + 1 has landed
-    __syncthreads();
-    if (q0 + 2 * QB < m) dma_queries(sQ + (i & 1) * QB * dp, ws, q0 + 2 * QB);
+    // This wave's part of block i + 1 has landed once only block i + 2's
+    // requests (if any) may still be in flight; M[] is written.
+    if (i + 2 < nb)
+      wait_vm_lgkm0<DMA>();
+    else
+      wait_vm_lgkm0<0>();
+    bare_barrier();
     // M[] of block i is rewritten by block i + 2, after the barrier of block
     // i + 1, which these reads precede.
     if (tid < QB)
-      ws.tmax[(int64_t)tile * ws.mq + q0 + tid] =
+      ws.tmax[tmax_at(ws, q0 + tid, tile)] =
           fmaxf(fmaxf(M[tid], M[QB + tid]), fmaxf(M[2 * QB + tid], M[3 * QB + tid]));
+    if (i + 3 < nb) dma_queries(sQ + slot * QB * dp, ws, blk(i + 3));
   }
+  __builtin_amdgcn_s_waitcnt(0);
 }
 
 // f32 cache: one thread per row, 16 queries at a time, d in chunks of 256.
@@ -430,16 +498,16 @@ __global__ void __launch_bounds__(256) lk_scan_f32(const float* __restrict__ cac
 }
 
 // Canonical float64 left-to-right dot of one query (in LDS as double) with a
-// row.  Rows are read 64 elements (eight 16-byte loads) ahead of the sums.
+// row.  Rows are read 128 elements (sixteen 16-byte loads) ahead of the sums.
 __device__ inline double canon_bf16(const double* qd, const uint16_t* __restrict__ row, int d) {
   double s = 0.0;
-  for (int k0 = 0; k0 < d; k0 += 64) {
-    uint4 v[8];
+  for (int k0 = 0; k0 < d; k0 += 128) {
+    uint4 v[16];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < 16; ++u)
       if (k0 + 8 * u < d) v[u] = *(const uint4*)(row + k0 + 8 * u);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < 16; ++u) {
       if (k0 + 8 * u >= d) break;
       const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
       const int k = k0 + 8 * u;
@@ -456,37 +524,6 @@ __device__ inline double canon_f32(const double* qd, const float* __restrict__ r
   double s = 0.0;
   for (int k = 0; k < d; ++k) s = fma(qd[k], (double)row[k], s);
   return s;
-}
-
-// Float64 dot with eight partial sums (any order within 2 d 2^-53 sum|q_k c_k|
-// of the canonical value), used only to rule rows out.
-__device__ inline double fast_bf16(const double* qd, const uint16_t* __restrict__ row, int d) {
-  double p[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int k0 = 0; k0 < d; k0 += 64) {
-    uint4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      v[u] = k0 + 8 * u < d ? *(const uint4*)(row + k0 + 8 * u) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int k = min(k0 + 8 * u, d - 8);  // past d the row chunk is zero
-      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        p[2 * e] = fma(qd[k + 2 * e], (double)__uint_as_float(w[e] << 16), p[2 * e]);
-        p[2 * e + 1] = fma(qd[k + 2 * e + 1], (double)__uint_as_float(w[e] & 0xFFFF0000u),
-                           p[2 * e + 1]);
-      }
-    }
-  }
-  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-}
-__device__ inline double fast_f32(const double* qd, const float* __restrict__ row, int d) {
-  double p[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int k = 0; k < d; k += 8)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) p[e] = fma(qd[k + e], (double)row[k + e], p[e]);
-  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
 }
 
 __device__ inline void better(double& bs, int64_t& bi, double s, int64_t i) {
@@ -509,25 +546,123 @@ __device__ inline double upper_d(float M, float N, double E) {
   return t + fma(fabs(t), 0x1p-40, 0x1p-1000);
 }
 
-// One workgroup per query.  Pass 1: L = max_t lower_d.  Pass 2, 2048 tiles at
-// a time: the tiles with upper_d >= L are listed in LDS and their rows split
-// over the threads; a row is rescored canonically unless its fast dot plus
-// 2^-40 |q| N_t (a bound on the difference of the two dots, with room)
-// stays below L.  (Max, lowest index) over the rescored rows is the result.
-// Both passes keep eight tile loads in flight per thread.
-constexpr int SEL_U = 8;
-constexpr int SEL_CHUNK = 256 * SEL_U;
+constexpr int BCH = 256;  // tiles per workgroup of lk_bound / lk_mark
+
+// Grid (tile chunks of BCH, query blocks).  Thread (r, qi) = (tid / 16,
+// tid % 16) reads tiles r, r + 16, ... of its chunk for query qi, so a
+// 16-thread group reads one contiguous 64-byte row of tmax.  Eight tiles are
+// loaded before they are used (two rounds per thread).
+template <typename F>
+__device__ inline void for_chunk_tiles(const LookupWs& ws, int q, F&& f) {
+  const int r = threadIdx.x >> 4;
+  const int t0 = blockIdx.x * BCH, t1 = min(ws.T, t0 + BCH);
+  for (int tb = t0 + r; tb < t1; tb += 128) {
+    float M[8], N[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = tb + 16 * u;
+      M[u] = t < t1 ? ws.tmax[tmax_at(ws, q, t)] : -INFINITY;
+      N[u] = t < t1 ? ws.nmax[t] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (tb + 16 * u < t1) f(tb + 16 * u, M[u], N[u]);
+  }
+}
+
+// L_q = max over tiles of lower_d, folded across workgroups with atomicMax on
+// the ordered key.
+__global__ void __launch_bounds__(256) lk_bound(int m, LookupWs ws) {
+  __shared__ double red[4][QB];
+  const int qi = threadIdx.x & 15, q = blockIdx.y * QB + qi;
+  const double E = q < m ? ws.E[q] : 0.0;
+  double L = -INFINITY;
+  if (q < m) for_chunk_tiles(ws, q, [&](int, float M, float N) { L = fmax(L, lower_d(M, N, E)); });
+  L = fmax(L, __shfl_xor(L, 16, 64));
+  L = fmax(L, __shfl_xor(L, 32, 64));
+  if ((threadIdx.x & 63) < QB) red[threadIdx.x >> 6][qi] = L;
+  __syncthreads();
+  if (threadIdx.x < QB && q < m) {
+    L = fmax(fmax(red[0][qi], red[1][qi]), fmax(red[2][qi], red[3][qi]));
+    atomicMax((unsigned long long*)&ws.Lkey[q], (unsigned long long)dkey(L));
+  }
+}
+
+// Lists every tile with upper_d >= L_q (any order) for the rescan.
+__global__ void __launch_bounds__(256) lk_mark(int m, LookupWs ws) {
+  const int qi = threadIdx.x & 15, q = blockIdx.y * QB + qi;
+  if (q >= m) return;
+  const double E = ws.E[q], L = dkey_inv(ws.Lkey[q]);
+  for_chunk_tiles(ws, q, [&](int t, float M, float N) {
+    if (upper_d(M, N, E) >= L) ws.list[(int64_t)q * ws.T + atomicAdd(&ws.cnt[q], 1)] = t;
+  });
+}
+
+// Eight products of a row chunk (8 elements from k) with the query in LDS.
+__device__ inline void chunk_dot(const double* qd, const uint16_t* __restrict__ row, int k,
+                                 double& p0, double& p1, const uint4& v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    p0 = fma(qd[k + 2 * e], (double)__uint_as_float(w[e] << 16), p0);
+    p1 = fma(qd[k + 2 * e + 1], (double)__uint_as_float(w[e] & 0xFFFF0000u), p1);
+  }
+}
+
+// Float64 dot of a row by the 8 lanes of a group: lane l8 takes the chunks
+// l8, l8 + 8, ... (8 elements each, so the group reads 128 contiguous bytes
+// of a bf16 row per step), two partial sums per lane, then a butterfly over
+// the group.  Some order of the same exact products as the canonical sum, so
+// the two differ by at most 2 d 2^-53 sum |q_k c_k|; used only to rule rows
+// out.
+__device__ inline double group_dot_bf16(const double* qd, const uint16_t* __restrict__ row, int d,
+                                        int l8) {
+  double p0 = 0.0, p1 = 0.0;
+  const int nch = d >> 3;
+  for (int c0 = l8; c0 < nch; c0 += 96) {  // one round for d <= 768
+    uint4 v[12];
+#pragma unroll
+    for (int u = 0; u < 12; ++u)
+      if (c0 + 8 * u < nch) v[u] = *(const uint4*)(row + 8 * (c0 + 8 * u));
+#pragma unroll
+    for (int u = 0; u < 12; ++u)
+      if (c0 + 8 * u < nch) chunk_dot(qd, row, 8 * (c0 + 8 * u), p0, p1, v[u]);
+  }
+  double s = p0 + p1;
+  s += __shfl_xor(s, 1, 64);
+  s += __shfl_xor(s, 2, 64);
+  s += __shfl_xor(s, 4, 64);
+  return s;
+}
+__device__ inline double group_dot_f32(const double* qd, const float* __restrict__ row, int d,
+                                       int l8) {
+  double p0 = 0.0, p1 = 0.0;
+  for (int k = l8 * 8; k < d; k += 64)
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      p0 = fma(qd[k + e], (double)row[k + e], p0);
+      p1 = fma(qd[k + e + 1], (double)row[k + e + 1], p1);
+    }
+  double s = p0 + p1;
+  s += __shfl_xor(s, 1, 64);
+  s += __shfl_xor(s, 2, 64);
+  s += __shfl_xor(s, 4, 64);
+  return s;
+}
+
+// One workgroup per query: the rows of the listed tiles go to 32 groups of 8
+// lanes; a row is rescored canonically (by the group's first lane) unless its
+// group dot plus 2^-40 |q| N_t (a bound on the difference of the two dots,
+// with room) stays below L.  (Max, lowest index) over the rescored rows is
+// the result; its float32 rounding goes through the thresholds.
 __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queries, int d,
                                                  const void* __restrict__ cache, int cache_bf16,
-                                                 int64_t n, int T, int tr, Thresholds th,
-                                                 LookupWs ws,
+                                                 int64_t n, int tr, Thresholds th, LookupWs ws,
                                                  int64_t* __restrict__ idx_out,
                                                  float* __restrict__ sim_out,
                                                  int32_t* __restrict__ k_out) {
   __shared__ double qd[MAX_D];
   __shared__ double red[4];
-  __shared__ int list[SEL_CHUNK];
-  __shared__ int nlist;
   __shared__ double rs[4];
   __shared__ int64_t ri[4];
   const int q = blockIdx.x;
@@ -538,51 +673,26 @@ __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queri
     qq += v * v;
   }
   const double qn = sqrt(block_sum_256(qq, red)) * (1.0 + 0x1p-40);
-  const double E = ws.E[q];
-  const float* tm = ws.tmax + q;
-  double L = -INFINITY;
-  for (int c0 = 0; c0 < T; c0 += SEL_CHUNK) {
-    float M[SEL_U], N[SEL_U];
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int t = c0 + u * 256 + (int)threadIdx.x;
-      M[u] = t < T ? tm[(int64_t)t * ws.mq] : -INFINITY;
-      N[u] = t < T ? ws.nmax[t] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) L = fmax(L, lower_d(M[u], N[u], E));
-  }
-  L = block_max_256(L, red);
+  const double L = dkey_inv(ws.Lkey[q]);
+  const int64_t rows = (int64_t)ws.cnt[q] * tr;
+  const int32_t* lst = ws.list + (int64_t)q * ws.T;
+  const int g = threadIdx.x >> 3, l8 = threadIdx.x & 7;
   double bs = -INFINITY;
   int64_t bi = INT64_MAX;
-  for (int c0 = 0; c0 < T; c0 += SEL_CHUNK) {
-    bool pass[SEL_U];
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int t = c0 + u * 256 + (int)threadIdx.x;
-      pass[u] = t < T && upper_d(tm[(int64_t)t * ws.mq], ws.nmax[t], E) >= L;
+  for (int64_t i = g; i < rows; i += 32) {
+    const int tt = lst[i / tr];
+    const int64_t row = (int64_t)tt * tr + i % tr;
+    if (row >= n) continue;  // uniform in the group
+    const double tol = 0x1p-40 * qn * (double)ws.nmax[tt] + 0x1p-1000;
+    if (cache_bf16) {
+      const uint16_t* c = (const uint16_t*)cache + row * (int64_t)d;
+      if (group_dot_bf16(qd, c, d, l8) + tol >= L && l8 == 0)
+        better(bs, bi, canon_bf16(qd, c, d), row);
+    } else {
+      const float* c = (const float*)cache + row * (int64_t)d;
+      if (group_dot_f32(qd, c, d, l8) + tol >= L && l8 == 0)
+        better(bs, bi, canon_f32(qd, c, d), row);
     }
-    if (threadIdx.x == 0) nlist = 0;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u)  // order is irrelevant to (max, lowest index)
-      if (pass[u]) list[atomicAdd(&nlist, 1)] = c0 + u * 256 + (int)threadIdx.x;
-    __syncthreads();
-    const int cnt = nlist;
-    for (int i = threadIdx.x; i < cnt * tr; i += 256) {
-      const int tt = list[i / tr];
-      const int64_t row = (int64_t)tt * tr + i % tr;
-      if (row >= n) continue;
-      const double tol = 0x1p-40 * qn * (double)ws.nmax[tt] + 0x1p-1000;
-      if (cache_bf16) {
-        const uint16_t* c = (const uint16_t*)cache + row * (int64_t)d;
-        if (fast_bf16(qd, c, d) + tol >= L) better(bs, bi, canon_bf16(qd, c, d), row);
-      } else {
-        const float* c = (const float*)cache + row * (int64_t)d;
-        if (fast_f32(qd, c, d) + tol >= L) better(bs, bi, canon_f32(qd, c, d), row);
-      }
-    }
-    __syncthreads();  // list and nlist are rewritten by the next chunk
   }
   // (max score, lowest index) reduction
   for (int o = 32; o > 0; o >>= 1) {
@@ -619,7 +729,7 @@ __global__ void __launch_bounds__(256) lk_select(const float* __restrict__ queri
 }
 
 struct WsPlan {
-  size_t off_qbf, off_E, off_tmax, off_nmax, total;
+  size_t off_qbf, off_E, off_tmax, off_nmax, off_Lkey, off_cnt, off_list, total;
 };
 
 // bf16 scans with d <= 768 (register-resident rows) use 128-row tiles, the rest 256.
@@ -630,10 +740,13 @@ WsPlan plan_ws(int32_t m, int64_t n, int32_t d, int tr) {
   const int64_t T = ceil_div(n, (int64_t)tr);
   const int64_t mq = ceil_div(m, QB) * QB;
   size_t o = 0;
-  p.off_qbf = o;  o = align_up(o + (size_t)mq * align_up(d, 64) * 2, 256);
+  p.off_qbf = o;  o = align_up(o + (size_t)mq * align_up(d, 128) * 2, 256);
   p.off_E = o;    o = align_up(o + (size_t)mq * 8, 256);
   p.off_tmax = o; o = align_up(o + (size_t)T * mq * 4, 256);
   p.off_nmax = o; o = align_up(o + (size_t)T * 4, 256);
+  p.off_Lkey = o; o = align_up(o + (size_t)mq * 8, 256);
+  p.off_cnt = o;  o = align_up(o + (size_t)mq * 4, 256);
+  p.off_list = o; o = align_up(o + (size_t)m * T * 4, 256);
   p.total = o;
   return p;
 }
@@ -687,21 +800,21 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)workspace;
   const int mq_pad = (int)ceil_div(m, QB) * QB;
-  const int dp = (int)align_up(d, 64);
-  LookupWs ws{(uint16_t*)(w + p.off_qbf), (double*)(w + p.off_E), (float*)(w + p.off_tmax),
-              (float*)(w + p.off_nmax), mq_pad, dp};
+  const int dp = (int)align_up(d, 128);
   const int T = (int)ceil_div(n, (int64_t)tr);
+  LookupWs ws{(uint16_t*)(w + p.off_qbf), (double*)(w + p.off_E), (float*)(w + p.off_tmax),
+              (float*)(w + p.off_nmax),   (uint64_t*)(w + p.off_Lkey), (int32_t*)(w + p.off_cnt),
+              (int32_t*)(w + p.off_list), mq_pad, dp, T};
   hipLaunchKernelGGL(lk_prep, dim3(mq_pad), dim3(256), 0, s, queries, m, mq_pad, d, dp, bf, ws.qbf,
-                     ws.E);
+                     ws.E, ws);
   NV_LAUNCH_CHECK("lk_prep");
   if (T > 0) {
     if (rr) {
-      const size_t lds = (size_t)2 * QB * dp * 2 + (size_t)2 * 4 * QB * 4 + RR_TILE * 4;
+      const size_t lds = (size_t)3 * QB * dp * 2 + (size_t)2 * 4 * QB * 4 + RR_TILE * 4;
       const void* fn = nullptr;
       switch (dp / 32) {
 #define NV_RR(ns) case ns: fn = (const void*)lk_scan_bf16<ns>; break;
-        NV_RR(2) NV_RR(4) NV_RR(6) NV_RR(8) NV_RR(10) NV_RR(12)
-        NV_RR(14) NV_RR(16) NV_RR(18) NV_RR(20) NV_RR(22) NV_RR(24)
+        NV_RR(4) NV_RR(8) NV_RR(12) NV_RR(16) NV_RR(20) NV_RR(24)
 #undef NV_RR
       }
       NV_HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
@@ -713,8 +826,7 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
     hipExtLaunchKernelGGL(lk_scan_bf16<ns>, dim3(T), dim3(256), (uint32_t)lds, s, ev.a, ev.b, \
                           0u, cb, n, (int)d, (int)m, ws);                                  \
     break;
-        NV_RR(2) NV_RR(4) NV_RR(6) NV_RR(8) NV_RR(10) NV_RR(12)
-        NV_RR(14) NV_RR(16) NV_RR(18) NV_RR(20) NV_RR(22) NV_RR(24)
+        NV_RR(4) NV_RR(8) NV_RR(12) NV_RR(16) NV_RR(20) NV_RR(24)
 #undef NV_RR
       }
       NV_LAUNCH_CHECK("lk_scan_bf16");
@@ -733,7 +845,14 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
       NV_LAUNCH_CHECK("lk_scan_f32");
     }
   }
-  hipLaunchKernelGGL(lk_select, dim3(m), dim3(256), 0, s, queries, d, cache, bf, n, T, tr, th, ws,
+  if (T > 0) {
+    const dim3 grid((unsigned)ceil_div(T, BCH), (unsigned)(mq_pad / QB));
+    hipLaunchKernelGGL(lk_bound, grid, dim3(256), 0, s, (int)m, ws);
+    NV_LAUNCH_CHECK("lk_bound");
+    hipLaunchKernelGGL(lk_mark, grid, dim3(256), 0, s, (int)m, ws);
+    NV_LAUNCH_CHECK("lk_mark");
+  }
+  hipLaunchKernelGGL(lk_select, dim3(m), dim3(256), 0, s, queries, d, cache, bf, n, tr, th, ws,
                      idx_out, sim_out, k_out);
   NV_LAUNCH_CHECK("lk_select");
   return NV_OK;
