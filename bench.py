@@ -57,7 +57,6 @@ def unet_flops_per_row(cfg):
     td = 4 * c0
     H, W = cfg["H"], cfg["W"]
     fl += 2 * c0 * td + 2 * td * td                       # time MLP
-    fl += 2 * cfg.get("pooled_dim", 0) * td                 # pooled vector -> time embedding
     fl += 2 * H * W * c0 * 9 * cfg["in_ch"]                 # conv_in
     specs = synth.param_specs(cfg)
     # walk the topology with spatial sizes
