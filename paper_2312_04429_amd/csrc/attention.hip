@@ -51,16 +51,22 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   const int q0 = qblk * (64 * QB) + wave * (16 * QB);
 
   // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8,
-  // zero past DH.
+  // zero past DH, scaled by scale * log2(e) so the scores come out of the
+  // multiply in the base-2 exponent domain.
+  const float sc = a.scale * LOG2E;
   half8 fq[QB][N32];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int q = q0 + qb * 16 + li;
     const _Float16* qrow = a.q + ((int64_t)row * a.S + (q < a.S ? q : 0)) * a.ldq + head * DH;
 #pragma unroll
-    for (int ks = 0; ks < N32; ++ks)
-      fq[qb][ks] = (q < a.S && ks * 32 + kc * 8 < DH) ? *(const half8*)(qrow + ks * 32 + kc * 8)
-                                                      : half8{};
+    for (int ks = 0; ks < N32; ++ks) {
+      half8 v = (q < a.S && ks * 32 + kc * 8 < DH) ? *(const half8*)(qrow + ks * 32 + kc * 8)
+                                                   : half8{};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (_Float16)((float)v[e] * sc);
+      fq[qb][ks] = v;
+    }
   }
 
   floatx4 acc[QB][DV / 16];
@@ -74,7 +80,9 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     mrun[qb] = -INFINITY;
     lrun[qb] = 0.f;
   }
-  const float sc = a.scale * LOG2E;
+  // When the head dim leaves a spare V^T row (DV > DH), that row holds ones:
+  // the same multiply then accumulates the softmax denominator in O^T row DH.
+  constexpr bool ONES = DV > DH;
 
   const _Float16* kbase = a.k + (int64_t)row * a.L * a.ldk + head * DH;
   const _Float16* vtbase = a.vt + (int64_t)head * DH * a.vt_ld + (int64_t)row * a.vt_row;
@@ -147,37 +155,59 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
           s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
       }
     }
-    const bool tail = (kb + 1) * KB > a.L;
-    half8 fp[QB][2];
+    // Keys past L (last block only) score -inf.
+    if ((kb + 1) * KB > a.L) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kb * KB + h * 16 + kc * 4 + r >= a.L) s[qb][h][r] = -INFINITY;
+    }
+    // Online softmax with a lazily moved reference: while no score of the wave
+    // exceeds its query's reference max by more than 2^RESCALE_LOG2 (p stays
+    // <= 256, exact enough in float16), the reference stays and nothing is
+    // rescaled; otherwise every lane moves to its new max and rescales.
+    constexpr float RESCALE_LOG2 = 8.0f;
+    float mloc[QB];
+    bool grow = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float mloc = -INFINITY;
+      float m = -INFINITY;
 #pragma unroll
       for (int h = 0; h < 4; ++h)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float v = s[qb][h][r] * sc;
-          if (tail && kb * KB + h * 16 + kc * 4 + r >= a.L) v = -INFINITY;
-          s[qb][h][r] = v;
-          mloc = fmaxf(mloc, v);
-        }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float mnew = fmaxf(mrun[qb], mloc);
-      const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
-      mrun[qb] = mnew;
+        for (int r = 0; r < 4; ++r) m = fmaxf(m, s[qb][h][r]);
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      mloc[qb] = m;
+      grow |= !(m <= mrun[qb] + RESCALE_LOG2);  // also true while mrun is -inf
+    }
+    if (__ballot(grow)) {  // uniform: the whole wave moves its references
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const float mnew = fmaxf(mrun[qb], mloc[qb]);
+        const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
+        mrun[qb] = mnew;
+        lrun[qb] *= alpha;
+#pragma unroll
+        for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
+      }
+    }
+    half8 fp[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
       float psum = 0.f;
 #pragma unroll
       for (int h = 0; h < 4; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[qb][h][r] - mnew);
-          psum += p;
+          const float p = __builtin_amdgcn_exp2f(s[qb][h][r] - mrun[qb]);
+          if (!ONES) psum += p;
           fp[qb][h >> 1][(h & 1) * 4 + r] = (_Float16)p;
         }
-      lrun[qb] = lrun[qb] * alpha + psum;
-#pragma unroll
-      for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
+      if (!ONES) lrun[qb] += psum;
     }
     // O^T += V^T P^T over two 32-key steps (rows d >= DH of the tile are never
     // written; they only feed output rows that are not stored)
@@ -199,6 +229,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     if (kb + 1 < nkb) stash(cur ^ 1, kb + 1, Sk, Sv);
     __syncthreads();
   };
+  if (ONES)
+    for (int i = tid; i < 2 * KB; i += 256) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
   fetch(0, rkA, rvA);
   if (1 < nkb) fetch(1, rkB, rvB);
   stash(0, 0, rkA, rvA);
@@ -209,9 +241,14 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    float l = lrun[qb];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    float l;
+    if (ONES) {  // O^T row DH: lanes with kc == (DH % 16) / 4 hold it in register DH % 4
+      l = __shfl(acc[qb][DH / 16][DH % 4], (((DH % 16) / 4) << 4) | li, 64);
+    } else {
+      l = lrun[qb];
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+    }
     const int q = q0 + qb * 16 + li;
     if (q >= a.S) continue;
     const float inv = 1.0f / l;
