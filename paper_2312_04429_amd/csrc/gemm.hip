@@ -859,8 +859,10 @@ hipError_t launch(const GemmArgs& g, int splits, hipStream_t s) {
 // 64 x 64 tiles with a three-deep ring by default (inside the network the
 // weights arrive cold from HBM, where the third buffer pays); K is split when it is long
 // (>= 40 tiles) or the grid is tiny, keeping >= MIN_KT tiles per split and
-// about 700 workgroups at most.  Large grids take 64 x 128 (wide N) or
-// 128 x 128 tiles; a long K over a mid-sized grid takes split 128 x 128.
+// about 700 workgroups at most.  Large grids take 128 x 128 tiles for very
+// wide (N >= 2560) or very deep (K >= 8192) products and the 320-channel
+// convolutions, 64 x 128 otherwise; a long K over a mid-sized grid takes
+// split 128 x 128.
 template <int MODE>
 hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   constexpr int MIN_KT = 10;
@@ -875,9 +877,14 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
       ++sp;
     return sp;
   };
-  if (t64 >= 1024)
-    return g.N >= 1024 ? launch_s<MODE, 64, 128, 2>(g, 1, s)
-                       : launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s);
+  if (t64 >= 1024) {
+    // large grids: 128 x 128 for very wide or very deep products and for the
+    // narrow 320-channel convolutions, 64 x 128 otherwise (graph-timed on the
+    // batched SD-1.5 and SDXL shapes)
+    const bool big = g.N >= 2560 || g.K >= 8192 || g.N <= 320;
+    return big ? launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s)
+               : launch_s<MODE, 64, 128, 2>(g, 1, s);
+  }
   if (t128 >= 128 && nk >= 128)
     return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 512), s);
   const bool split = nk >= 40 || t64 < 128;
