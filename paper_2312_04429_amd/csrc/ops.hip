@@ -431,6 +431,89 @@ __global__ void permute_k(StepArgs st, const float* __restrict__ src, float* __r
     dst[(int64_t)st.perm[b] * per_sample + e] = src[i];
 }
 
+// GroupNorm in one launch when a group fits in one workgroup's registers:
+// one 1024-thread workgroup per (row, group).  Thread t owns channel pair
+// t % vpp of the group (vpp = cg / 2) for pixels t / vpp + j * P (P = 1024 /
+// vpp), so its addresses advance by a constant and its affine parameters are
+// loaded once.  It holds the group's values in registers, takes the mean and
+// then the sum of squared deviations from it (two exact passes, each a
+// fixed-order block reduction), and writes the normalised, affine-mapped
+// (optionally SiLU) values: one read and one write of the activation, no
+// partials, no second launch.
+constexpr int GN1_T = 1024;
+constexpr int GN1_NV = 32;  // pixels per thread at most (more would spill)
+
+__device__ inline float block_sum_1024(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = 0.f;
+#pragma unroll
+  for (int w = 0; w < GN1_T / 64; ++w) r += red[w];
+  return r;
+}
+
+__device__ inline float h_lo(uint32_t u) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
+}
+__device__ inline float h_hi(uint32_t u) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
+}
+
+template <int NV>
+__global__ void __launch_bounds__(GN1_T) gn_group_k(GnArgs a) {
+  __shared__ float red[GN1_T / 64];
+  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
+  const int row = blockIdx.x / a.G, g = blockIdx.x % a.G;
+  const int t = threadIdx.x;
+  const bool on = t < P * vpp;
+  const int v = on ? t % vpp : 0, p0 = on ? t / vpp : 0;
+  const int c = g * cg + 2 * v;
+  const bool first = c < a.C1;
+  const int ld = first ? a.C1 : a.C2;
+  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
+                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
+  uint32_t x[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = p0 + j * P;
+    x[j] = (on && p < a.HW) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
+  }
+  float s1 = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) s1 += h_lo(x[j]) + h_hi(x[j]);  // absent pixels are zero
+  const float n = (float)a.HW * (float)cg;
+  const float mean = block_sum_1024(s1, red) / n;
+  float s2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    if (on && p0 + j * P < a.HW) {
+      const float d0 = h_lo(x[j]) - mean, d1 = h_hi(x[j]) - mean;
+      s2 += d0 * d0 + d1 * d1;
+    }
+  }
+  const float rstd = rsqrtf(block_sum_1024(s2, red) / n + a.eps);
+  if (!on) return;
+  const float k0 = rstd * a.gamma[c], k1 = rstd * a.gamma[c + 1];
+  const float f0 = a.beta[c] - mean * k0, f1 = a.beta[c + 1] - mean * k1;
+  _Float16* dst = a.out + (int64_t)row * a.HW * C + c;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = p0 + j * P;
+    if (p >= a.HW) continue;
+    float y0 = fmaf(h_lo(x[j]), k0, f0), y1 = fmaf(h_hi(x[j]), k1, f1);
+    if (a.silu) {
+      y0 = silu(y0);
+      y1 = silu(y1);
+    }
+    *(uint32_t*)(dst + (int64_t)p * C) =
+        (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y0) |
+        ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y1) << 16);
+  }
+}
+
 inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
 
 }  // namespace
@@ -439,6 +522,21 @@ hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
   const int C = a.C1 + a.C2;
   if (a.G < 4 || a.G > 256 || (a.G & (a.G - 1)) || C % a.G || C % 8 || C > GN_MAXC)
     return hipErrorInvalidValue;
+  const int cg = C / a.G;
+  if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / 2 <= GN1_T) {
+    const int P = GN1_T / (cg / 2);                  // pixels per round
+    const int nv = (int)ceil_div(a.HW, P);           // rounds
+    if (nv <= GN1_NV) {
+      const dim3 grid((unsigned)(rows * a.G)), blk(GN1_T);
+      if (nv <= 4)
+        hipLaunchKernelGGL(gn_group_k<4>, grid, blk, 0, s, a);
+      else if (nv <= 16)
+        hipLaunchKernelGGL(gn_group_k<16>, grid, blk, 0, s, a);
+      else
+        hipLaunchKernelGGL(gn_group_k<GN1_NV>, grid, blk, 0, s, a);
+      return hipGetLastError();
+    }
+  }
   const GnShape sh = gn_shape(C);
   const int nchunks = (int)ceil_div(a.HW, sh.P);
   if (nchunks > a.part_chunks) return hipErrorInvalidValue;  // partial scratch too small
