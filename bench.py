@@ -190,18 +190,23 @@ def build_lookup_inputs(wl, B, args, dev, torch, synth):
     if n > 2_000_000:  # too large for the host generator: drawn on the device, same recipe
         d_cache = synth.make_cache_device(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"], dev)
         cache = None
-        host_rows = lambda r: d_cache[torch.from_numpy(np.asarray(r, dtype=np.int64)).to(dev)] \
-            .view(torch.int16).cpu().numpy().view(np.uint16)
+        rows_f32 = lambda r: synth.from_bf16_bits(
+            d_cache[torch.from_numpy(np.asarray(r, dtype=np.int64)).to(dev)]
+            .view(torch.int16).cpu().numpy().view(np.uint16))
+    elif wl.get("cache_dtype") == "f32":
+        cache = synth.make_cache(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"], "f32")
+        d_cache = torch.from_numpy(cache).to(dev)
+        rows_f32 = lambda r: cache[np.asarray(r)]
     else:
         cache = synth.make_cache(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"])
         d_cache = torch.from_numpy(cache.view(np.int16)).to(dev)
-        host_rows = lambda r: cache[np.asarray(r)]
+        rows_f32 = lambda r: synth.from_bf16_bits(cache[np.asarray(r)])
     if "n_queries" in wl:  # retrieval-heavy: half planted (s in [0.95, 0.999]), half fresh draws
         m = wl["n_queries"]
         rng = np.random.default_rng(wl["query_seed"])
         planted = rng.choice(n, m // 2, replace=False)
-        near = synth.make_queries_at_sims(synth.from_bf16_bits(host_rows(planted)),
-                                          rng.uniform(0.95, 0.999, m // 2), wl["query_seed"])
+        near = synth.make_queries_at_sims(rows_f32(planted), rng.uniform(0.95, 0.999, m // 2),
+                                          wl["query_seed"])
         mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev).cpu().numpy()
         far = synth.cluster_queries_from(mu, m - m // 2, wl["sigma"], wl["query_seed"] + 1)
         q = np.empty((m, d), dtype=np.float32)
@@ -211,12 +216,11 @@ def build_lookup_inputs(wl, B, args, dev, torch, synth):
     if args.k is not None:
         sims = [BAND[args.k]] * B
     elif "query_sims" in wl:
-        sims = list(wl["query_sims"])
+        sims = list(wl["query_sims"])[:B]
     else:  # each sample's K drawn from the selector's K values, similarity inside its band
         ks = synth.make_k_values(B, sorted(k for k in BAND if k), wl["k_seed"])
         sims = [BAND[int(k)] for k in ks]
-    rows = host_rows(target)
-    q = synth.make_queries_at_sims(synth.from_bf16_bits(rows), sims, wl["query_seed"])
+    q = synth.make_queries_at_sims(rows_f32(target), sims, wl["query_seed"])
     return d_cache, cache, q, list(range(B))
 
 
@@ -364,6 +368,16 @@ def main():
                            "frac": d["tflops"] / (MFMA_PEAK_F16 / 1e12), "traffic": traffic_for(dom),
                            "launches_per_step": d["launches"] / args.steps,
                            "avg_launch_us": d["avg_us"]}
+    # achieved peaks on this GPU (matrix-core probe, device copy), reported beside the
+    # published ones
+    pk = P.nv_probe_peaks(dev)
+    out["peaks_measured"] = {"mfma_f16_tflops": pk["f16_tflops"], "mfma_bf16_tflops": pk["bf16_tflops"],
+                             "hbm_read_gbps": pk["hbm_read_gbps"]}
+    if out["roofline"]:
+        r = out["roofline"]
+        meas = pk["hbm_read_gbps"] if r["bound"] == "hbm" else pk["f16_tflops"]
+        r["peak_measured"] = meas
+        r["frac_of_measured"] = r["achieved"] / meas
     if args.calib_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         dst = src * 2.0                      # reads 1 GiB, writes 1 GiB
@@ -420,6 +434,9 @@ def scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
            "hbm_frac_scan_kernel": kby / (kms * 1e-3) / HBM_PEAK,
            "hbm_frac_lookup_warm": nbytes / (warm * 1e-3) / HBM_PEAK,
            "hbm_frac_lookup_cold": nbytes / (cold * 1e-3) / HBM_PEAK}
+    pk = P.nv_probe_peaks(dev)
+    out["hbm_read_gbps_measured"] = pk["hbm_read_gbps"]
+    out["hbm_frac_scan_kernel_of_measured"] = kby / (kms * 1e-3) / 1e9 / pk["hbm_read_gbps"]
     print(json.dumps(out))
 
 

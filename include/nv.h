@@ -252,6 +252,22 @@ int32_t nv_trace_disable(void);
 int32_t nv_trace_read(int32_t family, int64_t* launches, double* ms, double* flops,
                       double* bytes);
 
+/* ------------------------------------------------------------------------ *
+ * Matrix-core throughput probe (measurement support, not part of the path).
+ * Launches `blocks` workgroups of 256 threads; every wave issues iters x 8
+ * independent v_mfma_f32_16x16x32_{f16,bf16} (bf16 != 0 selects bf16) on
+ * register operands, i.e. blocks * 4 * iters * 8 * 16384 FLOPs.  Time it with
+ * events on `stream` to obtain the achieved dense matrix peak.  sink: device
+ * float[256], never written in practice (keeps the work live).
+ * Errors: NV_ERR_INVALID_ARG for a null sink or non-positive sizes.
+ * ------------------------------------------------------------------------ */
+int32_t nv_probe_mfma(int32_t bf16, int32_t iters, int32_t blocks, float* sink, void* stream);
+/* HBM read probe: reads bytes / 16 16-byte chunks of the device buffer buf
+ * once (`blocks` workgroups of 256 threads, grid-stride); time it with events
+ * for the achieved read bandwidth.  sink as above.  Errors: NV_ERR_INVALID_ARG
+ * for null pointers, bytes < 16 or blocks <= 0. */
+int32_t nv_probe_read(const void* buf, int64_t bytes, int32_t blocks, float* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -55,6 +55,8 @@ _sigs = {
     "nv_trace_disable": (I32, []),
     "nv_trace_read": (I32, [I32, C.POINTER(I64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                             C.POINTER(C.c_double)]),
+    "nv_probe_mfma": (I32, [I32, I32, I32, VP, VP]),
+    "nv_probe_read": (I32, [VP, I64, I32, VP, VP]),
     "nv_op_workspace": (SZ, []),
     "nv_op_linear": (I32, [VP, VP, VP, VP, VP, VP, I64, I32, I32, I32, VP, SZ, VP]),
     "nv_op_conv3x3": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, I32, I32, VP, SZ,

@@ -243,3 +243,33 @@ def nv_trace_read(family):
     N.check(N.lib.nv_trace_read(family, C.byref(n), C.byref(ms), C.byref(fl), C.byref(by)),
             "nv_trace_read")
     return int(n.value), ms.value, fl.value, by.value
+
+
+def nv_probe_peaks(device=None):
+    """Measured dense matrix-core throughput (float16 and bfloat16, TFLOP/s) from
+    nv_probe_mfma and HBM read bandwidth (GB/s) from nv_probe_read over 4 GiB;
+    each timed after a full-size warm-up launch."""
+    dev = torch.device(device or "cuda:0")
+    sink = torch.zeros(256, dtype=torch.float32, device=dev)
+    ev = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    out = {}
+    blocks, iters = 2048, 4096
+    for name, bf in (("f16", 0), ("bf16", 1)):
+        for timed in (False, True):
+            e0, e1 = ev()
+            e0.record()
+            N.check(N.lib.nv_probe_mfma(bf, iters, blocks, _p(sink), _stream()), "nv_probe_mfma")
+            e1.record()
+            torch.cuda.synchronize()
+        out[name + "_tflops"] = blocks * 4 * iters * 8 * 16384 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    buf = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+    for timed in (False, True):
+        e0, e1 = ev()
+        e0.record()
+        N.check(N.lib.nv_probe_read(_p(buf), buf.numel(), 8192, _p(sink), _stream()),
+                "nv_probe_read")
+        e1.record()
+        torch.cuda.synchronize()
+    out["hbm_read_gbps"] = buf.numel() / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del buf
+    return out

@@ -74,7 +74,7 @@ WORKLOADS = {
         unet="tiny", n_cache=1024, d=64, cache_dtype="f32", clusters=16, sigma=0.1,
         cache_seed=1, query_seed=2, query_sims=(0.99, 0.93, 0.85, 0.78, 0.70, 0.60),
         n_cluster_queries=2, N=20, guidance=7.5, thresholds=THRESHOLDS_TINY,
-        weight_seed=0, batch=1,
+        weight_seed=0, batch=1, cond_seed=3, uncond_seed=4,
     ),
     "sd15_b1": dict(
         unet="sd15", n_cache=100_000, d=768, cache_dtype="bf16", clusters=1000, sigma=0.05,
