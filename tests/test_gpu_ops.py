@@ -95,3 +95,14 @@ def test_conv3x3_two_sources(B, H, C1, C2, Cout, up):
             xi = U.upsample_nearest2(xi)
         ref = U.conv3x3(xi, w.astype(np.float32), b, 1).transpose(1, 2, 0)
         np.testing.assert_allclose(got[bi], ref, rtol=2e-3, atol=2e-3 * np.abs(ref).max())
+
+
+def test_peak_probes_run():
+    """The measured-peak probes run and report plausible figures (below the
+    published 2.5 PFLOP/s and 8 TB/s, above a tenth of them)."""
+    import paper_2312_04429_amd as P
+    print("probes", flush=True)
+    pk = P.nv_probe_peaks()
+    print(f"  {pk}", flush=True)
+    assert 250 < pk["f16_tflops"] < 2500 and 250 < pk["bf16_tflops"] < 2500
+    assert 800 < pk["hbm_read_gbps"] < 8000
