@@ -93,6 +93,17 @@ int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache, int3
  * noise[b] and its k is rewritten to 0 in k (device, in place), so the
  * caller's later nv_denoise runs it from scratch.
  * ------------------------------------------------------------------------ */
+/* Cache insertion after a miss: rows (device f32 [m][d], finite) become
+ * cache rows n .. n+m-1 of cache (device [capacity][d] of c_dtype; bf16 rows
+ * are rounded to nearest even), and payload[n + i] = entry[i] (device int32
+ * [capacity] and [m]; both NULL to leave the payload alone).  The caller
+ * owns n and capacity and passes n + m as the new row count afterwards.
+ * Errors: NV_ERR_INVALID_ARG for null rows / cache, m < 1, d < 1, n < 0,
+ * n + m > capacity, a bad c_dtype, or only one of entry / payload. */
+int32_t nv_cache_insert(const float* rows, int32_t m, int32_t d, void* cache, int32_t c_dtype,
+                        int64_t n, int64_t capacity, const int32_t* entry, int32_t* payload,
+                        void* stream);
+
 int32_t nv_gather_states(const float* store, int64_t n_store, int32_t n_slots,
                          const int32_t* slot_k, const int32_t* payload, int64_t n_rows,
                          const int64_t* idx, int32_t* k, const float* noise, int32_t B,
@@ -186,6 +197,23 @@ size_t nv_denoise_workspace(const nv_unet* net, int32_t B);
 int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent, const int32_t* k,
                    int32_t B, const float* cond, const float* uncond, const float* pooled,
                    float guidance, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The cache-miss side of Alg. 1 (Sec. 4.3: a request without a suitable
+ * cache generates from scratch and its intermediate states join the cache):
+ * exactly nv_denoise, and in addition, whenever sample b has completed
+ * slot_k[s] steps (including k[b] itself: the state it was given), its
+ * latent is copied to store[entry[b]][s], store being device f32
+ * [n_store][n_slots][in_ch][H][W] (the layout nv_gather_states reads).
+ * slot_k: HOST int32 [n_slots], 1 <= n_slots <= 16, each in [0, N].
+ * entry: HOST int64 [B], -1 (store nothing for b) or in [0, n_store).
+ * Slots a sample never reaches (slot_k < k[b]) are left as they were.
+ * Errors: those of nv_denoise, plus NV_ERR_INVALID_ARG for bad slots or
+ * entries, or a null store with entries to write. */
+int32_t nv_denoise_store(nv_unet* net, const nv_schedule* sched, float* latent,
+                         const int32_t* k, int32_t B, const float* cond, const float* uncond,
+                         const float* pooled, float guidance, float* store, int64_t n_store,
+                         int32_t n_slots, const int32_t* slot_k, const int64_t* entry,
+                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* One UNet evaluation per row for teacher-forced checks: sample b at step
  * index step_idx[b] (HOST int32 [B], 0 <= step_idx < N, timestep t_i of the

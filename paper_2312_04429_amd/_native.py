@@ -49,6 +49,9 @@ _sigs = {
     "nv_unet_destroy": (None, [VP]),
     "nv_denoise_workspace": (SZ, [VP, I32]),
     "nv_denoise": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, SZ, VP]),
+    "nv_denoise_store": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, I64,
+                               I32, VP, VP, VP, SZ, VP]),
+    "nv_cache_insert": (I32, [VP, I32, I32, VP, I32, I64, I64, VP, VP, VP]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
     "nv_trace_enable": (I32, [I32, I32]),

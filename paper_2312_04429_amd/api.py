@@ -152,6 +152,23 @@ class NvUNet:
         N.check(st, "nv_denoise")
         return latent
 
+    def nv_denoise_store(self, latent, k, cond, uncond, store, slot_k, entry, pooled=None,
+                         guidance=7.5, sched=(1000, 50, 0.00085, 0.012)):
+        """nv_denoise that also copies each sample's state after slot_k[s] steps to
+        store[entry[b]][s] (store: f32 [n_store][n_slots][C][H][W]; entry[b] = -1: none)."""
+        _need_cuda(latent, cond, uncond, pooled, store)
+        B = latent.shape[0]
+        kk = (C.c_int32 * B)(*[int(v) for v in k])
+        sk = (C.c_int32 * len(slot_k))(*[int(v) for v in slot_k])
+        ee = (C.c_int64 * B)(*[int(v) for v in entry])
+        s = N.make_schedule(*sched)
+        _own, addr, need = self._workspace(B, latent.device)
+        st = N.lib.nv_denoise_store(self._h, C.byref(s), _p(latent), kk, B, _p(cond), _p(uncond),
+                                    _p(pooled), float(guidance), _p(store), store.shape[0],
+                                    len(slot_k), sk, ee, C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_denoise_store")
+        return latent
+
     def nv_unet_eps(self, x, step_idx, cond, uncond, pooled=None,
                     sched=(1000, 50, 0.00085, 0.012)):
         """Per-row epsilon of one evaluation: (eps_uncond, eps_cond) [B][C][H][W] f32."""
@@ -273,3 +290,18 @@ def nv_probe_peaks(device=None):
     out["hbm_read_gbps"] = buf.numel() / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del buf
     return out
+
+
+def nv_cache_insert(rows, cache, n, entry=None, payload=None):
+    """Append f32 rows [m][d] to cache (f32, or bf16 bits / torch.bfloat16) at row n, and
+    payload[n + i] = entry[i] when both are given (int32 device tensors).  Returns n + m."""
+    _need_cuda(rows, cache, entry, payload)
+    assert rows.dtype == torch.float32 and rows.is_contiguous() and cache.is_contiguous()
+    m, d = rows.shape
+    cdt = N.NV_F32 if cache.dtype == torch.float32 else N.NV_BF16
+    if cdt == N.NV_BF16 and cache.dtype not in BF16_DTYPES:
+        raise ValueError("cache must be float32 or bfloat16 (bits)")
+    st = N.lib.nv_cache_insert(_p(rows), m, d, _p(cache), cdt, int(n), cache.shape[0], _p(entry),
+                               _p(payload), _stream())
+    N.check(st, "nv_cache_insert")
+    return int(n) + m

@@ -859,6 +859,48 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
 }
 
 // ---------------------------------------------------------------------------
+// Cache insertion on a miss (Alg. 1: the new prompt's embedding joins the
+// cache, its entry gets the states the full generation stored): rows n .. n+m
+// of the cache receive the float32 rows (rounded to bfloat16, nearest even,
+// for a bf16 cache), payload[n + i] = entry[i].
+namespace nv {
+namespace {
+__global__ void __launch_bounds__(256) cache_insert_k(const float* __restrict__ rows, int m,
+                                                      int d, void* __restrict__ cache,
+                                                      int cache_bf16, int64_t n,
+                                                      const int32_t* __restrict__ entry,
+                                                      int32_t* __restrict__ payload) {
+  const int64_t total = (int64_t)m * d;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const float v = rows[e];
+    if (cache_bf16)
+      ((uint16_t*)cache)[n * d + e] = f32_to_bf16_rne(v);
+    else
+      ((float*)cache)[n * d + e] = v;
+    if (payload && e % d == 0) payload[n + e / d] = entry[e / d];
+  }
+}
+}  // namespace
+}  // namespace nv
+
+extern "C" int32_t nv_cache_insert(const float* rows, int32_t m, int32_t d, void* cache,
+                                   int32_t c_dtype, int64_t n, int64_t capacity,
+                                   const int32_t* entry, int32_t* payload, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(rows && cache, "null rows or cache");
+  NV_CHECK_ARG(m >= 1 && d >= 1 && n >= 0 && n + m <= capacity, "need 1 <= m, n + m <= capacity");
+  NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
+  NV_CHECK_ARG((entry == nullptr) == (payload == nullptr), "entry and payload go together");
+  const int64_t total = (int64_t)m * d;
+  const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+  hipLaunchKernelGGL(cache_insert_k, dim3(blocks), dim3(256), 0, (hipStream_t)stream, rows, m, d,
+                     cache, c_dtype == NV_BF16, n, entry, payload);
+  NV_LAUNCH_CHECK("cache_insert_k");
+  return NV_OK;
+}
+
+// ---------------------------------------------------------------------------
 // State fetch: out[b] = store[payload[idx[b]]][slot of k[b]] for hits, noise[b]
 // otherwise (Alg. 1: retrieve the cached intermediate state of the match at K,
 // or start from scratch).

@@ -1144,11 +1144,19 @@ int32_t prep_call(nv_unet* net, const nv_schedule* sched, int32_t B, const float
 }
 }  // namespace
 
-extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent,
-                              const int32_t* k, int32_t B, const float* cond,
-                              const float* uncond, const float* pooled, float guidance,
-                              void* workspace, size_t workspace_bytes, void* stream) {
-  clear_error();
+// Snapshots of the cache-miss path: the state of sample b after slot_k[s]
+// steps goes to store[entry[b]][s] (entry[b] < 0: not stored).
+struct Snapshots {
+  float* store = nullptr;
+  int n_slots = 0;
+  int32_t slot_k[16] = {};
+  const int64_t* entry = nullptr;  // host [B]
+};
+
+static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* latent,
+                            const int32_t* k, int32_t B, const float* cond, const float* uncond,
+                            const float* pooled, float guidance, void* workspace,
+                            size_t workspace_bytes, void* stream, const Snapshots* snap) {
   NV_CHECK_ARG(latent && k, "null latent or k");
   NV_CHECK_ARG(std::isfinite(guidance), "guidance must be finite");
   Plan* P = nullptr;
@@ -1179,6 +1187,21 @@ extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* lat
     NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
   RunCtx rc{ws, 2 * B, s, (const float*)(ws + P->x_work), sa, (float*)(ws + P->splitk),
             SPLITK_BYTES};
+  // copy every sorted sample a whose step count equals a slot's K
+  auto take = [&](int a, int done) -> hipError_t {
+    if (!snap) return hipSuccess;
+    const int64_t e = snap->entry[sa.perm[a]];
+    if (e < 0) return hipSuccess;
+    for (int q = 0; q < snap->n_slots; ++q)
+      if (snap->slot_k[q] == done) {
+        hipError_t err = hipMemcpyAsync(snap->store + (e * snap->n_slots + q) * lat,
+                                        (const float*)(ws + P->x_work) + a * lat, lat * 4,
+                                        hipMemcpyDeviceToDevice, s);
+        if (err != hipSuccess) return err;
+      }
+    return hipSuccess;
+  };
+  for (int a = 0; a < B; ++a) NV_HIP_TRY(take(a, sa.kstep[a]));  // the states given
   NV_HIP_TRY(run_ops(P->pre, rc));
   for (int j = 0;; ++j) {
     int A = 0;
@@ -1190,9 +1213,46 @@ extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* lat
     NV_HIP_TRY(cfg_ddim_launch(rc.st, (const float*)(ws + P->eps), (float*)(ws + P->x_work),
                                c.out_ch, HW, A, guidance, (const float*)(ws + P->at),
                                (const float*)(ws + P->ap), s));
+    for (int a = 0; a < A; ++a) NV_HIP_TRY(take(a, sa.kstep[a] + j + 1));
   }
   NV_HIP_TRY(permute_launch(sa, (const float*)(ws + P->x_work), latent, lat, B, 0, s));
   return NV_OK;
+}
+
+extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent,
+                              const int32_t* k, int32_t B, const float* cond,
+                              const float* uncond, const float* pooled, float guidance,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
+                      workspace_bytes, stream, nullptr);
+}
+
+extern "C" int32_t nv_denoise_store(nv_unet* net, const nv_schedule* sched, float* latent,
+                                    const int32_t* k, int32_t B, const float* cond,
+                                    const float* uncond, const float* pooled, float guidance,
+                                    float* store, int64_t n_store, int32_t n_slots,
+                                    const int32_t* slot_k, const int64_t* entry,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(n_slots >= 1 && n_slots <= 16 && slot_k && entry, "need 1..16 slots and entries");
+  NV_CHECK_ARG(sched, "null schedule");
+  Snapshots sn;
+  sn.store = store;
+  sn.n_slots = n_slots;
+  sn.entry = entry;
+  for (int q = 0; q < n_slots; ++q) {
+    NV_CHECK_ARG(slot_k[q] >= 0 && slot_k[q] <= sched->N, "slot_k must be in [0, N]");
+    sn.slot_k[q] = slot_k[q];
+  }
+  bool any = false;
+  for (int b = 0; b < B && b < 64; ++b) {
+    NV_CHECK_ARG(entry[b] >= -1 && entry[b] < n_store, "entry[b] must be -1 or in [0, n_store)");
+    any |= entry[b] >= 0;
+  }
+  NV_CHECK_ARG(!any || store, "null store with entries to write");
+  return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
+                      workspace_bytes, stream, &sn);
 }
 
 extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const float* x,
