@@ -36,6 +36,10 @@ def parse():
     ap.add_argument("--k", type=int, default=None,
                     help="sd15_b1: place the query in this K's similarity band; "
                          "sdxl_b2: the skip count (default: first of the workload's K values)")
+    ap.add_argument("--miss", action="store_true",
+                    help="the cache-miss path instead: queries far from every cached prompt, "
+                         "full generation storing the states after each K of the table, and "
+                         "insertion of the new embeddings into the cache")
     ap.add_argument("--scan-only", action="store_true",
                     help="time the lookup alone, warm (back to back) and cold (a 2 GiB write "
                          "between repetitions evicts the cache from the Infinity Cache)")
@@ -248,8 +252,17 @@ def main():
         thr = [t_ for t_, _ in wl["thresholds"]]
         kv = [k for _, k in wl["thresholds"]]
         d_cache, cache, q, feed = build_lookup_inputs(wl, B, args, dev, torch, synth)
+        if args.miss:  # fresh cluster draws, new ones every step: no cached prompt within
+            # the table's bands (a repeated prompt would hit its own inserted row)
+            room = args.warmup + 2 * args.steps + 2  # steps, and rows the inserts may add
+            mu = synth.cluster_centres(wl["clusters"], wl["d"], wl["cache_seed"])
+            q = synth.cluster_queries_from(mu, room * q.shape[0], wl["sigma"], wl["query_seed"] + 5)
+            big = torch.empty((wl["n_cache"] + room * B, wl["d"]), dtype=d_cache.dtype, device=dev)
+            big[: wl["n_cache"]] = d_cache
+            d_cache = big
         d_q = t(q)
-        lws_bytes = P.nv_cache_lookup_workspace(q.shape[0], wl["n_cache"], wl["d"])
+        m_look = q.shape[0] // (args.warmup + 2 * args.steps + 2) if args.miss else q.shape[0]
+        lws_bytes = P.nv_cache_lookup_workspace(m_look, d_cache.shape[0], wl["d"])
         lws_own, lws_addr = P.workspace(lws_bytes, dev)
         lws = (lws_own, lws_addr, lws_bytes)
     if args.scan_only:
@@ -273,9 +286,28 @@ def main():
         rng = np.random.default_rng(77)
         store = rng.standard_normal((pool, len(slots), cfg["in_ch"], cfg["H"], cfg["W"]),
                                     dtype=np.float32)
-        payload = (np.arange(wl["n_cache"]) % pool).astype(np.int32)
+        payload = (np.arange(d_cache.shape[0]) % pool).astype(np.int32)
         d_store, d_payload = t(store), t(payload)
         nf = len(feed)
+        n_rows = [wl["n_cache"]]
+
+        m_step = q.shape[0] // (args.warmup + 2 * args.steps + 2) if args.miss else 0
+
+        def miss_step():
+            n = n_rows[0]
+            i = len(ks_seen)
+            qs = d_q[i * m_step:(i + 1) * m_step]
+            idx, sim, kk = P.nv_cache_lookup(qs, d_cache[:n], thr, kv, ws=lws)
+            idx, kk = idx[:nf], kk[:nf]
+            P.nv_gather_states(d_store, slots, d_payload, n, idx, kk, d_noise, out=x)
+            k_host = kk.cpu().tolist()
+            ks_seen.append(k_host)
+            entries = [(n + b) % pool for b in range(nf)]
+            net.nv_denoise_store(x, k_host, d_cond, d_unc, d_store, slots, entries,
+                                 pooled=d_pooled, guidance=wl["guidance"], sched=sched)
+            n_rows[0] = P.nv_cache_insert(qs[:nf], d_cache, n,
+                                          entry=t(np.asarray(entries, dtype=np.int32)),
+                                          payload=d_payload)
 
         def step():
             idx, sim, kk = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
@@ -285,6 +317,8 @@ def main():
             ks_seen.append(k_host)
             net.nv_denoise(x, k_host, d_cond, d_unc, pooled=d_pooled, guidance=wl["guidance"],
                            sched=sched)
+        if args.miss:
+            step = miss_step
     else:  # denoise-only workload (no cache in its recipe): a fixed skip count
         kfix = args.k if args.k is not None else wl["k_sweep"][0]
 
@@ -340,8 +374,11 @@ def main():
               "latent": [cfg["in_ch"], cfg["H"], cfg["W"]], "batch": B, "cfg_rows": 2 * B,
               "N": wl["N"], "K": K, "guidance": wl["guidance"]}
     if has_cache:
-        config["cache"] = f"{wl['n_cache']}x{wl['d']} bf16"
-        config["queries"] = int(q.shape[0])
+        config["cache"] = f"{wl['n_cache']}x{wl['d']} {wl.get('cache_dtype', 'bf16')}"
+        config["queries"] = int(m_look)
+    if args.miss:
+        config["path"] = ("cache miss: lookup, full generation storing the states after "
+                          "K = 5..25, insertion of the new embeddings")
     out = {
         "metric": "images/sec and UNet steps/sec at skip K (SD1.5-shape, 1 GPU); % MFMA peak",
         "value": images / dt, "unit": "images/s", "n_gpus": 1, "steps": args.steps,
@@ -386,7 +423,8 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(
-            cfg, weights, wl, ks_last, cache if has_cache else None, q if has_cache else None,
+            cfg, weights, wl, ks_last, cache if has_cache else None,
+            q[:m_look] if has_cache else None,
             cond, unc, d_cache if has_cache else None,
             synth.make_pooled(B, cfg["pooled_dim"], wl["pooled_seed"]) if d_pooled is not None
             else None)
