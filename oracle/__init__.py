@@ -7,7 +7,9 @@ from the paper's definitions:
   schedule.py  the DDIM timestep grid and cumulative alpha table (Sec. 2.1, Sec. 6);
   ddim.py      classifier-free guidance and the deterministic DDIM update, and the
                resume-from-step-K loop of approximate caching (Sec. 4.1);
-  unet.py      the latent-diffusion UNet epsilon predictor (Sec. 2.1), fp32.
+  unet.py      the latent-diffusion UNet epsilon predictor (Sec. 2.1), fp32;
+  lcbfu.py     cache maintenance under LCBFU and the hole-aware choice of the
+               state served (Sec. 5.4).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  The product path never imports it and shares no code with it.
