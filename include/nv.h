@@ -110,6 +110,90 @@ int32_t nv_gather_states(const float* store, int64_t n_store, int32_t n_slots,
                          int64_t latent_elems, float* out, void* stream);
 
 /* ------------------------------------------------------------------------ *
+ * Maintained cache (Sec. 5.4: LCBFU eviction, holes, dropping prompts).
+ *
+ * States live in a pool: device f32 [n_pool][latent_elems].  The table,
+ * device int32 [n_entries][n_slots], names for prompt (entry) e the pool
+ * state saved after slot_k[s] steps, or -1 for a hole.  payload (device
+ * int32 [n_rows], NULL = identity) maps a vector-DB row to its entry.
+ *
+ * nv_gather_pool: the hole-aware fetch.  For sample b with match idx[b] and
+ * selector K k[b], the state served is the one with the largest slot_k[s]
+ * <= k[b] whose table entry is in [0, n_pool); out[b] is that pool state and
+ * k[b] (device, in place) becomes its slot_k[s].  No such state (or
+ * k[b] <= 0, or idx / payload out of range): out[b] = noise[b], k[b] = 0.
+ * latent_elems a multiple of 4; pool, noise, out 16-byte aligned.
+ *
+ * nv_table_update: rec (device int32 [u][1 + n_slots]) holds an entry id
+ * then its new table row; rows with an id outside [0, n_entries) are
+ * ignored.  Ids must be distinct within one call.
+ *
+ * nv_cache_move_rows: row src[i] of the cache (device [n][d] of c_dtype)
+ * and payload[src[i]] (payload may be NULL) move to dst[i], for i < count
+ * (src, dst device int64 [count]); pairs outside [0, n) are ignored.  The
+ * dst values must be distinct and none may equal any src (the maintainer's
+ * compaction plan meets this: every dst is below every src).  d even.
+ *
+ * nv_denoise_store_pool: nv_denoise_store with the destinations given per
+ * state: dst HOST int32 [B][n_slots], pool index or -1 (not stored); the
+ * state of sample b after slot_k[s] steps goes to pool[dst[b][s]].  Each
+ * pool index may appear once.
+ * ------------------------------------------------------------------------ */
+int32_t nv_gather_pool(const float* pool, int64_t n_pool, const int32_t* table,
+                       int64_t n_entries, int32_t n_slots, const int32_t* slot_k,
+                       const int32_t* payload, int64_t n_rows, const int64_t* idx, int32_t* k,
+                       const float* noise, int32_t B, int64_t latent_elems, float* out,
+                       void* stream);
+int32_t nv_table_update(int32_t* table, int64_t n_entries, int32_t n_slots, const int32_t* rec,
+                        int32_t u, void* stream);
+int32_t nv_cache_move_rows(void* cache, int32_t c_dtype, int64_t n, int32_t d, int32_t* payload,
+                           const int64_t* src, const int64_t* dst, int32_t count, void* stream);
+
+/* LCBFU maintainer (host only; no GPU work).  Each stored state has the
+ * score f * K: f counts the requests served from it, starting at 1 when it
+ * is stored; K is its slot's step count.  Equal scores go to the state
+ * stored first.
+ *
+ * nv_lcbfu_create: slot_k HOST int32 [n_slots] (1..16 distinct values >= 1);
+ * state_capacity = the limit on stored states = pool size; entry_capacity
+ * >= state_capacity bounds entry ids (every live prompt holds a state).
+ * Returns the handle in *out; release it with nv_lcbfu_destroy.
+ *
+ * nv_lcbfu_access: B served requests (HOST row [B], HOST k [B], the k
+ * nv_gather_pool returned): each with k > 0 raises its state's f by one.
+ * A row out of range or a k naming no stored state is NV_ERR_INVALID_ARG
+ * (nothing is changed).
+ *
+ * nv_lcbfu_insert: makes room for and stores m new prompts (m * n_slots <=
+ * state_capacity).  First it evicts the fewest lowest-scored states that let
+ * m * n_slots new ones fit (exactly n_slots per prompt once full); a prompt
+ * left with no state is dropped: the live rows at or past the new row count
+ * (*n_kept) move, in ascending order, into the dropped rows below it.  Then
+ * prompt i gets the lowest free entry id entry_out[i] and the lowest free
+ * pool states state_out[i][s] (slot order), and row *n_kept + i.  All
+ * outputs are HOST arrays sized by the caller: entry_out [m], state_out
+ * [m][n_slots], move_src / move_dst [m * n_slots] (*n_moves used), upd
+ * [m * n_slots + m][1 + n_slots] (*n_upd records for nv_table_update: every
+ * entry whose table row changed, ascending, with its new row).
+ *
+ * nv_lcbfu_info: info HOST int64 [5] = rows, stored states, evictions so far,
+ * prompts dropped so far, states ever stored.
+ * nv_lcbfu_export: copies (each may be NULL) the table HOST int32
+ * [entry_capacity][n_slots], the row -> entry map HOST int32 [rows], and
+ * counts HOST int64 [state_capacity] (f of each pool state, 0 if free).
+ * ------------------------------------------------------------------------ */
+typedef struct nv_lcbfu nv_lcbfu;
+int32_t nv_lcbfu_create(int32_t n_slots, const int32_t* slot_k, int64_t state_capacity,
+                        int64_t entry_capacity, nv_lcbfu** out);
+void nv_lcbfu_destroy(nv_lcbfu* h);
+int32_t nv_lcbfu_access(nv_lcbfu* h, int32_t B, const int64_t* row, const int32_t* k);
+int32_t nv_lcbfu_insert(nv_lcbfu* h, int32_t m, int32_t* entry_out, int32_t* state_out,
+                        int64_t* move_src, int64_t* move_dst, int32_t* n_moves, int32_t* upd,
+                        int32_t* n_upd, int64_t* n_kept);
+int32_t nv_lcbfu_info(const nv_lcbfu* h, int64_t* info);
+int32_t nv_lcbfu_export(const nv_lcbfu* h, int32_t* table, int32_t* rows, int64_t* counts);
+
+/* ------------------------------------------------------------------------ *
  * Latent-diffusion UNet (Sec. 2.1: UNet backbone, text conditioning through
  * cross-attention, operating on latents).  Topology rule:
  *   conv_in; per level l: n_res ResBlocks (+ transformer of depth[l] if > 0),
@@ -214,6 +298,12 @@ int32_t nv_denoise_store(nv_unet* net, const nv_schedule* sched, float* latent,
                          const float* pooled, float guidance, float* store, int64_t n_store,
                          int32_t n_slots, const int32_t* slot_k, const int64_t* entry,
                          void* workspace, size_t workspace_bytes, void* stream);
+int32_t nv_denoise_store_pool(nv_unet* net, const nv_schedule* sched, float* latent,
+                              const int32_t* k, int32_t B, const float* cond,
+                              const float* uncond, const float* pooled, float guidance,
+                              float* pool, int64_t n_pool, int32_t n_slots,
+                              const int32_t* slot_k, const int32_t* dst, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* One UNet evaluation per row for teacher-forced checks: sample b at step
  * index step_idx[b] (HOST int32 [B], 0 <= step_idx < N, timestep t_i of the

@@ -52,6 +52,17 @@ _sigs = {
     "nv_denoise_store": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, I64,
                                I32, VP, VP, VP, SZ, VP]),
     "nv_cache_insert": (I32, [VP, I32, I32, VP, I32, I64, I64, VP, VP, VP]),
+    "nv_denoise_store_pool": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32,
+                                    VP, I64, I32, VP, VP, VP, SZ, VP]),
+    "nv_gather_pool": (I32, [VP, I64, VP, I64, I32, VP, VP, I64, VP, VP, VP, I32, I64, VP, VP]),
+    "nv_table_update": (I32, [VP, I64, I32, VP, I32, VP]),
+    "nv_cache_move_rows": (I32, [VP, I32, I64, I32, VP, VP, VP, I32, VP]),
+    "nv_lcbfu_create": (I32, [I32, VP, I64, I64, C.POINTER(VP)]),
+    "nv_lcbfu_destroy": (None, [VP]),
+    "nv_lcbfu_access": (I32, [VP, I32, VP, VP]),
+    "nv_lcbfu_insert": (I32, [VP, I32, VP, VP, VP, VP, VP, VP, VP, VP]),
+    "nv_lcbfu_info": (I32, [VP, VP]),
+    "nv_lcbfu_export": (I32, [VP, VP, VP, VP]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
     "nv_trace_enable": (I32, [I32, I32]),

@@ -84,6 +84,117 @@ def nv_gather_states(store, slot_k, payload, n_rows, idx, k, noise, out=None):
     return out
 
 
+def nv_gather_pool(pool, table, slot_k, payload, n_rows, idx, k, noise, out=None):
+    """Hole-aware fetch from a state pool: pool [n_pool][*latent] f32, table int32
+    [n_entries][n_slots]; returns out [B][*latent]; k becomes the K served (0: noise)."""
+    _need_cuda(pool, table, idx, k, noise, payload)
+    B = idx.shape[0]
+    lat = int(np.prod(noise.shape[1:]))
+    if table.dim() != 2 or table.shape[1] != len(slot_k) or table.dtype != torch.int32:
+        raise ValueError("table must be int32 [n_entries][len(slot_k)]")
+    if pool.dtype != torch.float32 or int(np.prod(pool.shape[1:])) != lat:
+        raise ValueError("pool must be float32 [n_pool][*latent]")
+    if k.shape[0] != B or noise.shape[0] != B or idx.dtype != torch.int64:
+        raise ValueError("idx (int64), k and noise need B rows")
+    if payload is not None and payload.shape[0] < n_rows:
+        raise ValueError("payload shorter than n_rows")
+    if out is None:
+        out = torch.empty_like(noise)
+    sk = (C.c_int32 * len(slot_k))(*[int(v) for v in slot_k])
+    st = N.lib.nv_gather_pool(_p(pool), pool.shape[0], _p(table), table.shape[0], len(slot_k), sk,
+                              _p(payload), int(n_rows), _p(idx), _p(k), _p(noise), B, lat,
+                              _p(out), _stream())
+    N.check(st, "nv_gather_pool")
+    return out
+
+
+def nv_table_update(table, rec):
+    """table int32 [n_entries][n_slots]; rec int32 [u][1 + n_slots] (device)."""
+    _need_cuda(table, rec)
+    assert table.dtype == torch.int32 and rec.dtype == torch.int32 and rec.is_contiguous()
+    if rec.dim() != 2 or rec.shape[1] != 1 + table.shape[1]:
+        raise ValueError("rec must be [u][1 + n_slots]")
+    u = rec.shape[0]
+    st = N.lib.nv_table_update(_p(table), table.shape[0], table.shape[1], _p(rec) if u else None,
+                               u, _stream())
+    N.check(st, "nv_table_update")
+
+
+def nv_cache_move_rows(cache, n, payload, src, dst):
+    """Move cache rows src[i] -> dst[i] (int64 device) and their payload entries."""
+    _need_cuda(cache, payload, src, dst)
+    count = src.shape[0]
+    if dst.shape[0] != count or src.dtype != torch.int64 or dst.dtype != torch.int64:
+        raise ValueError("src and dst must be int64 of one length")
+    if int(n) > cache.shape[0] or (payload is not None and payload.shape[0] < int(n)):
+        raise ValueError("n exceeds the cache or payload rows")
+    cdt = N.NV_F32 if cache.dtype == torch.float32 else N.NV_BF16
+    st = N.lib.nv_cache_move_rows(_p(cache), cdt, int(n), cache.shape[1], _p(payload),
+                                  _p(src) if count else None, _p(dst) if count else None, count,
+                                  _stream())
+    N.check(st, "nv_cache_move_rows")
+
+
+class NvLCBFU:
+    """Host LCBFU maintainer (native); arrays in and out are host numpy arrays."""
+
+    def __init__(self, slot_k, state_capacity, entry_capacity):
+        self.slot_k = [int(v) for v in slot_k]
+        self.S = len(self.slot_k)
+        self.cap, self.ecap = int(state_capacity), int(entry_capacity)
+        h = C.c_void_p()
+        sk = (C.c_int32 * self.S)(*self.slot_k)
+        N.check(N.lib.nv_lcbfu_create(self.S, sk, self.cap, self.ecap, C.byref(h)),
+                "nv_lcbfu_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            N.lib.nv_lcbfu_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def access(self, rows, ks):
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        ks = np.ascontiguousarray(ks, dtype=np.int32)
+        st = N.lib.nv_lcbfu_access(self._h, len(rows), rows.ctypes.data, ks.ctypes.data)
+        N.check(st, "nv_lcbfu_access")
+
+    def insert(self, m):
+        S = self.S
+        ent = np.empty(m, np.int32)
+        pools = np.empty((m, S), np.int32)
+        src = np.empty(m * S, np.int64)
+        dst = np.empty(m * S, np.int64)
+        upd = np.empty((m * S + m, 1 + S), np.int32)
+        nm, nu, kept = C.c_int32(), C.c_int32(), C.c_int64()
+        st = N.lib.nv_lcbfu_insert(self._h, int(m), ent.ctypes.data, pools.ctypes.data,
+                                   src.ctypes.data, dst.ctypes.data, C.byref(nm),
+                                   upd.ctypes.data, C.byref(nu), C.byref(kept))
+        N.check(st, "nv_lcbfu_insert")
+        return {"entries": ent, "pools": pools, "move_src": src[:nm.value],
+                "move_dst": dst[:nm.value], "upd": upd[:nu.value], "kept": kept.value}
+
+    def info(self):
+        out = np.zeros(5, np.int64)
+        N.check(N.lib.nv_lcbfu_info(self._h, out.ctypes.data), "nv_lcbfu_info")
+        return dict(zip(("rows", "states", "evicted", "dropped", "stored"), out.tolist()))
+
+    def export(self):
+        table = np.empty((self.ecap, self.S), np.int32)
+        rows = np.empty(self.info()["rows"], np.int32)
+        counts = np.empty(self.cap, np.int64)
+        st = N.lib.nv_lcbfu_export(self._h, table.ctypes.data, rows.ctypes.data,
+                                   counts.ctypes.data)
+        N.check(st, "nv_lcbfu_export")
+        return table, rows, counts
+
+
 def nv_unet_param_count(cfg):
     c = N.make_config(cfg)
     return int(N.lib.nv_unet_param_count(C.byref(c)))
@@ -167,6 +278,24 @@ class NvUNet:
                                     _p(pooled), float(guidance), _p(store), store.shape[0],
                                     len(slot_k), sk, ee, C.c_void_p(addr), need, _stream())
         N.check(st, "nv_denoise_store")
+        return latent
+
+    def nv_denoise_store_pool(self, latent, k, cond, uncond, pool, slot_k, dst, pooled=None,
+                              guidance=7.5, sched=(1000, 50, 0.00085, 0.012)):
+        """nv_denoise that also copies each sample's state after slot_k[s] steps to
+        pool[dst[b][s]] (pool: f32 [n_pool][C][H][W]; dst host [B][n_slots], -1: none)."""
+        _need_cuda(latent, cond, uncond, pooled, pool)
+        B = latent.shape[0]
+        kk = (C.c_int32 * B)(*[int(v) for v in k])
+        sk = (C.c_int32 * len(slot_k))(*[int(v) for v in slot_k])
+        dd = np.ascontiguousarray(dst, dtype=np.int32).reshape(B, len(slot_k))
+        s = N.make_schedule(*sched)
+        _own, addr, need = self._workspace(B, latent.device)
+        st = N.lib.nv_denoise_store_pool(self._h, C.byref(s), _p(latent), kk, B, _p(cond),
+                                         _p(uncond), _p(pooled), float(guidance), _p(pool),
+                                         pool.shape[0], len(slot_k), sk, dd.ctypes.data,
+                                         C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_denoise_store_pool")
         return latent
 
     def nv_unet_eps(self, x, step_idx, cond, uncond, pooled=None,

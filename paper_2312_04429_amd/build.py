@@ -13,7 +13,7 @@ SRC = os.environ.get("NV_BUILD_SRC") or os.path.join(HERE, "csrc")
 OUT_DIR = os.environ.get("NV_BUILD_DIR") or os.path.join(HERE, "_build")
 LIB = os.environ.get("NV_BUILD_OUT") or os.path.join(HERE, "libnv.so")
 SOURCES = ["lookup.hip", "gemm.hip", "attention.hip", "ops.hip", "unet.hip", "trace.hip",
-           "probe.hip"]
+           "probe.hip", "pool.hip", "lcbfu.cpp"]
 ARCH = os.environ.get("NV_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

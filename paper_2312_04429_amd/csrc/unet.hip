@@ -1145,12 +1145,12 @@ int32_t prep_call(nv_unet* net, const nv_schedule* sched, int32_t B, const float
 }  // namespace
 
 // Snapshots of the cache-miss path: the state of sample b after slot_k[s]
-// steps goes to store[entry[b]][s] (entry[b] < 0: not stored).
+// steps goes to state dst[b][s] of store (dst < 0: not stored).
 struct Snapshots {
   float* store = nullptr;
   int n_slots = 0;
   int32_t slot_k[16] = {};
-  const int64_t* entry = nullptr;  // host [B]
+  std::vector<int64_t> dst;  // [B][n_slots]
 };
 
 static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* latent,
@@ -1190,11 +1190,11 @@ static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* laten
   // copy every sorted sample a whose step count equals a slot's K
   auto take = [&](int a, int done) -> hipError_t {
     if (!snap) return hipSuccess;
-    const int64_t e = snap->entry[sa.perm[a]];
-    if (e < 0) return hipSuccess;
+    const int b = sa.perm[a];
     for (int q = 0; q < snap->n_slots; ++q)
-      if (snap->slot_k[q] == done) {
-        hipError_t err = hipMemcpyAsync(snap->store + (e * snap->n_slots + q) * lat,
+      if (snap->slot_k[q] == done && snap->dst[(size_t)b * snap->n_slots + q] >= 0) {
+        const int64_t to = snap->dst[(size_t)b * snap->n_slots + q];
+        hipError_t err = hipMemcpyAsync(snap->store + to * lat,
                                         (const float*)(ws + P->x_work) + a * lat, lat * 4,
                                         hipMemcpyDeviceToDevice, s);
         if (err != hipSuccess) return err;
@@ -1237,20 +1237,60 @@ extern "C" int32_t nv_denoise_store(nv_unet* net, const nv_schedule* sched, floa
   clear_error();
   NV_CHECK_ARG(n_slots >= 1 && n_slots <= 16 && slot_k && entry, "need 1..16 slots and entries");
   NV_CHECK_ARG(sched, "null schedule");
+  NV_CHECK_ARG(B >= 1 && B <= MAX_SAMPLES, "B must be in [1, 64]");
   Snapshots sn;
   sn.store = store;
   sn.n_slots = n_slots;
-  sn.entry = entry;
   for (int q = 0; q < n_slots; ++q) {
     NV_CHECK_ARG(slot_k[q] >= 0 && slot_k[q] <= sched->N, "slot_k must be in [0, N]");
     sn.slot_k[q] = slot_k[q];
   }
   bool any = false;
-  for (int b = 0; b < B && b < 64; ++b) {
+  sn.dst.assign((size_t)B * n_slots, -1);
+  for (int b = 0; b < B; ++b) {
     NV_CHECK_ARG(entry[b] >= -1 && entry[b] < n_store, "entry[b] must be -1 or in [0, n_store)");
     any |= entry[b] >= 0;
+    if (entry[b] >= 0)
+      for (int q = 0; q < n_slots; ++q) sn.dst[(size_t)b * n_slots + q] = entry[b] * n_slots + q;
   }
   NV_CHECK_ARG(!any || store, "null store with entries to write");
+  return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
+                      workspace_bytes, stream, &sn);
+}
+
+extern "C" int32_t nv_denoise_store_pool(nv_unet* net, const nv_schedule* sched, float* latent,
+                                         const int32_t* k, int32_t B, const float* cond,
+                                         const float* uncond, const float* pooled,
+                                         float guidance, float* pool, int64_t n_pool,
+                                         int32_t n_slots, const int32_t* slot_k,
+                                         const int32_t* dst, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(n_slots >= 1 && n_slots <= 16 && slot_k && dst, "need 1..16 slots and dst");
+  NV_CHECK_ARG(sched, "null schedule");
+  NV_CHECK_ARG(B >= 1 && B <= MAX_SAMPLES, "B must be in [1, 64]");
+  Snapshots sn;
+  sn.store = pool;
+  sn.n_slots = n_slots;
+  for (int q = 0; q < n_slots; ++q) {
+    NV_CHECK_ARG(slot_k[q] >= 0 && slot_k[q] <= sched->N, "slot_k must be in [0, N]");
+    sn.slot_k[q] = slot_k[q];
+  }
+  bool any = false;
+  sn.dst.assign((size_t)B * n_slots, -1);
+  for (int64_t i = 0; i < (int64_t)B * n_slots; ++i) {
+    NV_CHECK_ARG(dst[i] >= -1 && dst[i] < n_pool, "dst must be -1 or in [0, n_pool)");
+    any |= dst[i] >= 0;
+    sn.dst[i] = dst[i];
+  }
+  NV_CHECK_ARG(!any || pool, "null pool with states to write");
+  // two writes to one state would leave whichever ran last
+  std::vector<int32_t> used;
+  for (int64_t i = 0; i < (int64_t)B * n_slots; ++i)
+    if (dst[i] >= 0) used.push_back(dst[i]);
+  std::sort(used.begin(), used.end());
+  NV_CHECK_ARG(std::adjacent_find(used.begin(), used.end()) == used.end(),
+               "dst names one state twice");
   return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
                       workspace_bytes, stream, &sn);
 }

@@ -112,6 +112,26 @@ def cluster_queries_from(mu, m, sigma, seed):
     return (x / np.linalg.norm(x, axis=1, keepdims=True)).astype(np.float32)
 
 
+def make_prompt_stream(n, d, seed, p_new=0.35, sims=(0.97, 0.92, 0.87, 0.8, 0.7)):
+    """A stream of n request embeddings (float32 unit vectors [n][d]): request j is a
+    fresh draw with probability p_new, else a rewording of a uniformly chosen earlier
+    request, at a cosine similarity drawn uniformly from sims."""
+    rng = np.random.default_rng([seed, 8])
+    out = np.empty((n, d), dtype=np.float32)
+    for j in range(n):
+        g = rng.standard_normal(d)
+        if j == 0 or rng.random() < p_new:
+            out[j] = g / np.linalg.norm(g)
+            continue
+        t = out[int(rng.integers(0, j))].astype(np.float64)
+        t /= np.linalg.norm(t)
+        s = float(sims[int(rng.integers(0, len(sims)))])
+        g -= (g @ t) * t
+        g /= np.linalg.norm(g)
+        out[j] = s * t + np.sqrt(1.0 - s * s) * g
+    return out
+
+
 def make_contexts(b, length, dim, seed):
     """Text-encoder output stand-in: N(0, 1), rounded to bfloat16 values (float32 array)."""
     rng = np.random.default_rng([seed, 4])

@@ -98,3 +98,44 @@ def test_unet_entry_points_reject_null_handles():
     cfg = N.make_config(synth.unet_config("tiny", ch=(30, 64)))
     h = C.c_void_p()
     assert N.lib.nv_unet_create(C.byref(cfg), d, 10, C.byref(h)) == N.NV_ERR_INVALID_ARG
+
+
+def test_pool_entry_points_validate_before_launch():
+    """Hole-aware fetch, table updates, row moves and the pool-storing denoise reject
+    bad arguments synchronously (no GPU touched); empty updates / moves are no-ops."""
+    from paper_2312_04429_amd import _native as N
+    lib = N.lib
+    d = C.c_void_p(0x10000)
+    sk = (C.c_int32 * 2)(5, 10)
+
+    def gp(**o):
+        a = dict(pool=d, n_pool=4, table=d, n_ent=4, S=2, sk=sk, payload=d, n_rows=4, idx=d,
+                 k=d, noise=d, B=1, lat=16, out=d)
+        a.update(o)
+        return lib.nv_gather_pool(a["pool"], a["n_pool"], a["table"], a["n_ent"], a["S"],
+                                  a["sk"], a["payload"], a["n_rows"], a["idx"], a["k"],
+                                  a["noise"], a["B"], a["lat"], a["out"], None)
+    assert gp(idx=None) == N.NV_ERR_INVALID_ARG
+    assert gp(B=0) == N.NV_ERR_INVALID_ARG
+    assert gp(lat=18) == N.NV_ERR_INVALID_ARG
+    assert gp(pool=None) == N.NV_ERR_INVALID_ARG
+    assert gp(table=None) == N.NV_ERR_INVALID_ARG
+    assert gp(S=0) == N.NV_ERR_INVALID_ARG
+    assert gp(sk=(C.c_int32 * 2)(5, 0)) == N.NV_ERR_INVALID_ARG
+    assert gp(payload=None, n_rows=5) == N.NV_ERR_INVALID_ARG
+    assert gp(out=C.c_void_p(0x10004)) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_table_update(None, 4, 2, None, 0, None) == N.NV_OK
+    assert lib.nv_table_update(None, 4, 2, d, 1, None) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_table_update(d, 4, 17, d, 1, None) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_cache_move_rows(None, N.NV_BF16, 4, 8, None, None, None, 0, None) == N.NV_OK
+    assert lib.nv_cache_move_rows(d, N.NV_BF16, 4, 7, None, d, d, 1, None) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_cache_move_rows(d, 3, 4, 8, None, d, d, 1, None) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_cache_move_rows(d, N.NV_F32, 4, 8, None, None, d, 1, None) == \
+        N.NV_ERR_INVALID_ARG
+    s = N.make_schedule(1000, 50, 0.00085, 0.012)
+    k = (C.c_int32 * 1)(0)
+    dst = (C.c_int32 * 2)(0, 1)
+    assert lib.nv_denoise_store_pool(None, C.byref(s), d, k, 1, d, d, None, 7.5, d, 2, 2, sk,
+                                     None, d, 1 << 30, None) == N.NV_ERR_INVALID_ARG
+    assert lib.nv_denoise_store_pool(None, C.byref(s), d, k, 65, d, d, None, 7.5, d, 2, 2, sk,
+                                     dst, d, 1 << 30, None) == N.NV_ERR_INVALID_ARG
