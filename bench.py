@@ -32,7 +32,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="sd15_b1",
-                    help="sd15_b1 (default), sd15_b8_mixed, sdxl_b2, retrieval_heavy")
+                    help="sd15_b1 (default), sd15_b8_mixed, sdxl_b2, retrieval_heavy, "
+                         "sd15_lcbfu (a request stream through the LCBFU-maintained cache)")
     ap.add_argument("--k", type=int, default=None,
                     help="sd15_b1: place the query in this K's similarity band; "
                          "sdxl_b2: the skip count (default: first of the workload's K values)")
@@ -240,6 +241,8 @@ def main():
     import synth
 
     wl = synth.WORKLOADS[args.workload]
+    if "state_capacity" in wl:
+        return lcbfu_bench(args, wl)
     cfg = synth.unet_config(wl["unet"])
     S = synth.SCHEDULE_SD
     sched = (S["T"], wl["N"], S["beta_start"], S["beta_end"])
@@ -333,32 +336,13 @@ def main():
         step()
     torch.cuda.synchronize()
     print("[bench] timing", file=sys.stderr, flush=True)
-    fams = {"conv3x3_igemm": P.FAM_CONV, "linear_gemm": P.FAM_LINEAR, "attention": P.FAM_ATTN,
-            "cache_scan": P.FAM_SCAN}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    # Per-launch kernel times: HIP events that each dispatch of the traced
-    # families timestamps at kernel start and end, over a repeat of the timed
-    # steps (the timed run above carries no events).
-    kern = {}
-    if not args.no_trace:
-        print("[bench] traced repeat", file=sys.stderr, flush=True)
-        P.nv_trace_enable(sum(fams.values()), min(1 << 19, 8000 * args.steps * B + 64))
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        P.nv_trace_disable()
-        for name, f in fams.items():
-            n, kms, kfl, kby = P.nv_trace_read(f)
-            if n:
-                kern[name] = {"launches": n, "avg_us": 1e3 * kms / n,
-                              "total_ms_per_step": kms / args.steps,
-                              "tflops": kfl / (kms * 1e-3) / 1e12 if kms else None,
-                              "gbps": kby / (kms * 1e-3) / 1e9 if kms else None}
+    kern = trace_kernels(step, args, P, torch, B)
     ms = dt * 1e3 / args.steps
     ks_last = ks_seen[-1]
     K = ks_last[0] if len(ks_last) == 1 else ks_last
@@ -389,6 +373,50 @@ def main():
         "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16,
         "kernels": kern,
     }
+    add_roofline(out, kern, args, P, dev)
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = src * 2.0                      # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(
+            cfg, weights, wl, ks_last, cache if has_cache else None,
+            q[:m_look] if has_cache else None,
+            cond, unc, d_cache if has_cache else None,
+            synth.make_pooled(B, cfg["pooled_dim"], wl["pooled_seed"]) if d_pooled is not None
+            else None)
+    print(json.dumps(out))
+
+
+def trace_kernels(step, args, P, torch, B):
+    """Per-launch kernel times: HIP events that each dispatch of the traced families
+    timestamps at kernel start and end, over a repeat of the timed steps (the timed
+    run itself carries no events)."""
+    fams = {"conv3x3_igemm": P.FAM_CONV, "linear_gemm": P.FAM_LINEAR, "attention": P.FAM_ATTN,
+            "cache_scan": P.FAM_SCAN}
+    kern = {}
+    if args.no_trace:
+        return kern
+    print("[bench] traced repeat", file=sys.stderr, flush=True)
+    P.nv_trace_enable(sum(fams.values()), min(1 << 19, 8000 * args.steps * B + 64))
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    P.nv_trace_disable()
+    for name, f in fams.items():
+        n, kms, kfl, kby = P.nv_trace_read(f)
+        if n:
+            kern[name] = {"launches": n, "avg_us": 1e3 * kms / n,
+                          "total_ms_per_step": kms / args.steps,
+                          "tflops": kfl / (kms * 1e-3) / 1e12 if kms else None,
+                          "gbps": kby / (kms * 1e-3) / 1e9 if kms else None}
+    return kern
+
+
+def add_roofline(out, kern, args, P, dev):
+    """Roofline of the dominant traced kernel family, and the peaks measured on this GPU."""
     dom = max(kern, key=lambda k: kern[k]["total_ms_per_step"]) if kern else None
     d = kern.get(dom)
     out["kernel_timing"] = ("HIP events timestamped by each dispatch at kernel start / end, "
@@ -415,19 +443,190 @@ def main():
         meas = pk["hbm_read_gbps"] if r["bound"] == "hbm" else pk["f16_tflops"]
         r["peak_measured"] = meas
         r["frac_of_measured"] = r["achieved"] / meas
-    if args.calib_copy:
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        dst = src * 2.0                      # reads 1 GiB, writes 1 GiB
-        torch.cuda.synchronize()
-        del src, dst
+
+
+def oracle_maintainer_s(slots, cap):
+    """Seconds the oracle's maintainer takes for one insertion at the limit (|K-set|
+    evictions), timed on a 5000-state instance and scaled linearly to cap states (each
+    oracle eviction scans every stored state)."""
+    from oracle.lcbfu import LCBFU
+    small = 1000 * len(slots)
+    o = LCBFU(slots, small, small)
+    o.insert(1000)
+    rng = np.random.default_rng(0)
+    o.access(list(rng.integers(0, 1000, 2000)), list(rng.choice(slots, 2000)))
+    t0 = time.perf_counter()
+    for _ in range(10):
+        o.insert(1)
+    return (time.perf_counter() - t0) / 10 * cap / small
+
+
+def lcbfu_bench(args, wl):
+    """A request stream served through the LCBFU-maintained cache (Sec. 5.4): per
+    step, lookup over the live rows -> hole-aware fetch from the state pool (largest
+    stored K' <= K) -> access counts -> for misses, eviction / row compaction plan,
+    applied on the device -> the remaining N - K' guided steps, storing a miss's
+    states into the pool -> insertion of its embedding."""
+    import torch
+
+    import paper_2312_04429_amd as P
+    import synth
+    cfg = synth.unet_config(wl["unet"])
+    SD = synth.SCHEDULE_SD
+    sched = (SD["T"], wl["N"], SD["beta_start"], SD["beta_end"])
+    B, d, cap, n0 = wl["batch"], wl["d"], wl["state_capacity"], wl["n_prompts"]
+    thr = [t_ for t_, _ in wl["thresholds"]]
+    kv = [k for _, k in wl["thresholds"]]
+    slots = sorted(kv)
+    S = len(slots)
+    ecap = cap
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    lat = (cfg["in_ch"], cfg["H"], cfg["W"])
+    print(f"[bench] prefill: {n0} prompts, {cap} states", file=sys.stderr, flush=True)
+    d_cache = torch.empty((ecap, d), dtype=torch.bfloat16, device=dev)
+    d_cache[:n0] = synth.make_cache_device(n0, d, wl["clusters"], wl["sigma"], wl["cache_seed"],
+                                           dev)
+    pool = torch.empty((cap,) + lat, dtype=torch.float32, device=dev)
+    for i in range(0, cap, 1 << 16):
+        pool[i:i + (1 << 16)].normal_()
+    table = torch.full((ecap, S), -1, dtype=torch.int32, device=dev)
+    payload = torch.full((ecap,), -1, dtype=torch.int32, device=dev)
+    lc = P.NvLCBFU(slots, cap, ecap)
+    for i in range(0, n0, 100_000):
+        m = min(100_000, n0 - i)
+        plan = lc.insert(m)
+        assert plan["kept"] == i and len(plan["move_src"]) == 0
+        P.nv_table_update(table, t(plan["upd"]))
+        payload[i:i + m] = t(plan["entries"])
+    rng = np.random.default_rng(wl["access_seed"])
+    na, ex = wl["prefill_accesses"], wl["popularity_exponent"]
+    lc.access(np.minimum((n0 * rng.random(na) ** ex).astype(np.int64), n0 - 1),
+              rng.choice(slots, size=na).astype(np.int32))
+    n = [n0]
+    # the request stream (inputs, resident before timing)
+    R = (args.warmup + 2 * args.steps) * B
+    rq = np.random.default_rng(wl["query_seed"])
+    miss = rq.random(R) < wl["p_miss"]
+    tgt = np.minimum((n0 * rq.random(R) ** ex).astype(np.int64), n0 - 1)
+    sims = np.asarray([BAND[int(k)] for k in rq.choice(slots, size=R)])
+    q = np.empty((R, d), np.float32)
+    hit = np.nonzero(~miss)[0]
+    rows = d_cache[t(tgt[hit])].view(torch.int16).cpu().numpy().view(np.uint16)
+    q[hit] = synth.make_queries_at_sims(synth.from_bf16_bits(rows), sims[hit], wl["query_seed"])
+    mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev).cpu().numpy()
+    q[miss] = synth.cluster_queries_from(mu, int(miss.sum()), wl["sigma"], wl["query_seed"] + 1)
+    d_q = t(q)
+    lws_bytes = P.nv_cache_lookup_workspace(B, ecap, d)
+    lws_own, lws_addr = P.workspace(lws_bytes, dev)
+    lws = (lws_own, lws_addr, lws_bytes)
+    weights = synth.make_weights(cfg, wl["weight_seed"])
+    net = P.NvUNet(cfg, weights)
+    cond = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["cond_seed"])
+    unc = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["uncond_seed"])
+    d_cond, d_unc = t(cond), t(unc)
+    d_noise = t(synth.make_latents(B, *lat, 2000))
+    x = torch.empty_like(d_noise)
+    log = {"served": [], "selected": [], "host_s": 0.0, "moves": 0, "misses": 0}
+    counter = [0]
+
+    def step():
+        i = counter[0]
+        counter[0] += 1
+        qs = d_q[i * B:(i + 1) * B]
+        nn = n[0]
+        idx, sim, kk = P.nv_cache_lookup(qs, d_cache[:nn], thr, kv, ws=lws)
+        k_sel = kk.clone()                       # the selector's K, kept for the report
+        P.nv_gather_pool(pool, table, slots, payload, nn, idx, kk, d_noise, out=x)
+        idx_h, k_h = idx.cpu().numpy(), kk.cpu().numpy()
+        h0 = time.perf_counter()
+        lc.access(idx_h, k_h)
+        miss_b = [b for b in range(B) if k_h[b] == 0]
+        dst = np.full((B, S), -1, np.int32)
+        plan = lc.insert(len(miss_b)) if miss_b else None
+        for j, b in enumerate(miss_b):
+            dst[b] = plan["pools"][j]
+        log["host_s"] += time.perf_counter() - h0
+        if plan is not None:
+            if len(plan["move_src"]):
+                P.nv_cache_move_rows(d_cache, nn, payload, t(plan["move_src"]),
+                                     t(plan["move_dst"]))
+            P.nv_table_update(table, t(plan["upd"]))
+            nn = plan["kept"]
+            log["moves"] += len(plan["move_src"])
+        net.nv_denoise_store_pool(x, k_h.tolist(), d_cond, d_unc, pool, slots, dst,
+                                  guidance=wl["guidance"], sched=sched)
+        if plan is not None:
+            ent = t(plan["entries"])
+            for j, b in enumerate(miss_b):
+                nn = P.nv_cache_insert(qs[b:b + 1], d_cache, nn, entry=ent[j:j + 1],
+                                       payload=payload)
+        n[0] = nn
+        log["served"].append(k_h.tolist())
+        log["selected"].append(k_sel.cpu().tolist())
+        log["misses"] += len(miss_b)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    info0 = lc.info()
+    log.update(served=[], selected=[], host_s=0.0, moves=0, misses=0)
+    print("[bench] timing", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    info1 = lc.info()
+    served = [k for ks in log["served"] for k in ks]
+    selected = [k for ks in log["selected"] for k in ks]
+    stream = {
+        "requests": len(served), "misses": log["misses"],
+        "hit_rate": 1 - log["misses"] / len(served),
+        "served_k": {str(k): served.count(k) for k in [0] + slots},
+        "hole_fallbacks": sum(1 for a, b in zip(selected, served) if 0 < b < a),
+        "hole_misses": sum(1 for a, b in zip(selected, served) if a > 0 and b == 0),
+        "evicted": info1["evicted"] - info0["evicted"],
+        "prompts_dropped": info1["dropped"] - info0["dropped"], "row_moves": log["moves"],
+        "host_maintainer_us_per_step": 1e6 * log["host_s"] / args.steps,
+        "rows_live": info1["rows"], "states_live": info1["states"],
+    }
+    kern = trace_kernels(step, args, P, torch, B)
+    unet_steps = sum(wl["N"] - k for k in served)
+    fl_step = 2 * unet_flops_per_row(cfg)
+    ups = unet_steps / dt
+    config = {"workload": args.workload, "unet": "SD-1.5-shaped (859.5M params, random-init)",
+              "latent": list(lat), "batch": B, "cfg_rows": 2 * B, "N": wl["N"],
+              "K": "per request: the largest stored K' <= the selector's K",
+              "guidance": wl["guidance"],
+              "cache": f"{n0} prompts x {d} bf16 (rows change with the stream)",
+              "state_pool": f"{cap} states x {int(np.prod(lat)) * 4} B = "
+                            f"{cap * int(np.prod(lat)) * 4 / 1e9:.1f} GB in HBM",
+              "path": "maintained cache: lookup, hole-aware fetch, LCBFU eviction and row "
+                      "compaction on misses, generation storing a miss's 5 states, insertion"}
+    out = {
+        "metric": "images/sec and UNet steps/sec at skip K (SD1.5-shape, 1 GPU); % MFMA peak",
+        "value": len(served) / dt, "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": dt * 1e3 / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": config, "stream": stream,
+        "unet_steps_per_s": ups, "unet_step_ms": 1e3 / ups, "unet_step_tflop": fl_step / 1e12,
+        "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16, "kernels": kern,
+    }
+    add_roofline(out, kern, args, P, dev)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(
-            cfg, weights, wl, ks_last, cache if has_cache else None,
-            q[:m_look] if has_cache else None,
-            cond, unc, d_cache if has_cache else None,
-            synth.make_pooled(B, cfg["pooled_dim"], wl["pooled_seed"]) if d_pooled is not None
-            else None)
+        wl_cpu = dict(wl, n_cache=n[0])
+        cb = cpu_baseline(cfg, weights, wl_cpu, served, None, q[:len(served)], cond, unc,
+                          d_cache, None)
+        t_m = oracle_maintainer_s(slots, cap)
+        total = len(served) / cb["value"] + stream["misses"] * t_m
+        cb["value"] = len(served) / total
+        cb["sample"] += (f"; maintainer: one insertion at the limit {t_m:.2f} s (10 timed on "
+                         f"a 5000-state instance, scaled to {cap} states) x {stream['misses']} "
+                         "misses")
+        out["cpu_baseline"] = cb
     print(json.dumps(out))
 
 

@@ -91,6 +91,21 @@ WORKLOADS = {
         unet="sdxl", N=50, guidance=7.5, weight_seed=0, batch=2, k_sweep=(10, 20),
         cond_seed=3, uncond_seed=4, pooled_seed=6,
     ),
+    # A maintained cache at the paper's operating point (Sec. 5.4: about 1.5 M
+    # states for 300 k prompts under the storage limit): 300 k prompts with all
+    # five states each fill the 1.5 M-state pool, so every miss evicts five.
+    # Requests: a miss (a fresh draw from the prompts' clusters) with
+    # probability p_miss (0.12, the overall hit rate 0.88 the evaluation
+    # reports), else a rewording of a cached prompt chosen with power-law
+    # popularity, at a similarity inside a K band drawn uniformly.  Access
+    # counts before the stream: 4 per prompt on average, same popularity.
+    "sd15_lcbfu": dict(
+        unet="sd15", n_prompts=300_000, state_capacity=1_500_000, d=768, cache_dtype="bf16",
+        clusters=1000, sigma=0.05, cache_seed=41, query_seed=42, access_seed=43,
+        p_miss=0.12, popularity_exponent=3.0, prefill_accesses=1_200_000,
+        N=50, guidance=7.5, thresholds=THRESHOLDS_PAPER, weight_seed=0, batch=1,
+        cond_seed=3, uncond_seed=4,
+    ),
     # 256 queries (half planted within cosine 0.95 of cached rows, half fresh
     # cluster draws, interleaved); the first 16 feed a batch-16 SD-1.5 denoise
     # at their own K (misses start from noise, K = 0).
