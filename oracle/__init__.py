@@ -9,7 +9,9 @@ from the paper's definitions:
                resume-from-step-K loop of approximate caching (Sec. 4.1);
   unet.py      the latent-diffusion UNet epsilon predictor (Sec. 2.1), fp32;
   lcbfu.py     cache maintenance under LCBFU and the hole-aware choice of the
-               state served (Sec. 5.4).
+               state served (Sec. 5.4);
+  predictor.py the match predictor, a linear one-class SVM trained by SGD
+               (Sec. 5.2, Sec. 6).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  The product path never imports it and shares no code with it.
