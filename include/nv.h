@@ -194,6 +194,38 @@ int32_t nv_lcbfu_info(const nv_lcbfu* h, int64_t* info);
 int32_t nv_lcbfu_export(const nv_lcbfu* h, int32_t* table, int32_t* rows, int64_t* counts);
 
 /* ------------------------------------------------------------------------ *
+ * Match predictor (Sec. 5.2, Sec. 6: a one-class SVM over the cached prompt
+ * embeddings decides whether a close match is likely; if not, the request
+ * skips the cache and is generated from scratch, Alg. 1).
+ *
+ * Model: linear, decision value s(q) = w.q - rho, match predicted iff
+ * s(q) >= tau.  Training minimises
+ *   J(w, rho) = nu/2 |w|^2 - nu rho + (1/n) sum_i max(0, rho - w.x_i)
+ * by plain SGD in float64 from w = 0, rho = 0: at step t (0-based) over row
+ * i = order[t], eta = eta0 / (1 + eta0 nu t); if rho - w.x_i > 0,
+ * w -= eta (nu w - x_i) and rho -= eta (1 - nu), else w -= eta nu w and
+ * rho += eta nu.  Every w.x is a left-to-right sum of rounded float64
+ * products with no fused multiply-add, so results are bit-reproducible.
+ *
+ * nv_ocsvm_train (host only): rows HOST [n][d] of c_dtype (the vector DB's
+ * embeddings), order HOST int64 [T] (the visiting order; the caller draws
+ * it), w_out HOST float64 [d], rho_out HOST.
+ *
+ * nv_match_gate: scores the queries (device f32 [m][d]) with w (device
+ * float64 [d]) and, when idx / sim / k (device, a lookup's outputs for the
+ * same queries) are given, turns every query with s < tau into "no match":
+ * idx = -1, sim = -inf, k = 0.  score_out (device float64 [m]) may be NULL
+ * when idx is given, and idx / sim / k NULL to only score.  Applied after
+ * the lookup, it gives Alg. 1's result with the predictor in front.
+ * ------------------------------------------------------------------------ */
+int32_t nv_ocsvm_train(const void* rows, int32_t c_dtype, int64_t n, int32_t d, double nu,
+                       double eta0, const int64_t* order, int64_t T, double* w_out,
+                       double* rho_out);
+int32_t nv_match_gate(const float* queries, int32_t m, int32_t d, const double* w, double rho,
+                      double tau, double* score_out, int64_t* idx, float* sim, int32_t* k,
+                      void* stream);
+
+/* ------------------------------------------------------------------------ *
  * Latent-diffusion UNet (Sec. 2.1: UNet backbone, text conditioning through
  * cross-attention, operating on latents).  Topology rule:
  *   conv_in; per level l: n_res ResBlocks (+ transformer of depth[l] if > 0),

@@ -135,6 +135,37 @@ def nv_cache_move_rows(cache, n, payload, src, dst):
     N.check(st, "nv_cache_move_rows")
 
 
+def nv_ocsvm_train(rows, nu, order, eta0=1.0):
+    """Train the match predictor on host rows (numpy float32, or uint16 bfloat16 bits
+    [n][d]) in the visiting order (host int64 [T]).  Returns (w float64 [d], rho)."""
+    rows = np.ascontiguousarray(rows)
+    cdt = N.NV_BF16 if rows.dtype in (np.uint16, np.int16) else N.NV_F32
+    if cdt == N.NV_F32 and rows.dtype != np.float32:
+        raise ValueError("rows must be float32 or bfloat16 bits")
+    order = np.ascontiguousarray(order, dtype=np.int64)
+    n, d = rows.shape
+    w = np.empty(d, np.float64)
+    rho = C.c_double()
+    st = N.lib.nv_ocsvm_train(rows.ctypes.data, cdt, n, d, float(nu), float(eta0),
+                              order.ctypes.data, len(order), w.ctypes.data, C.byref(rho))
+    N.check(st, "nv_ocsvm_train")
+    return w, rho.value
+
+
+def nv_match_gate(queries, w, rho, tau=0.0, idx=None, sim=None, k=None, score=True):
+    """Decision values w.q - rho of the queries (float64 device [m]) and, when a
+    lookup's (idx, sim, k) are given, 'no match' for every query below tau."""
+    _need_cuda(queries, w, idx, sim, k)
+    assert queries.dtype == torch.float32 and queries.is_contiguous()
+    assert w.dtype == torch.float64 and w.numel() == queries.shape[1]
+    m, d = queries.shape
+    out = torch.empty(m, dtype=torch.float64, device=queries.device) if score else None
+    st = N.lib.nv_match_gate(_p(queries), m, d, _p(w), float(rho), float(tau), _p(out),
+                             _p(idx), _p(sim), _p(k), _stream())
+    N.check(st, "nv_match_gate")
+    return out
+
+
 class NvLCBFU:
     """Host LCBFU maintainer (native); arrays in and out are host numpy arrays."""
 
