@@ -132,3 +132,69 @@ def test_guidance_one_is_conditional_only():
     a = ddim.denoise(U.make_eps_fn(net, ctx[0], ctx[1]), x, 15, 20, S, 1.0)
     b = ddim.denoise(lambda v, t: (net(v, t, ctx[0]), net(v, t, ctx[0])), x, 15, 20, S, 1.0)
     np.testing.assert_allclose(a, b, rtol=1e-4, atol=1e-5)
+
+
+@pytest.mark.parametrize("i", [0, 10, 24, 49])
+def test_stochastic_step_eta0_and_eta1(i):
+    """eta = 0 is the deterministic update bit for bit (any z).  eta = 1 matches the
+    forward process's posterior q(x_prev | x_t, x_0) obtained by Gaussian conditioning
+    (Schur complement of the joint of x_prev and x_t given x_0): variance and mean."""
+    S = synth.SCHEDULE_SD
+    _, a_t, a_p = schedule.step_alphas(i, 50, S)
+    rng = np.random.default_rng(i)
+    x0 = rng.standard_normal(64).astype(np.float32)
+    e = rng.standard_normal(64).astype(np.float32)
+    xt = (np.sqrt(np.float32(a_t)) * x0 + np.sqrt(np.float32(1 - a_t)) * e).astype(np.float32)
+    z = rng.standard_normal(64).astype(np.float32)
+    assert np.array_equal(ddim.ddim_step_eta(xt, e, a_t, a_p, 0.0, z), ddim.ddim_step(xt, e, a_t, a_p))
+    at, ap = float(a_t), float(a_p)
+    cov = math.sqrt(at / ap) * (1 - ap)                 # Cov(x_prev, x_t | x_0)
+    var_post = (1 - ap) - cov * cov / (1 - at)
+    sig = float(ddim.ddim_sigma(a_t, a_p, 1.0))
+    assert abs(sig * sig - var_post) <= 1e-4 * var_post   # float32 sigma
+    mean_post = math.sqrt(ap) * x0.astype(np.float64) + cov / (1 - at) * (
+        xt.astype(np.float64) - math.sqrt(at) * x0)
+    got = ddim.ddim_step_eta(xt, e, a_t, a_p, 1.0, np.zeros(64, np.float32))
+    np.testing.assert_allclose(got, mean_post, rtol=0, atol=2e-5)
+
+
+@pytest.mark.parametrize("eta", [0.0, 0.5, 1.0])
+def test_stochastic_step_keeps_the_marginal(eta):
+    """With the true eps, every member of the family maps x_t ~ q(x_t | x_0) to
+    x_prev ~ q(x_prev | x_0): mean sqrt(a_prev) x_0, variance 1 - a_prev."""
+    S = synth.SCHEDULE_SD
+    _, a_t, a_p = schedule.step_alphas(20, 50, S)
+    rng = np.random.default_rng(7)
+    n = 400_000
+    x0 = np.float32(0.8)
+    e = rng.standard_normal(n).astype(np.float32)
+    z = rng.standard_normal(n).astype(np.float32)
+    xt = (np.sqrt(np.float32(a_t)) * x0 + np.sqrt(np.float32(1 - a_t)) * e).astype(np.float32)
+    xp = ddim.ddim_step_eta(xt, e, a_t, a_p, eta, z).astype(np.float64)
+    assert abs(xp.mean() - math.sqrt(float(a_p)) * 0.8) < 5e-3
+    assert abs(xp.var() - (1 - float(a_p))) < 5e-3
+
+
+def test_stochastic_step_by_hand_and_resumption():
+    """With eps = 0 the update is x_prev = sqrt(a_p / a_t) x_t + sigma z (worked by hand in
+    float64).  A run resumed at step i from the full run's state, with the same per-step
+    draws noise[step], reproduces the full run's tail exactly (draws are indexed by the
+    grid step, not by the resumed run's own count)."""
+    S = synth.SCHEDULE_SD
+    _, a_t, a_p = schedule.step_alphas(30, 50, S)
+    xt = np.array([0.5, -1.25, 2.0], np.float32)
+    z = np.array([1.0, 0.5, -2.0], np.float32)
+    sig = math.sqrt((1 - float(a_p)) / (1 - float(a_t))) * math.sqrt(1 - float(a_t) / float(a_p))
+    want = math.sqrt(float(a_p) / float(a_t)) * xt.astype(np.float64) + 0.7 * sig * z
+    got = ddim.ddim_step_eta(xt, np.zeros(3, np.float32), a_t, a_p, 0.7, z)
+    np.testing.assert_allclose(got, want, rtol=1e-6, atol=1e-7)
+    rng = np.random.default_rng(3)
+    noise = rng.standard_normal((20, 6)).astype(np.float32)
+    x = rng.standard_normal(6).astype(np.float32)
+    fn = lambda v, t: ((0.05 * v).astype(np.float32), (0.1 * v + 0.01).astype(np.float32))
+    states = {}
+    full = ddim.denoise(fn, x, 0, 20, S, 2.0, record=lambda i, v: states.__setitem__(i, v),
+                        eta=0.6, noise=noise)
+    for i in (3, 11):
+        tail = ddim.denoise(fn, states[i], i, 20, S, 2.0, eta=0.6, noise=noise)
+        assert np.array_equal(tail, full)
