@@ -41,6 +41,9 @@ def parse():
                     help="the cache-miss path instead: queries far from every cached prompt, "
                          "full generation storing the states after each K of the table, and "
                          "insertion of the new embeddings into the cache")
+    ap.add_argument("--predictor", action="store_true",
+                    help="sd15_lcbfu: put the match predictor (linear one-class SVM trained on "
+                         "the prefilled embeddings, nu = 0.001) in front of the lookup")
     ap.add_argument("--scan-only", action="store_true",
                     help="time the lookup alone, warm (back to back) and cold (a 2 GiB write "
                          "between repetitions evicts the cache from the Infinity Cache)")
@@ -517,6 +520,15 @@ def lcbfu_bench(args, wl):
     mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev).cpu().numpy()
     q[miss] = synth.cluster_queries_from(mu, int(miss.sum()), wl["sigma"], wl["query_seed"] + 1)
     d_q = t(q)
+    gate = None
+    if args.predictor:
+        print("[bench] training the match predictor", file=sys.stderr, flush=True)
+        host_rows = d_cache[:n0].view(torch.int16).cpu().numpy().view(np.uint16)
+        order = np.random.default_rng(wl["access_seed"] + 1).permutation(n0)
+        t0 = time.perf_counter()
+        w_p, rho_p = P.nv_ocsvm_train(host_rows, 0.001, order)
+        gate = (t(w_p), rho_p, time.perf_counter() - t0)
+        del host_rows
     lws_bytes = P.nv_cache_lookup_workspace(B, ecap, d)
     lws_own, lws_addr = P.workspace(lws_bytes, dev)
     lws = (lws_own, lws_addr, lws_bytes)
@@ -527,7 +539,7 @@ def lcbfu_bench(args, wl):
     d_cond, d_unc = t(cond), t(unc)
     d_noise = t(synth.make_latents(B, *lat, 2000))
     x = torch.empty_like(d_noise)
-    log = {"served": [], "selected": [], "host_s": 0.0, "moves": 0, "misses": 0}
+    log = {"served": [], "selected": [], "gated": [], "host_s": 0.0, "moves": 0, "misses": 0}
     counter = [0]
 
     def step():
@@ -537,6 +549,8 @@ def lcbfu_bench(args, wl):
         nn = n[0]
         idx, sim, kk = P.nv_cache_lookup(qs, d_cache[:nn], thr, kv, ws=lws)
         k_sel = kk.clone()                       # the selector's K, kept for the report
+        if gate is not None:
+            g_score = P.nv_match_gate(qs, gate[0], gate[1], 0.0, idx, sim, kk)
         P.nv_gather_pool(pool, table, slots, payload, nn, idx, kk, d_noise, out=x)
         idx_h, k_h = idx.cpu().numpy(), kk.cpu().numpy()
         h0 = time.perf_counter()
@@ -564,6 +578,8 @@ def lcbfu_bench(args, wl):
         n[0] = nn
         log["served"].append(k_h.tolist())
         log["selected"].append(k_sel.cpu().tolist())
+        if gate is not None:
+            log["gated"].append((g_score.cpu().numpy() >= 0.0).tolist())
         log["misses"] += len(miss_b)
 
     print("[bench] warmup", file=sys.stderr, flush=True)
@@ -571,7 +587,7 @@ def lcbfu_bench(args, wl):
         step()
     torch.cuda.synchronize()
     info0 = lc.info()
-    log.update(served=[], selected=[], host_s=0.0, moves=0, misses=0)
+    log.update(served=[], selected=[], gated=[], host_s=0.0, moves=0, misses=0)
     print("[bench] timing", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -592,6 +608,16 @@ def lcbfu_bench(args, wl):
         "host_maintainer_us_per_step": 1e6 * log["host_s"] / args.steps,
         "rows_live": info1["rows"], "states_live": info1["states"],
     }
+    if gate is not None:
+        said = [g for gs in log["gated"] for g in gs]       # predicted: a close match exists
+        pos = [s_ > 0 for s_ in selected]                  # the lookup found a usable match
+        tp = sum(1 for a, b in zip(said, pos) if a and b)
+        stream["predictor"] = {
+            "nu": 0.001, "tau": 0.0, "train_s": gate[2], "train_rows": n0,
+            "predicted_match": sum(said), "precision": tp / max(1, sum(said)),
+            "recall": tp / max(1, sum(pos)),
+            "note": "a request predicted to have no match is generated from scratch even if "
+                    "the cache holds one (a false negative)"}
     kern = trace_kernels(step, args, P, torch, B)
     unet_steps = sum(wl["N"] - k for k in served)
     fl_step = 2 * unet_flops_per_row(cfg)

@@ -314,6 +314,19 @@ int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* latent, const 
                    int32_t B, const float* cond, const float* uncond, const float* pooled,
                    float guidance, void* workspace, size_t workspace_bytes, void* stream);
 
+/* nv_denoise with DDIM's stochastic samplers (eta in [0, 1]): each update is
+ *   x <- sqrt(a_p) x0 + sqrt(1 - a_p - sigma^2) eps + sigma z,
+ *   sigma = eta sqrt((1 - a_p) / (1 - a_t)) sqrt(1 - a_t / a_p),
+ * with x0 = (x - sqrt(1 - a_t) eps) / sqrt(a_t) and z = noise[b][i] for
+ * sample b at grid step i; noise: device f32 [B][N][in_ch][H][W] of standard
+ * normal draws that the caller makes (a new seed after a cache hit makes the
+ * tail of the trajectory, and the image, differ: the diversity remedy of
+ * Sec. 9).  eta = 0 is the deterministic update of nv_denoise. */
+int32_t nv_denoise_eta(nv_unet* net, const nv_schedule* sched, float* latent, const int32_t* k,
+                       int32_t B, const float* cond, const float* uncond, const float* pooled,
+                       float guidance, float eta, const float* noise, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 /* The cache-miss side of Alg. 1 (Sec. 4.3: a request without a suitable
  * cache generates from scratch and its intermediate states join the cache):
  * exactly nv_denoise, and in addition, whenever sample b has completed

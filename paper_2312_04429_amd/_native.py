@@ -52,6 +52,8 @@ _sigs = {
     "nv_denoise_store": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, VP, I64,
                                I32, VP, VP, VP, SZ, VP]),
     "nv_cache_insert": (I32, [VP, I32, I32, VP, I32, I64, I64, VP, VP, VP]),
+    "nv_denoise_eta": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32, F32, VP,
+                             VP, SZ, VP]),
     "nv_denoise_store_pool": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, F32,
                                     VP, I64, I32, VP, VP, VP, SZ, VP]),
     "nv_gather_pool": (I32, [VP, I64, VP, I64, I32, VP, VP, I64, VP, VP, VP, I32, I64, VP, VP]),

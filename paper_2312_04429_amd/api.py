@@ -294,6 +294,24 @@ class NvUNet:
         N.check(st, "nv_denoise")
         return latent
 
+    def nv_denoise_eta(self, latent, k, cond, uncond, eta, noise, pooled=None, guidance=7.5,
+                       sched=(1000, 50, 0.00085, 0.012)):
+        """nv_denoise with DDIM's stochastic update: noise f32 [B][N][C][H][W] holds the
+        standard normal draws of every sample and grid step."""
+        _need_cuda(latent, cond, uncond, pooled, noise)
+        B = latent.shape[0]
+        if noise.dtype != torch.float32 or tuple(noise.shape[:2]) != (B, sched[1]) or \
+                noise[0, 0].numel() != latent[0].numel() or not noise.is_contiguous():
+            raise ValueError("noise must be contiguous float32 [B][N][*latent]")
+        kk = (C.c_int32 * B)(*[int(v) for v in k])
+        s = N.make_schedule(*sched)
+        _own, addr, need = self._workspace(B, latent.device)
+        st = N.lib.nv_denoise_eta(self._h, C.byref(s), _p(latent), kk, B, _p(cond), _p(uncond),
+                                  _p(pooled), float(guidance), float(eta), _p(noise),
+                                  C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_denoise_eta")
+        return latent
+
     def nv_denoise_store(self, latent, k, cond, uncond, store, slot_k, entry, pooled=None,
                          guidance=7.5, sched=(1000, 50, 0.00085, 0.012)):
         """nv_denoise that also copies each sample's state after slot_k[s] steps to

@@ -41,7 +41,7 @@ hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Ci
                           int C0, int rows, _Float16* out, hipStream_t s);
 hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C, int HW,
                            int samples, float guidance, const float* a_t, const float* a_prev,
-                           hipStream_t s);
+                           float eta, const float* z, int N, hipStream_t s);
 hipError_t eps_split_launch(const float* eps, int C, int HW, int samples, float* eu, float* ec,
                             hipStream_t s);
 hipError_t ctx_rows_launch(const StepArgs& st, const float* cond, const float* uncond,

@@ -370,12 +370,18 @@ __global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
   }
 }
 
-// eps = eps_u + s (eps_c - eps_u); x <- sqrt(a_p) (x - sqrt(1-a_t) eps)/sqrt(a_t) + sqrt(1-a_p) eps
+// eps = eps_u + s (eps_c - eps_u); x0 = (x - sqrt(1-a_t) eps) / sqrt(a_t);
+// x <- sqrt(a_p) x0 + sqrt(1 - a_p - sigma^2) eps + sigma z, with
+// sigma = eta sqrt((1-a_p)/(1-a_t)) sqrt(1 - a_t/a_p) (DDIM's family of
+// samplers; eta = 0 without z is the deterministic update).  z: the caller's
+// standard normal draws [samples][N][C][HW], indexed by the caller's sample
+// order and the grid step, or null.
 __global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __restrict__ eps,
                                                   float* __restrict__ x, int C, int HW,
                                                   int samples, float guidance,
                                                   const float* __restrict__ a_t,
-                                                  const float* __restrict__ a_prev) {
+                                                  const float* __restrict__ a_prev, float eta,
+                                                  const float* __restrict__ z, int N) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)samples * C * HW;
   if (i >= total) return;
@@ -389,7 +395,14 @@ __global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __re
   const float e = eu + guidance * (ec - eu);
   const float xv = x[i];
   const float x0 = (xv - sqrtf(1.0f - at) * e) / sqrtf(at);
-  x[i] = sqrtf(ap) * x0 + sqrtf(1.0f - ap) * e;
+  // one instruction sequence for both forms, so eta = 0 gives the deterministic bits
+  float sigma = 0.0f, zv = 0.0f;
+  if (z) {
+    sigma = eta * sqrtf((1.0f - ap) / (1.0f - at)) * sqrtf(1.0f - at / ap);
+    zv = z[((int64_t)st.perm[b] * N + step) * ((int64_t)C * HW) + rem];
+  }
+  const float v = sqrtf(ap) * x0 + sqrtf(fmaxf(1.0f - ap - sigma * sigma, 0.0f)) * e;
+  x[i] = v + sigma * zv;
 }
 
 // eps rows [rows][HW][C] float32 -> eps_u / eps_c [samples][C][HW].
@@ -598,10 +611,10 @@ hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Ci
 
 hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C, int HW,
                            int samples, float guidance, const float* a_t, const float* a_prev,
-                           hipStream_t s) {
+                           float eta, const float* z, int N, hipStream_t s) {
   const int64_t total = (int64_t)samples * C * HW;
   hipLaunchKernelGGL(cfg_ddim_k, dim3(blocks_for(total)), dim3(256), 0, s, st, eps, x, C, HW,
-                     samples, guidance, a_t, a_prev);
+                     samples, guidance, a_t, a_prev, eta, z, N);
   return hipGetLastError();
 }
 

@@ -1153,10 +1153,18 @@ struct Snapshots {
   std::vector<int64_t> dst;  // [B][n_slots]
 };
 
+// Stochastic DDIM (eta > 0): the caller's standard normal draws per sample and
+// grid step, device f32 [B][N][latent].
+struct Stochastic {
+  float eta = 0.0f;
+  const float* z = nullptr;
+};
+
 static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* latent,
                             const int32_t* k, int32_t B, const float* cond, const float* uncond,
                             const float* pooled, float guidance, void* workspace,
-                            size_t workspace_bytes, void* stream, const Snapshots* snap) {
+                            size_t workspace_bytes, void* stream, const Snapshots* snap,
+                            const Stochastic* sto = nullptr) {
   NV_CHECK_ARG(latent && k, "null latent or k");
   NV_CHECK_ARG(std::isfinite(guidance), "guidance must be finite");
   Plan* P = nullptr;
@@ -1212,7 +1220,8 @@ static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* laten
     NV_HIP_TRY(run_ops(P->step, rc));
     NV_HIP_TRY(cfg_ddim_launch(rc.st, (const float*)(ws + P->eps), (float*)(ws + P->x_work),
                                c.out_ch, HW, A, guidance, (const float*)(ws + P->at),
-                               (const float*)(ws + P->ap), s));
+                               (const float*)(ws + P->ap), sto ? sto->eta : 0.0f,
+                               sto ? sto->z : nullptr, N, s));
     for (int a = 0; a < A; ++a) NV_HIP_TRY(take(a, sa.kstep[a] + j + 1));
   }
   NV_HIP_TRY(permute_launch(sa, (const float*)(ws + P->x_work), latent, lat, B, 0, s));
@@ -1226,6 +1235,21 @@ extern "C" int32_t nv_denoise(nv_unet* net, const nv_schedule* sched, float* lat
   clear_error();
   return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
                       workspace_bytes, stream, nullptr);
+}
+
+extern "C" int32_t nv_denoise_eta(nv_unet* net, const nv_schedule* sched, float* latent,
+                                  const int32_t* k, int32_t B, const float* cond,
+                                  const float* uncond, const float* pooled, float guidance,
+                                  float eta, const float* noise, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  clear_error();
+  NV_CHECK_ARG(noise, "null noise");
+  NV_CHECK_ARG(eta >= 0.0f && eta <= 1.0f, "eta must be in [0, 1]");
+  Stochastic sto;
+  sto.eta = eta;
+  sto.z = noise;
+  return denoise_impl(net, sched, latent, k, B, cond, uncond, pooled, guidance, workspace,
+                      workspace_bytes, stream, nullptr, &sto);
 }
 
 extern "C" int32_t nv_denoise_store(nv_unet* net, const nv_schedule* sched, float* latent,
