@@ -11,7 +11,9 @@ from the paper's definitions:
   lcbfu.py     cache maintenance under LCBFU and the hole-aware choice of the
                state served (Sec. 5.4);
   predictor.py the match predictor, a linear one-class SVM trained by SGD
-               (Sec. 5.2, Sec. 6).
+               (Sec. 5.2, Sec. 6);
+  ivf.py       an inverted-file approximate index over the cached embeddings
+               (the indexed vector-DB search of Sec. 5.3 / Sec. 6).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  The product path never imports it and shares no code with it.
