@@ -194,6 +194,52 @@ int32_t nv_lcbfu_info(const nv_lcbfu* h, int64_t* info);
 int32_t nv_lcbfu_export(const nv_lcbfu* h, int32_t* table, int32_t* rows, int64_t* counts);
 
 /* ------------------------------------------------------------------------ *
+ * IVF approximate index over the cached embeddings (the paper's vector DB
+ * searches through an index, Sec. 5.3 / Sec. 6; an exact scan is
+ * nv_cache_lookup).  Scores are the lookup's canonical float64 scores; every
+ * order is total (ties to the lower list / row), so results are
+ * reproducible bit for bit.
+ *
+ * nv_ivf_build: cache device [n][d] of c_dtype (d a multiple of 8, <= 2048);
+ * init HOST int64 [L] (1 <= L <= min(n, 8192)): the rows that start the
+ * centroids.  iters Lloyd steps (0..100) each assign every row to its best
+ * centroid (lower list on ties) and replace each non-empty list's centroid
+ * by its normalised mean: the float64 sum of its rows in ascending row
+ * order, divided by the correctly rounded square root of the left-to-right
+ * sum of squares, rounded to float32 and then to the cache type.  A final
+ * assignment gives lists (device int64 [n]); perm (device int64 [n]) holds
+ * the row ids grouped by list, ascending within a list; offsets (device
+ * int64 [L + 1]) delimit the lists; ivf_rows (device [n][d] of c_dtype)
+ * receives the rows in perm order; cents (device [L][d] of c_dtype) the
+ * centroids; *max_list (HOST) the longest list.  Synchronous on `stream`.
+ * workspace >= nv_ivf_build_workspace(n, d, L), 256-byte aligned.
+ *
+ * nv_ivf_search: queries device f32 [m][d] (1 <= m <= 4096); the index as
+ * built; 1 <= nprobe <= min(L, 256).  Each query ranks the lists by its
+ * score against their centroids (higher first, lower list on ties), scans
+ * the first nprobe, and returns the best row among them (higher score
+ * first, lower row on ties): idx_out (device int64 [m], the original row
+ * id, -1 if every probed list is empty), sim_out (device f32 [m], the score
+ * rounded to float32, -inf if none) and k_out (device int32 [m], the
+ * selector's K as in nv_cache_lookup).  probed_out (device int32
+ * [m][nprobe], may be NULL) receives the lists probed, in rank order.
+ * workspace >= nv_ivf_search_workspace(m, L, nprobe, max_list).
+ * nprobe = L gives the exact lookup's results.
+ * ------------------------------------------------------------------------ */
+size_t nv_ivf_build_workspace(int64_t n, int32_t d, int32_t L);
+int32_t nv_ivf_build(const void* cache, int32_t c_dtype, int64_t n, int32_t d,
+                     const int64_t* init, int32_t L, int32_t iters, void* cents, int64_t* lists,
+                     int64_t* perm, int64_t* offsets, void* ivf_rows, int64_t* max_list,
+                     void* workspace, size_t workspace_bytes, void* stream);
+size_t nv_ivf_search_workspace(int32_t m, int32_t L, int32_t nprobe, int64_t max_list);
+int32_t nv_ivf_search(const float* queries, int32_t m, int32_t d, const void* cents, int32_t L,
+                      const void* ivf_rows, int32_t c_dtype, const int64_t* perm,
+                      const int64_t* offsets, int64_t max_list, int32_t nprobe,
+                      const float* thresholds, const int32_t* k_values, int32_t J,
+                      int64_t* idx_out, float* sim_out, int32_t* k_out, int32_t* probed_out,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ *
  * Match predictor (Sec. 5.2, Sec. 6: a one-class SVM over the cached prompt
  * embeddings decides whether a close match is likely; if not, the request
  * skips the cache and is generated from scratch, Alg. 1).

@@ -135,6 +135,58 @@ def nv_cache_move_rows(cache, n, payload, src, dst):
     N.check(st, "nv_cache_move_rows")
 
 
+class NvIVF:
+    """IVF index over a device cache (f32, or bf16 as torch.bfloat16 / int16 bits):
+    centroids, row lists and the rows in list order, built on the device."""
+
+    def __init__(self, cache, init, iters=0):
+        _need_cuda(cache)
+        assert cache.is_contiguous() and cache.dim() == 2
+        n, d = cache.shape
+        self.dtype = N.NV_F32 if cache.dtype == torch.float32 else N.NV_BF16
+        if self.dtype == N.NV_BF16 and cache.dtype not in BF16_DTYPES:
+            raise ValueError("cache must be float32 or bfloat16 (bits)")
+        init = np.ascontiguousarray(init, dtype=np.int64)
+        L = len(init)
+        dev = cache.device
+        self.n, self.d, self.L = n, d, L
+        self.cents = torch.empty((L, d), dtype=cache.dtype, device=dev)
+        self.lists = torch.empty(n, dtype=torch.int64, device=dev)
+        self.perm = torch.empty(n, dtype=torch.int64, device=dev)
+        self.offsets = torch.empty(L + 1, dtype=torch.int64, device=dev)
+        self.rows = torch.empty_like(cache)
+        need = int(N.lib.nv_ivf_build_workspace(n, d, L))
+        own, addr = workspace(need, dev)
+        mx = C.c_int64()
+        st = N.lib.nv_ivf_build(_p(cache), self.dtype, n, d, init.ctypes.data, L, int(iters),
+                                _p(self.cents), _p(self.lists), _p(self.perm), _p(self.offsets),
+                                _p(self.rows), C.byref(mx), C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_ivf_build")
+        del own
+        self.max_list = mx.value
+
+    def search(self, queries, nprobe, thresholds, k_values, probed=False):
+        """(idx int64, sim f32, K int32[, probed lists int32 [m][nprobe]]) on device."""
+        _need_cuda(queries)
+        assert queries.dtype == torch.float32 and queries.is_contiguous()
+        m = queries.shape[0]
+        dev = queries.device
+        idx = torch.empty(m, dtype=torch.int64, device=dev)
+        sim = torch.empty(m, dtype=torch.float32, device=dev)
+        kk = torch.empty(m, dtype=torch.int32, device=dev)
+        pr = torch.empty((m, nprobe), dtype=torch.int32, device=dev) if probed else None
+        thr = (C.c_float * len(thresholds))(*thresholds)
+        kv = (C.c_int32 * len(k_values))(*k_values)
+        need = int(N.lib.nv_ivf_search_workspace(m, self.L, nprobe, self.max_list))
+        own, addr = workspace(need, dev)
+        st = N.lib.nv_ivf_search(_p(queries), m, self.d, _p(self.cents), self.L, _p(self.rows),
+                                 self.dtype, _p(self.perm), _p(self.offsets), self.max_list,
+                                 int(nprobe), thr, kv, len(thresholds), _p(idx), _p(sim), _p(kk),
+                                 _p(pr), C.c_void_p(addr), need, _stream())
+        N.check(st, "nv_ivf_search")
+        return (idx, sim, kk, pr) if probed else (idx, sim, kk)
+
+
 def nv_ocsvm_train(rows, nu, order, eta0=1.0):
     """Train the match predictor on host rows (numpy float32, or uint16 bfloat16 bits
     [n][d]) in the visiting order (host int64 [T]).  Returns (w float64 [d], rho)."""

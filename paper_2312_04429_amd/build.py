@@ -13,7 +13,7 @@ SRC = os.environ.get("NV_BUILD_SRC") or os.path.join(HERE, "csrc")
 OUT_DIR = os.environ.get("NV_BUILD_DIR") or os.path.join(HERE, "_build")
 LIB = os.environ.get("NV_BUILD_OUT") or os.path.join(HERE, "libnv.so")
 SOURCES = ["lookup.hip", "gemm.hip", "attention.hip", "ops.hip", "unet.hip", "trace.hip",
-           "probe.hip", "pool.hip", "lcbfu.cpp", "predictor.hip"]
+           "probe.hip", "pool.hip", "lcbfu.cpp", "predictor.hip", "ivf.hip"]
 ARCH = os.environ.get("NV_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -27,11 +27,12 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # per score).  probe.hip: the same form, which is what reaches the matrix
 # cores' rate in a pure multiply loop (about 2.2 PFLOP/s against 1.2 with
 # accumulators in AGPRs).
-# predictor.hip: no multiply-add contraction, so its float64 sums round
-# exactly as written.
+# predictor.hip, ivf.hip: no multiply-add contraction, so their float64 sums
+# round exactly as written.
 EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
          "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-         "predictor.hip": ["-ffp-contract=off"]}
+         "predictor.hip": ["-ffp-contract=off"],
+         "ivf.hip": ["-ffp-contract=off"]}
 
 
 def _compile(src):

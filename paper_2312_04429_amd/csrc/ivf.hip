@@ -1,0 +1,504 @@
+// Inverted-file (IVF) approximate search over the cached prompt embeddings:
+// the indexed vector-DB search the paper's system runs (Sec. 5.3, Sec. 6),
+// built and searched on the GPU.  The rows are partitioned into L lists
+// around unit centroids; a query ranks the lists by its score against their
+// centroids and scans the rows of the best nprobe.
+//
+// Every score is the canonical one of the exact lookup (float64 sum of exact
+// products, left to right), every order is total (ties to the lower list /
+// row), and the centroid update sums in a fixed order, so an index and each
+// search result are reproducible bit for bit.
+//   build:  centroids = rows at caller-drawn indices; `iters` Lloyd steps
+//           (assign every row with the exact lookup, then the normalised float64
+//           mean of each non-empty list, rows in ascending order, rounded to
+//           float32 and on to the cache type); a final assignment; the rows
+//           sorted by list (stable radix sort: ascending rows within a list),
+//           list offsets, and a copy of the rows in list order, so a probe
+//           reads one contiguous block.
+//   search: centroid scores per (query, list); the best nprobe lists per query
+//           (repeated arg-max in one workgroup); every probed row rescored
+//           canonically by one thread; per-(query, probe, chunk) best rows
+//           merged in a final pass; float32 similarity and the selector's K.
+#include <hipcub/hipcub.hpp>
+
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
+#include "common.h"
+
+using namespace nv;
+
+namespace nv {
+namespace {
+constexpr int ASSIGN_BATCH = 1024;  // rows per exact-lookup call in the assignment
+
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ inline uint16_t f32_to_bf16_rne_i(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// canonical float64 score of a float32 query against one stored row
+__device__ inline double canon_dot(const float* __restrict__ q, const void* __restrict__ row,
+                                   int bf, int d) {
+  double s = 0.0;
+  if (bf) {
+    const uint16_t* r = (const uint16_t*)row;
+    for (int k = 0; k < d; k += 8) {
+      const u32x4 v = *(const u32x4*)(r + k);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s += (double)q[k + 2 * e] * (double)__uint_as_float(v[e] << 16);
+        s += (double)q[k + 2 * e + 1] * (double)__uint_as_float(v[e] & 0xFFFF0000u);
+      }
+    }
+  } else {
+    const float* r = (const float*)row;
+    for (int k = 0; k < d; k += 4) {
+      const floatx4 v = *(const floatx4*)(r + k);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s += (double)q[k + e] * (double)v[e];
+    }
+  }
+  return s;
+}
+
+// (score, id) order: higher score first, lower id on ties
+__device__ inline bool better_pair(double s, int64_t i, double bs, int64_t bi) {
+  return s > bs || (s == bs && i < bi);
+}
+
+__global__ void __launch_bounds__(256) gather_rows_k(const void* __restrict__ src, int bf, int d,
+                                                     const int64_t* __restrict__ idx, int64_t cnt,
+                                                     void* __restrict__ dst) {
+  const int64_t words = (int64_t)d * (bf ? 2 : 4) / 4;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < cnt * words;
+       t += (int64_t)gridDim.x * 256) {
+    const int64_t r = t / words, w = t % words;
+    ((uint32_t*)dst)[r * words + w] = ((const uint32_t*)src)[idx[r] * words + w];
+  }
+}
+
+__global__ void __launch_bounds__(256) rows_to_f32_k(const void* __restrict__ src, int bf, int d,
+                                                     int64_t r0, int cnt, float* __restrict__ out) {
+  const int64_t total = (int64_t)cnt * d;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * 256) {
+    const int64_t e = r0 * d + t;
+    out[t] = bf ? bf16_to_f32(((const uint16_t*)src)[e]) : ((const float*)src)[e];
+  }
+}
+
+__global__ void iota_k(int64_t* v, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    v[i] = i;
+}
+
+// offsets[l] = first position of list l in the sorted keys (binary search)
+__global__ void offsets_k(const int64_t* __restrict__ keys, int64_t n, int L,
+                          int64_t* __restrict__ off) {
+  const int l = blockIdx.x * blockDim.x + threadIdx.x;
+  if (l > L) return;
+  int64_t lo = 0, hi = n;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (keys[mid] < l) lo = mid + 1; else hi = mid;
+  }
+  off[l] = lo;
+}
+
+// sums[l][k] = sum over the rows of list l, in ascending row order, of row[k] (float64)
+__global__ void __launch_bounds__(64) list_sums_k(const void* __restrict__ rows, int bf, int d,
+                                                  const int64_t* __restrict__ perm,
+                                                  const int64_t* __restrict__ off,
+                                                  double* __restrict__ sums) {
+  const int l = blockIdx.x;
+  const int k = blockIdx.y * 64 + threadIdx.x;
+  if (k >= d) return;
+  double s = 0.0;
+  for (int64_t j = off[l]; j < off[l + 1]; ++j) {
+    const int64_t r = perm[j];
+    s += bf ? (double)bf16_to_f32(((const uint16_t*)rows)[r * d + k])
+            : (double)((const float*)rows)[r * d + k];
+  }
+  sums[(int64_t)l * d + k] = s;
+}
+
+// centroid l = sums[l] / sqrt(left-to-right sum of squares), float32 then cache type
+__global__ void __launch_bounds__(256) list_normalise_k(const double* __restrict__ sums, int d,
+                                                        const int64_t* __restrict__ off, int bf,
+                                                        void* __restrict__ cents) {
+  __shared__ double nrm;
+  const int l = blockIdx.x;
+  if (off[l + 1] == off[l]) return;  // empty list keeps its centroid
+  const double* s = sums + (int64_t)l * d;
+  if (threadIdx.x == 0) {
+    double a = 0.0;
+    for (int k = 0; k < d; ++k) a = __dadd_rn(a, __dmul_rn(s[k], s[k]));
+    // the correctly rounded square root: of sqrt's result and its two neighbours,
+    // the one whose square is nearest a
+    const double r = sqrt(a);
+    double best = r, err = fabs(fma(r, r, -a));
+    const double cand[2] = {nextafter(r, 0.0), nextafter(r, INFINITY)};
+    for (int c = 0; c < 2; ++c) {
+      const double e = fabs(fma(cand[c], cand[c], -a));
+      if (e < err) {
+        best = cand[c];
+        err = e;
+      }
+    }
+    nrm = best;
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < d; k += 256) {
+    const float v = (float)(s[k] / nrm);
+    if (bf)
+      ((uint16_t*)cents)[(int64_t)l * d + k] = f32_to_bf16_rne_i(v);
+    else
+      ((float*)cents)[(int64_t)l * d + k] = v;
+  }
+}
+
+// cs[j][l]: canonical score of query j against centroid l (one thread each)
+__global__ void __launch_bounds__(256) cent_scores_k(const float* __restrict__ q, int m, int d,
+                                                     const void* __restrict__ cents, int bf,
+                                                     int L, double* __restrict__ cs) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)m * L) return;
+  const int j = (int)(t / L), l = (int)(t % L);
+  const char* row = (const char*)cents + (int64_t)l * d * (bf ? 2 : 4);
+  cs[t] = canon_dot(q + (int64_t)j * d, row, bf, d);
+}
+
+// the nprobe best lists of query j, in rank order
+__global__ void __launch_bounds__(256) top_lists_k(const double* __restrict__ cs, int L,
+                                                   int nprobe, int32_t* __restrict__ probed) {
+  __shared__ double rs[256];
+  __shared__ int ri[256];
+  __shared__ unsigned char taken[8192];
+  const int j = blockIdx.x, t = threadIdx.x;
+  const double* c = cs + (int64_t)j * L;
+  for (int l = t; l < L; l += 256) taken[l] = 0;
+  __syncthreads();
+  for (int p = 0; p < nprobe; ++p) {
+    double bs = -INFINITY;
+    int bi = -1;
+    for (int l = t; l < L; l += 256)
+      if (!taken[l] && (bi < 0 || c[l] > bs)) {  // ascending l: strict '>' keeps the lower
+        bs = c[l];
+        bi = l;
+      }
+    rs[t] = bs;
+    ri[t] = bi;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (t < w) {
+        const int oi = ri[t + w];
+        if (oi >= 0 && (ri[t] < 0 || better_pair(rs[t + w], oi, rs[t], ri[t]))) {
+          rs[t] = rs[t + w];
+          ri[t] = oi;
+        }
+      }
+      __syncthreads();
+    }
+    if (t == 0) {
+      probed[(int64_t)j * nprobe + p] = ri[0];
+      taken[ri[0]] = 1;
+    }
+    __syncthreads();
+  }
+}
+
+// best probed row per (query, probe, chunk of 256 list positions)
+__global__ void __launch_bounds__(256) probe_scan_k(const float* __restrict__ q, int d,
+                                                    const void* __restrict__ lrows, int bf,
+                                                    const int64_t* __restrict__ perm,
+                                                    const int64_t* __restrict__ off,
+                                                    const int32_t* __restrict__ probed,
+                                                    int nprobe, int chunks,
+                                                    double* __restrict__ ps,
+                                                    int64_t* __restrict__ pi) {
+  __shared__ double rs[256];
+  __shared__ int64_t ri[256];
+  const int jp = blockIdx.x, ch = blockIdx.y, t = threadIdx.x;
+  const int j = jp / nprobe;
+  const int l = probed[jp];
+  const int64_t pos = off[l] + (int64_t)ch * 256 + t;
+  double bs = -INFINITY;
+  int64_t bi = -1;
+  if (off[l] + (int64_t)ch * 256 < off[l + 1] && pos < off[l + 1]) {
+    bs = canon_dot(q + (int64_t)j * d, (const char*)lrows + pos * d * (bf ? 2 : 4), bf, d);
+    bi = perm[pos];
+  }
+  rs[t] = bs;
+  ri[t] = bi;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w && ri[t + w] >= 0 && (ri[t] < 0 || better_pair(rs[t + w], ri[t + w], rs[t], ri[t]))) {
+      rs[t] = rs[t + w];
+      ri[t] = ri[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    ps[(int64_t)jp * chunks + ch] = rs[0];
+    pi[(int64_t)jp * chunks + ch] = ri[0];
+  }
+}
+
+struct Sel {
+  float t[16];
+  int32_t k[16];
+  int J;
+};
+
+__global__ void __launch_bounds__(256) probe_final_k(const double* __restrict__ ps,
+                                                     const int64_t* __restrict__ pi, int per_q,
+                                                     Sel sel, int64_t* __restrict__ idx,
+                                                     float* __restrict__ sim,
+                                                     int32_t* __restrict__ kk) {
+  __shared__ double rs[256];
+  __shared__ int64_t ri[256];
+  const int j = blockIdx.x, t = threadIdx.x;
+  double bs = -INFINITY;
+  int64_t bi = -1;
+  for (int c = t; c < per_q; c += 256) {
+    const int64_t i = pi[(int64_t)j * per_q + c];
+    const double s = ps[(int64_t)j * per_q + c];
+    if (i >= 0 && (bi < 0 || better_pair(s, i, bs, bi))) {
+      bs = s;
+      bi = i;
+    }
+  }
+  rs[t] = bs;
+  ri[t] = bi;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w && ri[t + w] >= 0 && (ri[t] < 0 || better_pair(rs[t + w], ri[t + w], rs[t], ri[t]))) {
+      rs[t] = rs[t + w];
+      ri[t] = ri[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    const int64_t b = ri[0];
+    const float s = b >= 0 ? (float)rs[0] : -INFINITY;
+    int32_t k = 0;
+    if (b >= 0)
+      for (int a = 0; a < sel.J; ++a)
+        if (s > sel.t[a]) {
+          k = sel.k[a];
+          break;
+        }
+    idx[j] = b;
+    sim[j] = s;
+    kk[j] = k;
+  }
+}
+
+inline int bits_for(int L) {
+  int b = 1;
+  while ((1 << b) < L) ++b;
+  return b;
+}
+
+struct BuildWs {
+  size_t qf, lk, idx_tmp, sim_tmp, k_tmp, keys, keys_sorted, vals, sums, sort_tmp, total;
+  size_t sort_bytes, lk_bytes;
+};
+
+inline BuildWs plan_build(int64_t n, int d, int L) {
+  BuildWs w{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  w.lk_bytes = nv_cache_lookup_workspace(ASSIGN_BATCH, L, d);
+  size_t sb = 0;
+  hipcub::DeviceRadixSort::SortPairs(nullptr, sb, (const int64_t*)nullptr, (int64_t*)nullptr,
+                                     (const int64_t*)nullptr, (int64_t*)nullptr, (int)n, 0,
+                                     bits_for(L));
+  w.sort_bytes = sb;
+  w.qf = take((size_t)ASSIGN_BATCH * d * 4);
+  w.lk = take(w.lk_bytes);
+  w.idx_tmp = take((size_t)ASSIGN_BATCH * 8);
+  w.sim_tmp = take((size_t)ASSIGN_BATCH * 4);
+  w.k_tmp = take((size_t)ASSIGN_BATCH * 4);
+  w.keys = take((size_t)n * 8);
+  w.keys_sorted = take((size_t)n * 8);
+  w.vals = take((size_t)n * 8);
+  w.sums = take((size_t)L * d * 8);
+  w.sort_tmp = take(sb);
+  w.total = o;
+  return w;
+}
+
+}  // namespace
+}  // namespace nv
+
+extern "C" size_t nv_ivf_build_workspace(int64_t n, int32_t d, int32_t L) {
+  if (n < 1 || d < 1 || L < 1) return 0;
+  return plan_build(n, d, L).total;
+}
+
+extern "C" int32_t nv_ivf_build(const void* cache, int32_t c_dtype, int64_t n, int32_t d,
+                                const int64_t* init, int32_t L, int32_t iters, void* cents,
+                                int64_t* lists, int64_t* perm, int64_t* offsets, void* ivf_rows,
+                                int64_t* max_list, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  clear_error();
+  NV_CHECK_ARG(cache && init && cents && lists && perm && offsets && ivf_rows && max_list,
+               "null argument");
+  NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
+  NV_CHECK_ARG(n >= 1 && n < (int64_t(1) << 31), "n must be in [1, 2^31)");
+  NV_CHECK_ARG(L >= 1 && L <= 8192 && L <= n, "L must be in [1, min(n, 8192)]");
+  NV_CHECK_ARG(iters >= 0 && iters <= 100, "iters must be in [0, 100]");
+  if (d % 8 != 0 || d < 8 || d > 2048) {
+    set_error("d must be a multiple of 8 in [8, 2048]");
+    return NV_ERR_UNSUPPORTED;
+  }
+  const BuildWs w = plan_build(n, d, L);
+  if (!workspace || workspace_bytes < w.total || ((uintptr_t)workspace & 255)) {
+    set_error("ivf build workspace missing, misaligned or smaller than nv_ivf_build_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  for (int l = 0; l < L; ++l) NV_CHECK_ARG(init[l] >= 0 && init[l] < n, "init out of range");
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const int bf = c_dtype == NV_BF16;
+  int64_t* keys_sorted = (int64_t*)(ws + w.keys_sorted);
+  int64_t* vals = (int64_t*)(ws + w.vals);
+  // initial centroids: the rows at init (host indices staged through the key buffer)
+  NV_HIP_TRY(hipMemcpyAsync(keys_sorted, init, (size_t)L * 8, hipMemcpyHostToDevice, s));
+  hipLaunchKernelGGL(gather_rows_k, dim3((unsigned)std::min<int64_t>(ceil_div((int64_t)L * d, 256), 4096)),
+                     dim3(256), 0, s, cache, bf, d, (const int64_t*)keys_sorted, (int64_t)L, cents);
+  NV_LAUNCH_CHECK("gather_rows_k");
+  const float thr_none[1] = {1e30f};
+  const int32_t k_none[1] = {0};
+  auto assign = [&]() -> int32_t {
+    for (int64_t r0 = 0; r0 < n; r0 += ASSIGN_BATCH) {
+      const int cnt = (int)std::min<int64_t>(ASSIGN_BATCH, n - r0);
+      hipLaunchKernelGGL(rows_to_f32_k, dim3((unsigned)std::min<int64_t>(ceil_div((int64_t)cnt * d, 256), 2048)),
+                         dim3(256), 0, s, cache, bf, d, r0, cnt, (float*)(ws + w.qf));
+      NV_LAUNCH_CHECK("rows_to_f32_k");
+      const int32_t st = nv_cache_lookup((const float*)(ws + w.qf), cnt, cents, c_dtype, L, d,
+                                         thr_none, k_none, 1, lists + r0,
+                                         (float*)(ws + w.sim_tmp), (int32_t*)(ws + w.k_tmp),
+                                         ws + w.lk, w.lk_bytes, stream);
+      if (st != NV_OK) return st;
+    }
+    return NV_OK;
+  };
+  auto sort_lists = [&]() -> int32_t {
+    hipLaunchKernelGGL(iota_k, dim3((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)), dim3(256),
+                       0, s, vals, n);
+    NV_LAUNCH_CHECK("iota_k");
+    size_t sb = w.sort_bytes;
+    NV_HIP_TRY(hipcub::DeviceRadixSort::SortPairs(ws + w.sort_tmp, sb, (const int64_t*)lists,
+                                                  keys_sorted, (const int64_t*)vals, perm, (int)n,
+                                                  0, bits_for(L), s));
+    hipLaunchKernelGGL(offsets_k, dim3((unsigned)ceil_div(L + 1, 256)), dim3(256), 0, s,
+                       (const int64_t*)keys_sorted, n, L, offsets);
+    NV_LAUNCH_CHECK("offsets_k");
+    return NV_OK;
+  };
+  for (int it = 0; it < iters; ++it) {
+    int32_t st = assign();
+    if (st != NV_OK) return st;
+    st = sort_lists();
+    if (st != NV_OK) return st;
+    hipLaunchKernelGGL(list_sums_k, dim3((unsigned)L, (unsigned)ceil_div(d, 64)), dim3(64), 0, s,
+                       cache, bf, d, (const int64_t*)perm, (const int64_t*)offsets,
+                       (double*)(ws + w.sums));
+    NV_LAUNCH_CHECK("list_sums_k");
+    hipLaunchKernelGGL(list_normalise_k, dim3((unsigned)L), dim3(256), 0, s,
+                       (const double*)(ws + w.sums), d, (const int64_t*)offsets, bf, cents);
+    NV_LAUNCH_CHECK("list_normalise_k");
+  }
+  int32_t st = assign();
+  if (st != NV_OK) return st;
+  st = sort_lists();
+  if (st != NV_OK) return st;
+  hipLaunchKernelGGL(gather_rows_k, dim3(4096), dim3(256), 0, s, cache, bf, d,
+                     (const int64_t*)perm, n, ivf_rows);
+  NV_LAUNCH_CHECK("gather_rows_k");
+  std::vector<int64_t> off(L + 1);
+  NV_HIP_TRY(hipMemcpyAsync(off.data(), offsets, (size_t)(L + 1) * 8, hipMemcpyDeviceToHost, s));
+  NV_HIP_TRY(hipStreamSynchronize(s));
+  int64_t mx = 0;
+  for (int l = 0; l < L; ++l) mx = std::max(mx, off[l + 1] - off[l]);
+  *max_list = mx;
+  return NV_OK;
+}
+
+extern "C" size_t nv_ivf_search_workspace(int32_t m, int32_t L, int32_t nprobe, int64_t max_list) {
+  if (m < 1 || L < 1 || nprobe < 1 || max_list < 0) return 0;
+  const int64_t chunks = std::max<int64_t>(1, ceil_div(max_list, 256));
+  return align_up((size_t)m * L * 8, 256) + align_up((size_t)m * nprobe * 4, 256) +
+         2 * align_up((size_t)m * nprobe * chunks * 8, 256);
+}
+
+extern "C" int32_t nv_ivf_search(const float* queries, int32_t m, int32_t d, const void* cents,
+                                 int32_t L, const void* ivf_rows, int32_t c_dtype,
+                                 const int64_t* perm, const int64_t* offsets, int64_t max_list,
+                                 int32_t nprobe, const float* thresholds, const int32_t* k_values,
+                                 int32_t J, int64_t* idx_out, float* sim_out, int32_t* k_out,
+                                 int32_t* probed_out, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  clear_error();
+  NV_CHECK_ARG(queries && cents && ivf_rows && perm && offsets && idx_out && sim_out && k_out,
+               "null argument");
+  NV_CHECK_ARG(m >= 1 && m <= 4096, "m must be in [1, 4096]");
+  NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
+  NV_CHECK_ARG(L >= 1 && L <= 8192, "L must be in [1, 8192]");
+  NV_CHECK_ARG(nprobe >= 1 && nprobe <= L && nprobe <= 256, "nprobe must be in [1, min(L, 256)]");
+  NV_CHECK_ARG(max_list >= 0 && max_list < (int64_t(1) << 31), "bad max_list");
+  NV_CHECK_ARG(thresholds && k_values && J >= 1 && J <= 16, "need 1..16 thresholds");
+  if (d % 8 != 0 || d < 8 || d > 2048) {
+    set_error("d must be a multiple of 8 in [8, 2048]");
+    return NV_ERR_UNSUPPORTED;
+  }
+  Sel sel{};
+  sel.J = J;
+  for (int a = 0; a < J; ++a) {
+    NV_CHECK_ARG(std::isfinite(thresholds[a]), "thresholds must be finite");
+    NV_CHECK_ARG(a == 0 || thresholds[a] < thresholds[a - 1], "thresholds must descend");
+    NV_CHECK_ARG(k_values[a] >= 0, "k_values must be >= 0");
+    sel.t[a] = thresholds[a];
+    sel.k[a] = k_values[a];
+  }
+  const size_t need = nv_ivf_search_workspace(m, L, nprobe, max_list);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255)) {
+    set_error("ivf search workspace missing, misaligned or too small");
+    return NV_ERR_WORKSPACE;
+  }
+  const int chunks = (int)std::max<int64_t>(1, ceil_div(max_list, 256));
+  NV_CHECK_ARG((int64_t)m * nprobe <= 65535 * 64 && chunks <= 65535, "search too large");
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  double* cs = (double*)ws;
+  int32_t* probed = probed_out ? probed_out
+                               : (int32_t*)(ws + align_up((size_t)m * L * 8, 256));
+  char* after = ws + align_up((size_t)m * L * 8, 256) + align_up((size_t)m * nprobe * 4, 256);
+  double* ps = (double*)after;
+  int64_t* pi = (int64_t*)(after + align_up((size_t)m * nprobe * chunks * 8, 256));
+  const int bf = c_dtype == NV_BF16;
+  hipLaunchKernelGGL(cent_scores_k, dim3((unsigned)ceil_div((int64_t)m * L, 256)), dim3(256), 0, s,
+                     queries, m, d, cents, bf, L, cs);
+  NV_LAUNCH_CHECK("cent_scores_k");
+  hipLaunchKernelGGL(top_lists_k, dim3((unsigned)m), dim3(256), 0, s, (const double*)cs, L, nprobe,
+                     probed);
+  NV_LAUNCH_CHECK("top_lists_k");
+  hipLaunchKernelGGL(probe_scan_k, dim3((unsigned)(m * nprobe), (unsigned)chunks), dim3(256), 0, s,
+                     queries, d, ivf_rows, bf, perm, offsets, (const int32_t*)probed, nprobe,
+                     chunks, ps, pi);
+  NV_LAUNCH_CHECK("probe_scan_k");
+  hipLaunchKernelGGL(probe_final_k, dim3((unsigned)m), dim3(256), 0, s, (const double*)ps,
+                     (const int64_t*)pi, nprobe * chunks, sel, idx_out, sim_out, k_out);
+  NV_LAUNCH_CHECK("probe_final_k");
+  return NV_OK;
+}
