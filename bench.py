@@ -47,6 +47,10 @@ def parse():
     ap.add_argument("--scan-only", action="store_true",
                     help="time the lookup alone, warm (back to back) and cold (a 2 GiB write "
                          "between repetitions evicts the cache from the Infinity Cache)")
+    ap.add_argument("--ivf", default=None, metavar="L:NPROBE[:ITERS]",
+                    help="with --scan-only: also build an IVF index (L lists from seeded row "
+                         "samples, ITERS Lloyd steps) and time its search at NPROBE probes, "
+                         "with recall against the exact lookup")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the event tracing of kernel launches (for counter passes)")
@@ -700,7 +704,67 @@ def scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
     pk = P.nv_probe_peaks(dev)
     out["hbm_read_gbps_measured"] = pk["hbm_read_gbps"]
     out["hbm_frac_scan_kernel_of_measured"] = kby / (kms * 1e-3) / 1e9 / pk["hbm_read_gbps"]
+    if args.ivf:
+        out["ivf"] = ivf_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m)
     print(json.dumps(out))
+
+
+def ivf_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
+    """Build an IVF index over the same cache and time its search beside the exact
+    lookup: warm time per batch of queries, recall@1 (same row as the exact lookup)
+    and K agreement."""
+    parts = [int(v) for v in args.ivf.split(":")]
+    L, nprobe = parts[0], parts[1]
+    iters = parts[2] if len(parts) > 2 else 0
+    n = d_cache.shape[0]
+    init = np.random.default_rng(wl["cache_seed"] + 7).choice(n, L, replace=False)
+    print(f"[bench] ivf build L={L} iters={iters}", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    index = P.NvIVF(d_cache, init, iters)
+    torch.cuda.synchronize()
+    build_s = time.perf_counter() - t0
+    ei, es, ek = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
+    for _ in range(max(args.warmup, 1)):
+        gi, gs, gk = index.search(d_q, nprobe, thr, kv)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        gi, gs, gk = index.search(d_q, nprobe, thr, kv)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    # one query alone (the batch-1 serving case), IVF and exact
+    q1 = d_q[:1]
+    for _ in range(3):
+        index.search(q1, nprobe, thr, kv)
+        P.nv_cache_lookup(q1, d_cache, thr, kv, ws=lws)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        index.search(q1, nprobe, thr, kv)
+    e1.record()
+    torch.cuda.synchronize()
+    ms1 = e0.elapsed_time(e1) / args.steps
+    e0.record()
+    for _ in range(args.steps):
+        P.nv_cache_lookup(q1, d_cache, thr, kv, ws=lws)
+    e1.record()
+    torch.cuda.synchronize()
+    ex1 = e0.elapsed_time(e1) / args.steps
+    same = (gi == ei).cpu().numpy()
+    ek_h, gk_h = ek.cpu().numpy(), gk.cpu().numpy()
+    hits = ek_h > 0
+    sizes = np.diff(index.offsets.cpu().numpy())
+    return {"L": L, "nprobe": nprobe, "lloyd_steps": iters, "build_s": build_s,
+            "search_ms_warm": ms, "queries": int(m),
+            "search_ms_warm_1_query": ms1, "exact_lookup_ms_warm_1_query": ex1,
+            "recall_at_1": float(same.mean()),
+            "recall_at_1_on_exact_hits": float(same[hits].mean()) if hits.any() else None,
+            "k_agreement": float((ek_h == gk_h).mean()),
+            "list_sizes": {"min": int(sizes.min()), "median": int(np.median(sizes)),
+                           "max": int(sizes.max())}}
 
 
 if __name__ == "__main__":

@@ -201,7 +201,7 @@ int32_t nv_lcbfu_export(const nv_lcbfu* h, int32_t* table, int32_t* rows, int64_
  * reproducible bit for bit.
  *
  * nv_ivf_build: cache device [n][d] of c_dtype (d a multiple of 8, <= 2048);
- * init HOST int64 [L] (1 <= L <= min(n, 8192)): the rows that start the
+ * init HOST int64 [L] (1 <= L <= min(n, 4096)): the rows that start the
  * centroids.  iters Lloyd steps (0..100) each assign every row to its best
  * centroid (lower list on ties) and replace each non-empty list's centroid
  * by its normalised mean: the float64 sum of its rows in ascending row

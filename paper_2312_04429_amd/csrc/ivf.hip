@@ -16,9 +16,10 @@
 //           list offsets, and a copy of the rows in list order, so a probe
 //           reads one contiguous block.
 //   search: centroid scores per (query, list); the best nprobe lists per query
-//           (repeated arg-max in one workgroup); every probed row rescored
-//           canonically by one thread; per-(query, probe, chunk) best rows
-//           merged in a final pass; float32 similarity and the selector's K.
+//           (a bitonic sort in one workgroup); every probed row rescored
+//           canonically (rows staged through LDS with coalesced loads, one
+//           thread per row); per-(query, probe, chunk) best rows merged in a
+//           final pass; float32 similarity and the selector's K.
 #include <hipcub/hipcub.hpp>
 
 #include <algorithm>
@@ -38,31 +39,6 @@ __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32
 __device__ inline uint16_t f32_to_bf16_rne_i(float f) {
   const uint32_t u = __float_as_uint(f);
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
-// canonical float64 score of a float32 query against one stored row
-__device__ inline double canon_dot(const float* __restrict__ q, const void* __restrict__ row,
-                                   int bf, int d) {
-  double s = 0.0;
-  if (bf) {
-    const uint16_t* r = (const uint16_t*)row;
-    for (int k = 0; k < d; k += 8) {
-      const u32x4 v = *(const u32x4*)(r + k);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        s += (double)q[k + 2 * e] * (double)__uint_as_float(v[e] << 16);
-        s += (double)q[k + 2 * e + 1] * (double)__uint_as_float(v[e] & 0xFFFF0000u);
-      }
-    }
-  } else {
-    const float* r = (const float*)row;
-    for (int k = 0; k < d; k += 4) {
-      const floatx4 v = *(const floatx4*)(r + k);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) s += (double)q[k + e] * (double)v[e];
-    }
-  }
-  return s;
 }
 
 // (score, id) order: higher score first, lower id on ties
@@ -161,53 +137,172 @@ __global__ void __launch_bounds__(256) list_normalise_k(const double* __restrict
   }
 }
 
-// cs[j][l]: canonical score of query j against centroid l (one thread each)
-__global__ void __launch_bounds__(256) cent_scores_k(const float* __restrict__ q, int m, int d,
-                                                     const void* __restrict__ cents, int bf,
-                                                     int L, double* __restrict__ cs) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)m * L) return;
-  const int j = (int)(t / L), l = (int)(t % L);
-  const char* row = (const char*)cents + (int64_t)l * d * (bf ? 2 : 4);
-  cs[t] = canon_dot(q + (int64_t)j * d, row, bf, d);
+// Canonical scores of up to 256 consecutive stored rows against one float32
+// query, one row per thread.  The rows pass through LDS in slices of 32 words
+// (64 bf16 or 32 f32 values per row): every slice is read with coalesced
+// 16-byte loads, and each thread then adds its row's products in k order from
+// a conflict-free padded layout (row stride 33 words).
+constexpr int SLICE_W = 32;
+
+__device__ inline double canon_rows_block(const float* __restrict__ q, const char* __restrict__ rows,
+                                          int nrows, int bf, int d, uint32_t (*tile)[SLICE_W + 1],
+                                          float* qs) {
+  const int t = threadIdx.x;
+  const int row_words = d * (bf ? 2 : 4) / 4;
+  double s = 0.0;
+  for (int w0 = 0; w0 < row_words; w0 += SLICE_W) {
+    const int ws = min(SLICE_W, row_words - w0);       // words in this slice (multiple of 4)
+    for (int c = t; c < 256 * (SLICE_W / 4); c += 256) {
+      const int r = c / (SLICE_W / 4), part = c % (SLICE_W / 4);
+      if (r < nrows && part * 4 < ws) {
+        const u32x4 v = *(const u32x4*)((const uint32_t*)rows + (int64_t)r * row_words + w0 +
+                                         part * 4);
+        tile[r][part * 4] = v[0];
+        tile[r][part * 4 + 1] = v[1];
+        tile[r][part * 4 + 2] = v[2];
+        tile[r][part * 4 + 3] = v[3];
+      }
+    }
+    const int k0 = bf ? 2 * w0 : w0;
+    const int nk = bf ? 2 * ws : ws;
+    if (t < nk) qs[t] = q[k0 + t];
+    __syncthreads();
+    if (t < nrows) {
+      if (bf) {
+        for (int w = 0; w < ws; ++w) {
+          const uint32_t v = tile[t][w];
+          s += (double)qs[2 * w] * (double)__uint_as_float(v << 16);
+          s += (double)qs[2 * w + 1] * (double)__uint_as_float(v & 0xFFFF0000u);
+        }
+      } else {
+        for (int w = 0; w < ws; ++w) s += (double)qs[w] * (double)__uint_as_float(tile[t][w]);
+      }
+    }
+    __syncthreads();
+  }
+  return s;
 }
 
-// the nprobe best lists of query j, in rank order
+// cs[j][l]: canonical score of query j against centroid l (256 centroids per block)
+__global__ void __launch_bounds__(256) cent_scores_k(const float* __restrict__ q, int d,
+                                                     const void* __restrict__ cents, int bf,
+                                                     int L, double* __restrict__ cs) {
+  __shared__ uint32_t tile[256][SLICE_W + 1];
+  __shared__ float qs[2 * SLICE_W];
+  const int j = blockIdx.y, l0 = blockIdx.x * 256;
+  const int nrows = min(256, L - l0);
+  const double v = canon_rows_block(q + (int64_t)j * d,
+                                    (const char*)cents + (int64_t)l0 * d * (bf ? 2 : 4), nrows,
+                                    bf, d, tile, qs);
+  if ((int)threadIdx.x < nrows) cs[(int64_t)j * L + l0 + threadIdx.x] = v;
+}
+
+// the nprobe best lists of query j in rank order (higher score first, lower
+// list on ties).  Scores map to order-preserving 64-bit keys; a most-
+// significant-byte-first radix select finds the nprobe-th largest key K*
+// (eight 256-bin histograms in LDS); the lists above K*, and the lowest-
+// numbered lists equal to it (an index-order prefix count), are compacted and
+// each is placed at its rank among the selected.
+constexpr int TOP_MAX_L = 4096;
+constexpr int TOP_PER_T = TOP_MAX_L / 256;
+
+__device__ inline uint64_t order_key(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  return (u >> 63) ? ~u : (u | (uint64_t(1) << 63));
+}
+
+// exclusive prefix sum over the block of one value per thread (256 threads)
+__device__ inline int block_excl_scan(int v, int* sh) {
+  const int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {
+    const int a = t >= o ? sh[t - o] : 0;
+    __syncthreads();
+    sh[t] += a;
+    __syncthreads();
+  }
+  const int incl = sh[t];
+  __syncthreads();
+  return incl - v;
+}
+
 __global__ void __launch_bounds__(256) top_lists_k(const double* __restrict__ cs, int L,
                                                    int nprobe, int32_t* __restrict__ probed) {
-  __shared__ double rs[256];
-  __shared__ int ri[256];
-  __shared__ unsigned char taken[8192];
+  __shared__ int hist[256];
+  __shared__ int scan_sh[256];
+  __shared__ uint64_t sel_key[256];
+  __shared__ int sel_idx[256];
+  __shared__ uint64_t kstar_sh;
+  __shared__ int need_sh;
   const int j = blockIdx.x, t = threadIdx.x;
-  const double* c = cs + (int64_t)j * L;
-  for (int l = t; l < L; l += 256) taken[l] = 0;
-  __syncthreads();
-  for (int p = 0; p < nprobe; ++p) {
-    double bs = -INFINITY;
-    int bi = -1;
-    for (int l = t; l < L; l += 256)
-      if (!taken[l] && (bi < 0 || c[l] > bs)) {  // ascending l: strict '>' keeps the lower
-        bs = c[l];
-        bi = l;
-      }
-    rs[t] = bs;
-    ri[t] = bi;
+  // thread t owns lists t * TOP_PER_T .. (index order within and across threads)
+  uint64_t key[TOP_PER_T];
+#pragma unroll
+  for (int e = 0; e < TOP_PER_T; ++e) {
+    const int l = t * TOP_PER_T + e;
+    key[e] = l < L ? order_key(cs[(int64_t)j * L + l]) : 0;
+  }
+  uint64_t prefix = 0, mask = 0;
+  int need = nprobe;  // how many of the remaining candidates to take from the top
+  for (int byte = 7; byte >= 0; --byte) {
+    hist[t] = 0;
     __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if (t < w) {
-        const int oi = ri[t + w];
-        if (oi >= 0 && (ri[t] < 0 || better_pair(rs[t + w], oi, rs[t], ri[t]))) {
-          rs[t] = rs[t + w];
-          ri[t] = oi;
-        }
-      }
-      __syncthreads();
+#pragma unroll
+    for (int e = 0; e < TOP_PER_T; ++e) {
+      const int l = t * TOP_PER_T + e;
+      if (l < L && (key[e] & mask) == prefix)
+        atomicAdd(&hist[(key[e] >> (8 * byte)) & 255], 1);
     }
+    __syncthreads();
     if (t == 0) {
-      probed[(int64_t)j * nprobe + p] = ri[0];
-      taken[ri[0]] = 1;
+      int acc = 0, b = 255;
+      for (; b > 0; --b) {
+        if (acc + hist[b] >= need) break;
+        acc += hist[b];
+      }
+      need_sh = need - acc;
+      kstar_sh = prefix | ((uint64_t)b << (8 * byte));
     }
     __syncthreads();
+    need = need_sh;
+    prefix = kstar_sh;
+    mask |= (uint64_t)255 << (8 * byte);
+    __syncthreads();
+  }
+  const uint64_t kstar = prefix;  // the nprobe-th largest key; take `need` lists equal to it
+  int eq = 0;
+#pragma unroll
+  for (int e = 0; e < TOP_PER_T; ++e) {
+    const int l = t * TOP_PER_T + e;
+    eq += (l < L && key[e] == kstar);
+  }
+  int eq_before = block_excl_scan(eq, scan_sh);
+  int take = 0;
+#pragma unroll
+  for (int e = 0; e < TOP_PER_T; ++e) {
+    const int l = t * TOP_PER_T + e;
+    if (l < L && (key[e] > kstar || (key[e] == kstar && eq_before++ < need))) ++take;
+  }
+  int pos = block_excl_scan(take, scan_sh);
+  eq_before = block_excl_scan(eq, scan_sh);
+#pragma unroll
+  for (int e = 0; e < TOP_PER_T; ++e) {
+    const int l = t * TOP_PER_T + e;
+    if (l < L && (key[e] > kstar || (key[e] == kstar && eq_before++ < need))) {
+      sel_key[pos] = key[e];
+      sel_idx[pos] = l;
+      ++pos;
+    }
+  }
+  __syncthreads();
+  if (t < nprobe) {
+    const uint64_t k = sel_key[t];
+    const int l = sel_idx[t];
+    int rank = 0;
+    for (int o = 0; o < nprobe; ++o)
+      rank += sel_key[o] > k || (sel_key[o] == k && sel_idx[o] < l);
+    probed[(int64_t)j * nprobe + rank] = l;
   }
 }
 
@@ -220,17 +315,22 @@ __global__ void __launch_bounds__(256) probe_scan_k(const float* __restrict__ q,
                                                     int nprobe, int chunks,
                                                     double* __restrict__ ps,
                                                     int64_t* __restrict__ pi) {
+  __shared__ uint32_t tile[256][SLICE_W + 1];
+  __shared__ float qs[2 * SLICE_W];
   __shared__ double rs[256];
   __shared__ int64_t ri[256];
   const int jp = blockIdx.x, ch = blockIdx.y, t = threadIdx.x;
   const int j = jp / nprobe;
   const int l = probed[jp];
-  const int64_t pos = off[l] + (int64_t)ch * 256 + t;
+  const int64_t p0 = off[l] + (int64_t)ch * 256;
+  const int nrows = (int)max<int64_t>(0, min<int64_t>(256, off[l + 1] - p0));
   double bs = -INFINITY;
   int64_t bi = -1;
-  if (off[l] + (int64_t)ch * 256 < off[l + 1] && pos < off[l + 1]) {
-    bs = canon_dot(q + (int64_t)j * d, (const char*)lrows + pos * d * (bf ? 2 : 4), bf, d);
-    bi = perm[pos];
+  if (nrows > 0) {
+    bs = canon_rows_block(q + (int64_t)j * d, (const char*)lrows + p0 * d * (bf ? 2 : 4), nrows,
+                          bf, d, tile, qs);
+    if (t < nrows) bi = perm[p0 + t];
+    else bs = -INFINITY;
   }
   rs[t] = bs;
   ri[t] = bi;
@@ -355,7 +455,7 @@ extern "C" int32_t nv_ivf_build(const void* cache, int32_t c_dtype, int64_t n, i
                "null argument");
   NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
   NV_CHECK_ARG(n >= 1 && n < (int64_t(1) << 31), "n must be in [1, 2^31)");
-  NV_CHECK_ARG(L >= 1 && L <= 8192 && L <= n, "L must be in [1, min(n, 8192)]");
+  NV_CHECK_ARG(L >= 1 && L <= 4096 && L <= n, "L must be in [1, min(n, 4096)]");
   NV_CHECK_ARG(iters >= 0 && iters <= 100, "iters must be in [0, 100]");
   if (d % 8 != 0 || d < 8 || d > 2048) {
     set_error("d must be a multiple of 8 in [8, 2048]");
@@ -454,7 +554,7 @@ extern "C" int32_t nv_ivf_search(const float* queries, int32_t m, int32_t d, con
                "null argument");
   NV_CHECK_ARG(m >= 1 && m <= 4096, "m must be in [1, 4096]");
   NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
-  NV_CHECK_ARG(L >= 1 && L <= 8192, "L must be in [1, 8192]");
+  NV_CHECK_ARG(L >= 1 && L <= 4096, "L must be in [1, 4096]");
   NV_CHECK_ARG(nprobe >= 1 && nprobe <= L && nprobe <= 256, "nprobe must be in [1, min(L, 256)]");
   NV_CHECK_ARG(max_list >= 0 && max_list < (int64_t(1) << 31), "bad max_list");
   NV_CHECK_ARG(thresholds && k_values && J >= 1 && J <= 16, "need 1..16 thresholds");
@@ -487,8 +587,8 @@ extern "C" int32_t nv_ivf_search(const float* queries, int32_t m, int32_t d, con
   double* ps = (double*)after;
   int64_t* pi = (int64_t*)(after + align_up((size_t)m * nprobe * chunks * 8, 256));
   const int bf = c_dtype == NV_BF16;
-  hipLaunchKernelGGL(cent_scores_k, dim3((unsigned)ceil_div((int64_t)m * L, 256)), dim3(256), 0, s,
-                     queries, m, d, cents, bf, L, cs);
+  hipLaunchKernelGGL(cent_scores_k, dim3((unsigned)ceil_div(L, 256), (unsigned)m), dim3(256), 0, s,
+                     queries, d, cents, bf, L, cs);
   NV_LAUNCH_CHECK("cent_scores_k");
   hipLaunchKernelGGL(top_lists_k, dim3((unsigned)m), dim3(256), 0, s, (const double*)cs, L, nprobe,
                      probed);
