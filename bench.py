@@ -41,6 +41,9 @@ def parse():
                     help="the cache-miss path instead: queries far from every cached prompt, "
                          "full generation storing the states after each K of the table, and "
                          "insertion of the new embeddings into the cache")
+    ap.add_argument("--eta", type=float, default=None,
+                    help="run DDIM's stochastic update with this eta (noise per sample and grid "
+                         "step drawn once before timing), the seed-change variant")
     ap.add_argument("--predictor", action="store_true",
                     help="sd15_lcbfu: put the match predictor (linear one-class SVM trained on "
                          "the prefilled embeddings, nu = 0.001) in front of the lookup")
@@ -319,14 +322,24 @@ def main():
                                           entry=t(np.asarray(entries, dtype=np.int32)),
                                           payload=d_payload)
 
+        d_z = None
+        if args.eta is not None:  # standard normal draws per sample and grid step
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(99)
+            d_z = torch.randn((B, wl["N"]) + tuple(noise.shape[1:]), generator=gen, device=dev)
+
         def step():
             idx, sim, kk = P.nv_cache_lookup(d_q, d_cache, thr, kv, ws=lws)
             idx, kk = idx[:nf], kk[:nf]  # the queries that feed this batch
             P.nv_gather_states(d_store, slots, d_payload, wl["n_cache"], idx, kk, d_noise, out=x)
             k_host = kk.cpu().tolist()          # the one device -> host crossing per batch
             ks_seen.append(k_host)
-            net.nv_denoise(x, k_host, d_cond, d_unc, pooled=d_pooled, guidance=wl["guidance"],
-                           sched=sched)
+            if d_z is None:
+                net.nv_denoise(x, k_host, d_cond, d_unc, pooled=d_pooled,
+                               guidance=wl["guidance"], sched=sched)
+            else:
+                net.nv_denoise_eta(x, k_host, d_cond, d_unc, args.eta, d_z, pooled=d_pooled,
+                                   guidance=wl["guidance"], sched=sched)
         if args.miss:
             step = miss_step
     else:  # denoise-only workload (no cache in its recipe): a fixed skip count
@@ -370,6 +383,8 @@ def main():
     if args.miss:
         config["path"] = ("cache miss: lookup, full generation storing the states after "
                           "K = 5..25, insertion of the new embeddings")
+    if args.eta is not None:
+        config["sampler"] = f"DDIM eta={args.eta} (caller-drawn noise per sample and grid step)"
     out = {
         "metric": "images/sec and UNet steps/sec at skip K (SD1.5-shape, 1 GPU); % MFMA peak",
         "value": images / dt, "unit": "images/s", "n_gpus": 1, "steps": args.steps,
