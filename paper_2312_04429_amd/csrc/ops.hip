@@ -531,11 +531,147 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
 
 }  // namespace
 
+// GroupNorm for few (row, group) pairs (batch 1 gives 2 x 32): one workgroup
+// per pair would leave most of the chip idle and each workgroup bound by its
+// own outstanding memory requests.  Each pair's pixels are split into S
+// contiguous ranges instead, one workgroup each, over the same thread layout
+// as gn_group_k.  gn_part_k: per range, the mean and the sum of squared
+// deviations from it (two exact passes over registers).  gn_split_apply_k:
+// merges the S partials of its pair in range order (pairwise update, float64),
+// then normalises its range (+ affine, SiLU).
+template <int NV>
+__global__ void __launch_bounds__(GN1_T) gn_part_k(GnArgs a, int S) {
+  __shared__ float red[GN1_T / 64];
+  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
+  const int pair = blockIdx.x / S, sp = blockIdx.x % S;
+  const int row = pair / a.G, g = pair % a.G;
+  const int HWs = (a.HW + S - 1) / S;
+  const int lo = sp * HWs, hi = min(a.HW, lo + HWs);
+  float* out = a.part + (int64_t)blockIdx.x * 2;
+  if (hi <= lo) {
+    if (threadIdx.x == 0) out[0] = out[1] = 0.f;
+    return;
+  }
+  const int t = threadIdx.x;
+  const bool on = t < P * vpp;
+  const int v = on ? t % vpp : 0, p0 = lo + (on ? t / vpp : 0);
+  const int c = g * cg + 2 * v;
+  const bool first = c < a.C1;
+  const int ld = first ? a.C1 : a.C2;
+  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
+                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
+  uint32_t x[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = p0 + j * P;
+    x[j] = (on && p < hi) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
+  }
+  float s1 = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) s1 += h_lo(x[j]) + h_hi(x[j]);
+  const float n = (float)(hi - lo) * (float)cg;
+  const float mean = block_sum_1024(s1, red) / n;
+  float s2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    if (on && p0 + j * P < hi) {
+      const float d0 = h_lo(x[j]) - mean, d1 = h_hi(x[j]) - mean;
+      s2 += d0 * d0 + d1 * d1;
+    }
+  }
+  const float m2 = block_sum_1024(s2, red);
+  if (t == 0) {
+    out[0] = mean;
+    out[1] = m2;
+  }
+}
+
+template <int NV>
+__global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
+  __shared__ float st[2];
+  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
+  const int pair = blockIdx.x / S, sp = blockIdx.x % S;
+  const int row = pair / a.G, g = pair % a.G;
+  const int HWs = (a.HW + S - 1) / S;
+  const int lo = sp * HWs, hi = min(a.HW, lo + HWs);
+  const int t = threadIdx.x;
+  const bool on = t < P * vpp && lo < hi;
+  const int v = on ? t % vpp : 0, p0 = lo + (on ? t / vpp : 0);
+  const int c = g * cg + 2 * v;
+  const bool first = c < a.C1;
+  const int ld = first ? a.C1 : a.C2;
+  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
+                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
+  uint32_t x[NV];  // issued first: their latency overlaps the merge below
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = p0 + j * P;
+    x[j] = (on && p < hi) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
+  }
+  if (t == 0) {
+    double n = 0.0, mean = 0.0, m2 = 0.0;
+    for (int q = 0; q < S; ++q) {
+      const int qlo = q * HWs, qhi = min(a.HW, qlo + HWs);
+      const float* pp = a.part + ((int64_t)pair * S + q) * 2;
+      chan_merge(n, mean, m2, (double)(max(0, qhi - qlo) * cg), (double)pp[0], (double)pp[1]);
+    }
+    st[0] = (float)mean;
+    st[1] = rsqrtf((float)(m2 / n) + a.eps);
+  }
+  __syncthreads();
+  if (!on) return;
+  const float mean = st[0], rstd = st[1];
+  const float k0 = rstd * a.gamma[c], k1 = rstd * a.gamma[c + 1];
+  const float f0 = a.beta[c] - mean * k0, f1 = a.beta[c + 1] - mean * k1;
+  _Float16* dst = a.out + (int64_t)row * a.HW * C + c;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = p0 + j * P;
+    if (p >= hi) continue;
+    float y0 = fmaf(h_lo(x[j]), k0, f0), y1 = fmaf(h_hi(x[j]), k1, f1);
+    if (a.silu) {
+      y0 = silu(y0);
+      y1 = silu(y1);
+    }
+    *(uint32_t*)(dst + (int64_t)p * C) =
+        (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y0) |
+        ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y1) << 16);
+  }
+}
+
+constexpr int GN_SPLIT_MAX = 8;
+constexpr int GN_SPLIT_TARGET = 256;  // pairs below which the split form is considered
+
 hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
   const int C = a.C1 + a.C2;
   if (a.G < 4 || a.G > 256 || (a.G & (a.G - 1)) || C % a.G || C % 8 || C > GN_MAXC)
     return hipErrorInvalidValue;
   const int cg = C / a.G;
+  const int pairs = rows * a.G;
+  // the split form pays a second launch: worth it only where one workgroup per pair
+  // would walk more than 16 pixel rounds (or not fit at all)
+  const bool long_pairs = cg % 2 == 0 && cg / 2 <= GN1_T &&
+                          ceil_div(a.HW, GN1_T / (cg / 2)) > 16;
+  if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / 2 <= GN1_T && pairs < GN_SPLIT_TARGET &&
+      a.part_chunks >= GN_SPLIT_MAX && long_pairs) {
+    const int S = std::min(GN_SPLIT_MAX, std::max(2, 2 * GN_SPLIT_TARGET / pairs));
+    const int P = GN1_T / (cg / 2);
+    const int nv = (int)ceil_div(ceil_div(a.HW, S), P);
+    if (nv <= GN1_NV) {
+      const dim3 grid((unsigned)(pairs * S)), blk(GN1_T);
+      if (nv <= 4) {
+        hipLaunchKernelGGL(gn_part_k<4>, grid, blk, 0, s, a, S);
+        hipLaunchKernelGGL(gn_split_apply_k<4>, grid, blk, 0, s, a, S);
+      } else if (nv <= 16) {
+        hipLaunchKernelGGL(gn_part_k<16>, grid, blk, 0, s, a, S);
+        hipLaunchKernelGGL(gn_split_apply_k<16>, grid, blk, 0, s, a, S);
+      } else {
+        hipLaunchKernelGGL(gn_part_k<GN1_NV>, grid, blk, 0, s, a, S);
+        hipLaunchKernelGGL(gn_split_apply_k<GN1_NV>, grid, blk, 0, s, a, S);
+      }
+      return hipGetLastError();
+    }
+  }
   if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / 2 <= GN1_T) {
     const int P = GN1_T / (cg / 2);                  // pixels per round
     const int nv = (int)ceil_div(a.HW, P);           // rounds
