@@ -22,12 +22,13 @@
 namespace nv {
 namespace {
 
-constexpr int QB = 2;    // 16-query column blocks per wave
 constexpr int KB = 64;   // keys per block
 constexpr int VROW = KB + 8;  // halfs per LDS V^T row
 constexpr float LOG2E = 1.4426950408889634f;
 
-template <int DH>
+// QB: 16-query column blocks per wave (2; 1 where the grid would otherwise
+// leave compute units idle, e.g. 1024 or 256 queries per head at batch 1)
+template <int DH, int QB>
 __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
@@ -266,13 +267,13 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
 }
 
-template <int DH>
-hipError_t launch(const AttnArgs& a, hipStream_t s) {
+template <int DH, int QB>
+hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   constexpr int KCH = DH / 8, KST = KCH % 2 ? KCH : KCH + 1, DV = (DH + 15) / 16 * 16;
   const size_t lds = (size_t)2 * (KB * KST * 8 + DV * VROW) * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -283,8 +284,17 @@ hipError_t launch(const AttnArgs& a, hipStream_t s) {
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
   const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes);
-  hipExtLaunchKernelGGL((attn_f16<DH>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u, a);
+  hipExtLaunchKernelGGL((attn_f16<DH, QB>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
+                        a);
   return hipGetLastError();
+}
+
+// Two query blocks per wave share every K / V tile between more queries; one
+// per wave doubles the workgroups where two would leave compute units idle.
+template <int DH>
+hipError_t launch(const AttnArgs& a, hipStream_t s) {
+  const int64_t wgs2 = ceil_div(a.S, 128) * a.heads * a.rows;
+  return wgs2 < 256 ? launch_qb<DH, 1>(a, s) : launch_qb<DH, 2>(a, s);
 }
 
 }  // namespace
