@@ -35,6 +35,31 @@ def test_linear(M, N, K):
     np.testing.assert_allclose(got, ref, rtol=2e-3, atol=2e-3 * np.abs(ref).max())
 
 
+def test_split_k_repeatable():
+    """Split-K products sum their float32 partial tiles in split order: repeated calls,
+    interleaved with other split products on the same scratch, give bit-identical outputs,
+    within tolerance of the oracle."""
+    import paper_2312_04429_amd as P
+    shapes = [(2, 1280, 1280), (128, 1280, 11520), (154, 640, 768), (512, 1280, 5120)]
+    t = lambda a: torch.from_numpy(a).cuda()
+    first = {}
+    for rep in range(3):
+        for M, N, K in shapes:
+            print(f"split-K linear rep={rep} M={M} N={N} K={K}", flush=True)
+            rng = np.random.default_rng(7 * M + N + K)
+            x = _h(rng.standard_normal((M, K)))
+            w = _h(rng.standard_normal((N, K)) * 0.05)
+            b = rng.standard_normal(N).astype(np.float32)
+            got = P.nv_op_linear(t(x), t(w), t(b)).cpu()
+            if rep == 0:
+                first[(M, N, K)] = got
+                ref = U.linear(x.astype(np.float32), w.astype(np.float32), b)
+                np.testing.assert_allclose(got.float().numpy(), ref, rtol=2e-3,
+                                           atol=2e-3 * np.abs(ref).max())
+            else:
+                assert torch.equal(got, first[(M, N, K)]), (rep, M, N, K)
+
+
 @pytest.mark.parametrize("B,H,W,Cin,Cout,stride,up", [
     (1, 5, 7, 8, 16, 1, 0), (2, 16, 16, 32, 64, 1, 0), (2, 64, 64, 320, 320, 1, 0),
     (2, 32, 32, 640, 640, 2, 0), (2, 8, 8, 1280, 1280, 1, 0), (2, 16, 16, 96, 32, 1, 1),
