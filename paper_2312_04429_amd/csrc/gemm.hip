@@ -742,7 +742,34 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
 }
 
 // Sum split-K partials in split order and apply the epilogue, four
-// consecutive columns per thread (N % 4 == 0, checked by the launcher).
+// consecutive columns per thread (N % 4 == 0, checked by the launcher).  The
+// loads of up to RED_CHUNK splits are issued together before their adds (a
+// loop of load-then-add would pay one memory round trip per split); the adds
+// still run in split order, so the sum does not change.
+constexpr int RED_CHUNK = 8;
+
+// NQ quads at p + k * off (k < NQ), each summed over the splits into v[k].
+template <int NQ>
+__device__ inline void sum_splits(const float* __restrict__ p, int off, int64_t MN, int splits,
+                                  float (&v)[NQ][4]) {
+  constexpr int CH = RED_CHUNK / NQ;
+  for (int s0 = 0; s0 < splits; s0 += CH) {
+    float4 q[CH][NQ];
+#pragma unroll
+    for (int u = 0; u < CH; ++u)
+#pragma unroll
+      for (int k = 0; k < NQ; ++k)
+        if (s0 + u < splits) q[u][k] = *(const float4*)(p + (s0 + u) * MN + k * off);
+#pragma unroll
+    for (int u = 0; u < CH; ++u)
+#pragma unroll
+      for (int k = 0; k < NQ; ++k)
+        if (s0 + u < splits) {
+          v[k][0] += q[u][k].x; v[k][1] += q[u][k].y; v[k][2] += q[u][k].z; v[k][3] += q[u][k].w;
+        }
+  }
+}
+
 __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
   const int64_t MN = g.M * (int64_t)g.N;
   const int nq = g.N / 4;
@@ -754,23 +781,15 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
       const int64_t m = e / per_row;
       const int rem = (int)(e - m * per_row);
       const int na = (rem >> 2) * 32 + (rem & 3) * 4;
-      float a[4] = {0.f, 0.f, 0.f, 0.f}, gt[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < splits; ++s) {
-        const float4 pa = *(const float4*)(g.partial + s * MN + m * g.N + na);
-        const float4 pg = *(const float4*)(g.partial + s * MN + m * g.N + na + 16);
-        a[0] += pa.x; a[1] += pa.y; a[2] += pa.z; a[3] += pa.w;
-        gt[0] += pg.x; gt[1] += pg.y; gt[2] += pg.z; gt[3] += pg.w;
-      }
-      store_geglu4(g, m, na, a, gt, g.vec_ok);
+      float ag[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};  // "a", gate
+      sum_splits<2>(g.partial + m * g.N + na, 16, MN, splits, ag);
+      store_geglu4(g, m, na, ag[0], ag[1], g.vec_ok);
     } else {
       const int64_t m = e / nq;
       const int n = (int)(e - m * nq) * 4;
-      float v[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < splits; ++s) {
-        const float4 p = *(const float4*)(g.partial + s * MN + m * g.N + n);
-        v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
-      }
-      store_out4(g, m, n, v, g.vec_ok);
+      float v[1][4] = {{0.f, 0.f, 0.f, 0.f}};
+      sum_splits<1>(g.partial + m * g.N + n, 0, MN, splits, v);
+      store_out4(g, m, n, v[0], g.vec_ok);
     }
   }
 }
