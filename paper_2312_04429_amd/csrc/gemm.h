@@ -40,6 +40,13 @@ struct GemmArgs {
   // split-K scratch (float32 partials), optional
   float* partial;
   size_t partial_bytes;
+  // LayerNorm of the A rows folded into the product (dense, one source, K % 64
+  // == 0, no split): w holds gamma[k] * W[n][k], bias holds beta . W[n] (+ the
+  // layer's bias), ln_c1[n] = sum_k w[n][k]; the kernel takes each row's mean
+  // and 1/sqrt(var + ln_eps) over its K values and forms
+  // rstd * (acc - mean * ln_c1[n]) before the epilogue.
+  const float* ln_c1;
+  float ln_eps;
   // filled by gemm_launch: byte extents of src1 / src2
   uint64_t bytes1, bytes2;
   int n_major;  // tile order: weight columns outermost (filled by gemm_launch)

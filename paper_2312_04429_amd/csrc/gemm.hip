@@ -538,7 +538,7 @@ __device__ __forceinline__ void mma_tile(const _Float16* __restrict__ a,
   }
 }
 
-template <int MODE, int BM, int BN, int STAGES>
+template <int MODE, int BM, int BN, int STAGES, bool LN>
 __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 16, FN = WN / 16;
@@ -674,14 +674,65 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   // per-wave count of loads in flight fixed for the waits below.
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s) issue(s);
+  // Folded LayerNorm: TPR threads per A row each sum CPT of the row's eight
+  // 16-byte chunks per k tile, shifted by the row's first value (k = 0, in
+  // chunk slot r & 7) so that the one-pass variance does not cancel: the
+  // shifted pair d (float16) enters sum d and sum d^2 through float32 dot2.
+  constexpr int TPR = 256 / BM, CPT = 8 / TPR;
+  const int st_row = tid / TPR, st_slot = (tid % TPR) * CPT;
+  half2v st_shift = {(_Float16)0.f, (_Float16)0.f};
+  const half2v st_one = {(_Float16)1.f, (_Float16)1.f};
+  float st_s1 = 0.f, st_s2 = 0.f;
   for (int kt = kt0; kt < kt1; ++kt) {
     wait_vmcnt<(STAGES - 2) * OPS>();  // this wave's loads of tile kt have landed
     ring_barrier();                    // everyone's have; buffer (kt - 1) is free
     issue((kt - kt0 + STAGES - 1) % STAGES);
     const _Float16* A = ring + ((kt - kt0) % STAGES) * TILE_H;
     mma_tile<FM, FN>(A, A + BM * 64, wm * WM, wn * WN, li, kc, acc);
+    if (LN) {
+      const _Float16* ar = A + st_row * 64;
+      if (kt == 0) st_shift = half2v{ar[(st_row & 7) * 8], ar[(st_row & 7) * 8]};
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) {
+        const half8 h = *(const half8*)(ar + (st_slot + c) * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const half2v d = half2v{h[2 * e], h[2 * e + 1]} - st_shift;
+          st_s1 = __builtin_amdgcn_fdot2(d, st_one, st_s1, false);
+          st_s2 = __builtin_amdgcn_fdot2(d, d, st_s2, false);
+        }
+      }
+    }
   }
   wait_vmcnt<0>();  // drain the requests past the last tile before the workgroup ends
+  if (LN) {
+    __shared__ float2 lnst[BM];  // (mean, 1 / sqrt(var + eps)) per tile row
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) {
+      st_s1 += __shfl_xor(st_s1, o, 64);
+      st_s2 += __shfl_xor(st_s2, o, 64);
+    }
+    if (tid % TPR == 0) {
+      const float inv_k = 1.0f / (float)g.K;
+      const float mu = st_s1 * inv_k;
+      const float var = fmaxf(st_s2 * inv_k - mu * mu, 0.f);
+      lnst[st_row] = make_float2((float)st_shift[0] + mu, rsqrtf(var + g.ln_eps));
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const float2 st = lnst[wm * WM + i * 16 + li];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int n = n0 + wn * WN + j * 16 + kc * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float c1 = n + r < g.N ? g.ln_c1[n + r] : 0.f;
+          acc[i][j][r] = st.y * (acc[i][j][r] - st.x * c1);
+        }
+      }
+    }
+  }
 
   // Operands are swapped in the multiply (weights as the row operand), so lane
   // (li, kc) of block (i, j) holds row m = ... + i * 16 + li and the four
@@ -826,12 +877,12 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int MODE, int BM, int BN, int STAGES>
-hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
+template <int MODE, int BM, int BN, int STAGES, bool LN>
+hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   const size_t lds = (size_t)STAGES * (BM + BN) * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES, LN>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -845,14 +896,22 @@ hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
   const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
   const TraceEv ev = trace_begin(fam, flops, bytes);
-  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES>), grid, dim3(256), (uint32_t)lds, s, ev.a,
-                        ev.b, 0u, g, kps);
+  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN>), grid, dim3(256), (uint32_t)lds, s,
+                        ev.a, ev.b, 0u, g, kps);
   if (splits > 1) {
     const int64_t total = g.M * (int64_t)(g.N / 4);
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
     hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
   }
   return hipGetLastError();
+}
+
+// A folded LayerNorm needs every k tile of a row in one workgroup: no split.
+template <int MODE, int BM, int BN, int STAGES>
+hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
+  if constexpr (MODE == 0)
+    if (g.ln_c1) return launch_s_t<0, BM, BN, STAGES, true>(g, 1, s);
+  return launch_s_t<MODE, BM, BN, STAGES, false>(g, splits, s);
 }
 
 // Streamed kernel when every 64-deep k tile lies inside one source and tap.
@@ -919,6 +978,7 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
 
 template <int MODE>
 hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
+  if (g.ln_c1 && (MODE != 0 || g.src2 || !streamable<MODE>(g))) return hipErrorInvalidValue;
   if (streamable<MODE>(g)) return dispatch_streamed<MODE>(g, s);
   // Larger tiles move fewer bytes per flop (64, 43 and 32 flop per byte of
   // L2 traffic for 128x128, 128x64, 64x64).  At these problem sizes a

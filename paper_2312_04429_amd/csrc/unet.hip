@@ -45,6 +45,17 @@ struct ParamInfo {
   }
 };
 
+// Transformer LayerNorms can be folded into the products that consume them
+// (self-attention q|k|v, cross-attention q, GEGLU) when the channel count is
+// whole 64-deep k tiles, as the streamed GEMM requires:
+//   LN(x) W^T = rstd * (x (gamma W)^T - mean * sum_k gamma_k W[n][k]) + beta W^T.
+// A call folds them when the LayerNorm's input is at most LN_FOLD_MAX_ELEMS
+// values (8192 tokens of 320 channels: batch-1 shapes, where the products are
+// latency-bound and the saved launch pays); on larger inputs the row
+// statistics' extra LDS reads cost more than the launch saves.
+inline bool ln_folded(int ch) { return ch % 64 == 0; }
+constexpr int64_t LN_FOLD_MAX_ELEMS = 8192 * 320;
+
 int heads_for(const nv_unet_config& c, int ch) {
   return c.n_heads > 0 ? c.n_heads : ch / c.head_dim;
 }
@@ -446,9 +457,28 @@ void emit_conv(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
 }
 
 // y[M][N] = x[M][K] W^T (+bias) (+residual) ; x may be a 2-source concat
+// A LayerNorm folded into the product that consumes it: used by a call whose
+// rows (R * HW) are at most max_rows, which then reads the LayerNorm's input.
+struct LnFold {
+  const _Float16* w = nullptr;  // gamma-scaled weights
+  const float* c1 = nullptr;    // row sums of w
+  const float* c2 = nullptr;    // beta . W (+ the layer's bias)
+  size_t x_off = 0;             // the LayerNorm's input
+  float eps = 0.f;
+  int64_t max_rows = -1;        // -1: never folded
+  bool on(int64_t rows) const { return rows <= max_rows; }
+  void apply(GemmArgs& g, const RunCtx& c) const {
+    g.w = w;
+    g.bias = c2;
+    g.ln_c1 = c1;
+    g.ln_eps = eps;
+    g.src1 = H16(c, x_off);
+  }
+};
+
 void emit_linear(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
                  const _Float16* w, const float* bias, int N, const Ten& out, const Ten* residual,
-                 bool geglu = false) {
+                 bool geglu = false, const LnFold& lf = LnFold{}) {
   const size_t o1 = x1.off, o2 = x2 ? x2->off : 0, oo = out.off;
   const size_t ores = residual ? residual->off : 0;
   const bool has2 = x2 != nullptr, hasr = residual != nullptr;
@@ -469,6 +499,7 @@ void emit_linear(Builder& B, std::vector<Op>& ops, const Ten& x1, const Ten* x2,
       g.ld_res = ldo;
     }
     g.geglu = geglu;
+    if (lf.on(g.M)) lf.apply(g, c);
     g.out = c.ws + oo;
     g.ldo = ldo;
     return gemm_run(g, c);
@@ -522,29 +553,51 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
   B.drop(g);
   for (int j = 0; j < depth; ++j) {
     const std::string b = n + ".blk" + std::to_string(j);
-    // self-attention
-    Ten t = B.alloc(HW, C);
-    {
+    // LayerNorm: its own kernel into t, or, for a call whose LayerNorm input
+    // is small (at most LN_FOLD_MAX_ELEMS values) and channels that suit the
+    // streamed kernel, folded into the product that consumes it (weights
+    // packed both ways)
+    const int64_t fold_rows = ln_folded(C) ? LN_FOLD_MAX_ELEMS / C : -1;
+    const float eps = cfg.ln_eps;
+    auto emit_ln = [&](const char* ln, Ten& t) {
+      t = B.alloc(HW, C);
       const size_t xi = h.off, to = t.off;
-      const float* lg = B.W32(b + ".ln1.g");
-      const float* lb = B.W32(b + ".ln1.b");
-      const float eps = cfg.ln_eps;
+      const float* lg = B.W32(b + ln + ".g");
+      const float* lb = B.W32(b + ln + ".b");
       ops.push_back([=](const RunCtx& c) {
-        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
+        const int64_t rows = (int64_t)c.R * HW;
+        if (rows <= fold_rows) return hipSuccess;  // folded into the product
+        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), rows, C, eps, c.s);
       });
-    }
+    };
+    auto fold_of = [&](const std::string& wname, const std::string& cname) {
+      LnFold f;
+      if (fold_rows < 0) return f;
+      f.w = B.W16(wname);
+      f.c1 = B.W32(cname + ".c1");
+      f.c2 = B.W32(cname + ".c2");
+      f.x_off = h.off;
+      f.eps = eps;
+      f.max_rows = fold_rows;
+      return f;
+    };
+    // self-attention
+    Ten t;
+    emit_ln(".ln1", t);
     // Q|K as token rows, V written transposed (channel rows, Rmax*HW tokens
     // each) so the attention kernel reads both K and V^T tiles as rows
     Ten qk = B.alloc(HW, 2 * C);
     Ten vt = B.alloc(HW, C);
     {
       const _Float16* w = B.W16(b + ".attn1.qkv.w");
+      const LnFold lf = fold_of(b + ".attn1.qkv.wln", b + ".attn1.qkv");
       const size_t xi = t.off, qko = qk.off, vto = vt.off;
       const int64_t vld = (int64_t)B.Rmax_ * HW;
       ops.push_back([=](const RunCtx& c) {
         GemmArgs g = dense_args(3 * C, C, w, nullptr);
         g.M = (int64_t)c.R * HW;
         g.src1 = H16(c, xi);
+        if (lf.on(g.M)) lf.apply(g, c);
         g.out = H16(c, qko);
         g.ldo = 2 * C;
         g.vt = H16(c, vto);
@@ -584,18 +637,10 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
     emit_linear(B, ops, a, nullptr, B.W16(b + ".attn1.o.w"), B.W32(b + ".attn1.o.b"), C, h, &h);
     B.drop(a);
     // cross-attention
-    t = B.alloc(HW, C);
-    {
-      const size_t xi = h.off, to = t.off;
-      const float* lg = B.W32(b + ".ln2.g");
-      const float* lb = B.W32(b + ".ln2.b");
-      const float eps = cfg.ln_eps;
-      ops.push_back([=](const RunCtx& c) {
-        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
-      });
-    }
     Ten qc = B.alloc(HW, C);
-    emit_linear(B, ops, t, nullptr, B.W16(b + ".attn2.q.w"), nullptr, C, qc, nullptr);
+    emit_ln(".ln2", t);
+    emit_linear(B, ops, t, nullptr, B.W16(b + ".attn2.q.w"), nullptr, C, qc, nullptr, false,
+                fold_of(b + ".attn2.q.wln", b + ".attn2.q"));
     B.drop(t);
     // context K|V of this block: computed once per call into a region reserved
     // before any per-step buffer, so no step op can overwrite it
@@ -630,19 +675,10 @@ Ten build_tr(Builder& B, std::vector<Op>& ops, const Ten& x, const std::string& 
     emit_linear(B, ops, a, nullptr, B.W16(b + ".attn2.o.w"), B.W32(b + ".attn2.o.b"), C, h, &h);
     B.drop(a);
     // GEGLU feed-forward
-    t = B.alloc(HW, C);
-    {
-      const size_t xi = h.off, to = t.off;
-      const float* lg = B.W32(b + ".ln3.g");
-      const float* lb = B.W32(b + ".ln3.b");
-      const float eps = cfg.ln_eps;
-      ops.push_back([=](const RunCtx& c) {
-        return layernorm_launch(H16(c, xi), lg, lb, H16(c, to), (int64_t)c.R * HW, C, eps, c.s);
-      });
-    }
     Ten f = B.alloc(HW, 4 * C);
+    emit_ln(".ln3", t);
     emit_linear(B, ops, t, nullptr, B.W16(b + ".ff1.w"), B.W32(b + ".ff1.b"), 8 * C, f, nullptr,
-                true);
+                true, fold_of(b + ".ff1.wln", b + ".ff1"));
     B.drop(t);
     emit_linear(B, ops, f, nullptr, B.W16(b + ".ff2.w"), B.W32(b + ".ff2.b"), C, h, &h);
     B.drop(f);
@@ -897,6 +933,25 @@ bool pack_weights(nv_unet* net, const float* blob) {
   auto end16 = [&]() {
     while (h16.size() % 128) h16.push_back((_Float16)0.f);
   };
+  // One weight row W[n][0..K) to float16; with a folded LayerNorm (gam, bet
+  // non-null) the row is gamma-scaled and c1 / c2 gain
+  // sum_k float16(gamma_k W[n][k]) and bias + sum_k beta_k W[n][k] (float64 sums).
+  auto push_row = [&](const float* wr, int K, const float* gam, const float* bet, double bias,
+                      std::vector<float>& c1, std::vector<float>& c2) {
+    if (!gam) {
+      for (int k = 0; k < K; ++k) h16.push_back((_Float16)wr[k]);
+      return;
+    }
+    double s1 = 0.0, s2 = bias;
+    for (int k = 0; k < K; ++k) {
+      const _Float16 h = (_Float16)(gam[k] * wr[k]);
+      h16.push_back(h);
+      s1 += (double)(float)h;
+      s2 += (double)bet[k] * (double)wr[k];
+    }
+    c1.push_back((float)s1);
+    c2.push_back((float)s2);
+  };
   // ResBlock time projections stacked
   int ttot = 0;
   for (auto& p : net->params) {
@@ -960,14 +1015,40 @@ bool pack_weights(nv_unet* net, const float* blob) {
     }
     // 2-D linear weights
     if (ends(".attn1.q.w")) {
-      const std::string b = n.substr(0, n.size() - 10);
-      begin16(b + ".attn1.qkv.w");
-      for (const char* part : {".attn1.q.w", ".attn1.k.w", ".attn1.v.w"}) {
-        const float* s2 = P(b + part);
-        const int64_t cnt = S(b + part)[0] * S(b + part)[1];
-        for (int64_t i = 0; i < cnt; ++i) h16.push_back((_Float16)s2[i]);
+      const std::string b = n.substr(0, n.size() - 10);  // strip ".attn1.q.w"
+      const int K = (int)p.shape[1];
+      std::vector<float> c1, c2;
+      for (const bool fold : {false, true}) {
+        if (fold && !ln_folded(K)) break;
+        const float* gam = fold ? P(b + ".ln1.g") : nullptr;
+        const float* bet = fold ? P(b + ".ln1.b") : nullptr;
+        begin16(b + (fold ? ".attn1.qkv.wln" : ".attn1.qkv.w"));
+        for (const char* part : {".attn1.q.w", ".attn1.k.w", ".attn1.v.w"}) {
+          const float* s2 = P(b + part);
+          for (int64_t r = 0; r < S(b + part)[0]; ++r)
+            push_row(s2 + r * K, K, gam, bet, 0.0, c1, c2);
+        }
+        end16();
       }
-      end16();
+      if (!c1.empty()) {
+        put32(b + ".attn1.qkv.c1", c1.data(), (int64_t)c1.size());
+        put32(b + ".attn1.qkv.c2", c2.data(), (int64_t)c2.size());
+      }
+      continue;
+    }
+    if (ends(".attn2.q.w") && ln_folded((int)p.shape[1])) {
+      const std::string b = n.substr(0, n.size() - 10);  // strip ".attn2.q.w"
+      const int K = (int)p.shape[1];
+      std::vector<float> c1, c2;
+      for (const bool fold : {false, true}) {
+        begin16(fold ? b + ".attn2.q.wln" : n);
+        for (int64_t r = 0; r < p.shape[0]; ++r)
+          push_row(src + r * K, K, fold ? P(b + ".ln2.g") : nullptr,
+                   fold ? P(b + ".ln2.b") : nullptr, 0.0, c1, c2);
+        end16();
+      }
+      put32(b + ".attn2.q.c1", c1.data(), (int64_t)c1.size());
+      put32(b + ".attn2.q.c2", c2.data(), (int64_t)c2.size());
       continue;
     }
     if (ends(".attn1.k.w") || ends(".attn1.v.w") || ends(".attn2.v.w")) continue;
@@ -983,14 +1064,26 @@ bool pack_weights(nv_unet* net, const float* blob) {
       continue;
     }
     if (ends(".ff1.w")) {
+      const std::string b = n.substr(0, n.size() - 6);  // strip ".ff1.w"
       const int C8 = (int)p.shape[0], C4 = C8 / 2, K = (int)p.shape[1];
-      begin16(n);
-      for (int r = 0; r < C8; ++r) {
-        const int grp = r / 32, wi = r % 32;
-        const int srow = wi < 16 ? grp * 16 + wi : C4 + grp * 16 + (wi - 16);
-        for (int k = 0; k < K; ++k) h16.push_back((_Float16)src[(int64_t)srow * K + k]);
+      const float* bias = P(b + ".ff1.b");
+      std::vector<float> c1, c2;
+      for (const bool fold : {false, true}) {
+        if (fold && !ln_folded(K)) break;
+        const float* gam = fold ? P(b + ".ln3.g") : nullptr;
+        const float* bet = fold ? P(b + ".ln3.b") : nullptr;
+        begin16(fold ? b + ".ff1.wln" : n);
+        for (int r = 0; r < C8; ++r) {
+          const int grp = r / 32, wi = r % 32;
+          const int srow = wi < 16 ? grp * 16 + wi : C4 + grp * 16 + (wi - 16);
+          push_row(src + (int64_t)srow * K, K, gam, bet, bias[srow], c1, c2);
+        }
+        end16();
       }
-      end16();
+      if (!c1.empty()) {
+        put32(b + ".ff1.c1", c1.data(), (int64_t)c1.size());
+        put32(b + ".ff1.c2", c2.data(), (int64_t)c2.size());
+      }
       continue;
     }
     begin16(n);
