@@ -22,14 +22,16 @@
 namespace nv {
 namespace {
 
-constexpr int KB = 64;   // keys per block
-constexpr int VROW = KB + 8;  // halfs per LDS V^T row
 constexpr float LOG2E = 1.4426950408889634f;
 
 // QB: 16-query column blocks per wave (2; 1 where the grid would otherwise
-// leave compute units idle, e.g. 1024 or 256 queries per head at batch 1)
-template <int DH, int QB>
+// leave compute units idle, e.g. 1024 or 256 queries per head at batch 1).
+// KB: keys per block (64, or 128, which halves the barriers and max
+// reductions per key at the price of registers).
+template <int DH, int QB, int KB>
 __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
+  constexpr int VROW = KB + 8;                 // halfs per LDS V^T row
+  constexpr int NH = KB / 16, NS = KB / 32;    // 16-key quarters, 32-key PV steps
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
@@ -140,9 +142,9 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     const _Float16* K_ = sK[cur];
     const _Float16* V_ = sVt[cur];
     // S^T for 4 key quarters x QB query blocks; lane holds keys h*16 + 4*kc + r.
-    floatx4 s[QB][4];
+    floatx4 s[QB][NH];
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < NH; ++h) {
       const _Float16* kr = &K_[(h * 16 + li) * KROW];
       half8 fk[N32];
 #pragma unroll
@@ -161,7 +163,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-        for (int h = 0; h < 4; ++h)
+        for (int h = 0; h < NH; ++h)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (kb * KB + h * 16 + kc * 4 + r >= a.L) s[qb][h][r] = -INFINITY;
@@ -177,7 +179,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     for (int qb = 0; qb < QB; ++qb) {
       float m = -INFINITY;
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
+      for (int h = 0; h < NH; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r) m = fmaxf(m, s[qb][h][r]);
       m = fmaxf(m, __shfl_xor(m, 16, 64));
@@ -196,12 +198,12 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
         for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
       }
     }
-    half8 fp[QB][2];
+    half8 fp[QB][NS];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float psum = 0.f;
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
+      for (int h = 0; h < NH; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float p = __builtin_amdgcn_exp2f(s[qb][h][r] - mrun[qb]);
@@ -215,7 +217,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < DV / 16; ++j) {
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < NS; ++st) {
         const _Float16* vr = &V_[(j * 16 + li) * VROW + st * 32];
         const half4 lo = *(const half4*)(vr + kc * 4);
         const half4 hi = *(const half4*)(vr + 16 + kc * 4);
@@ -267,13 +269,14 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
 }
 
-template <int DH, int QB>
+template <int DH, int QB, int KB>
 hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   constexpr int KCH = DH / 8, KST = KCH % 2 ? KCH : KCH + 1, DV = (DH + 15) / 16 * 16;
+  constexpr int VROW = KB + 8;
   const size_t lds = (size_t)2 * (KB * KST * 8 + DV * VROW) * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -284,7 +287,7 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
   const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes);
-  hipExtLaunchKernelGGL((attn_f16<DH, QB>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
+  hipExtLaunchKernelGGL((attn_f16<DH, QB, KB>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
                         a);
   return hipGetLastError();
 }
@@ -294,7 +297,13 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
 template <int DH>
 hipError_t launch(const AttnArgs& a, hipStream_t s) {
   const int64_t wgs2 = ceil_div(a.S, 128) * a.heads * a.rows;
-  return wgs2 < 256 ? launch_qb<DH, 1>(a, s) : launch_qb<DH, 2>(a, s);
+  if (wgs2 < 256) return launch_qb<DH, 1, 64>(a, s);
+  // 128-key blocks for 40-dim heads when at most two workgroups per CU exist
+  // (batch 1 at 4,096 queries): the larger register set (216 VGPRs) costs no
+  // occupancy there; on larger grids three 64-key workgroups per CU win
+  if constexpr (DH == 40)
+    if (wgs2 <= 512) return launch_qb<DH, 2, 128>(a, s);
+  return launch_qb<DH, 2, 64>(a, s);
 }
 
 }  // namespace

@@ -62,6 +62,43 @@ def test_eps_teacher_forced(tiny):
         assert du <= EPS_TOL and dc <= EPS_TOL
 
 
+def test_eps_teacher_forced_strong_layernorm():
+    """Transformer LayerNorms with gains far from 1 and large shifts, and output projections
+    scaled up so that the transformer branches weigh on epsilon (in the oracle, dropping the
+    shifts or the gains moves epsilon by 0.18 and 0.17 here): the products that fold the
+    LayerNorm (gamma-scaled weights, row statistics in the kernel, beta . W in the bias) must
+    still match the oracle, which applies the LayerNorm first."""
+    import paper_2312_04429_amd as P
+    cfg = synth.unet_config("tiny")
+    w = dict(synth.make_weights(cfg, 0))
+    rng = np.random.default_rng(21)
+    for k in list(w):
+        if ".ln" in k and k.endswith(".g"):
+            w[k] = (2.0 * (1.0 + rng.uniform(-0.5, 0.5, w[k].shape))).astype(np.float32)
+        elif ".ln" in k and k.endswith(".b"):
+            w[k] = rng.normal(0.0, 1.0, w[k].shape).astype(np.float32)
+        elif k.endswith((".attn1.o.w", ".attn2.o.w", ".ff2.w")):
+            w[k] = (w[k] * 8.0).astype(np.float32)
+    net = P.NvUNet(cfg, w)
+    try:
+        ora = U.UNet(cfg, w)
+        B, N = 2, 20
+        x = synth.make_latents(B, 4, cfg["H"], cfg["W"], 17)
+        cond, unc = _ctx(cfg, B, 31), _ctx(cfg, B, 32)
+        steps = [3, 15]
+        print("tiny eps parity, strong LayerNorm parameters", flush=True)
+        eu, ec = net.nv_unet_eps(t(x), steps, t(cond), t(unc), sched=SCHED(N))
+        eu, ec = eu.cpu().numpy(), ec.cpu().numpy()
+        for b in range(B):
+            ts = schedule.timesteps(N, 1000)[steps[b]]
+            ru, rc = ora(x[b], ts, unc[b]), ora(x[b], ts, cond[b])
+            du, dc = np.abs(eu[b] - ru).max(), np.abs(ec[b] - rc).max()
+            print(f"  b{b} t={ts} maxabs u {du:.2e} c {dc:.2e}", flush=True)
+            assert du <= EPS_TOL and dc <= EPS_TOL
+    finally:
+        net.close()
+
+
 def _cached_state(ora, cfg, i, K, N):
     """State after K steps of a full oracle run for cached entry i (own prompt, own x_N)."""
     ctx = _ctx(cfg, 2, 1000 + i)
