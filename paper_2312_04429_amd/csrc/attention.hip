@@ -297,7 +297,13 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
 template <int DH>
 hipError_t launch(const AttnArgs& a, hipStream_t s) {
   const int64_t wgs2 = ceil_div(a.S, 128) * a.heads * a.rows;
-  if (wgs2 < 256) return launch_qb<DH, 1, 64>(a, s);
+  if (wgs2 < 256) {
+    // 80-dim heads over at most one workgroup per CU (batch 1 at 1,024
+    // queries): 128-key blocks; the kernel holds one wave per SIMD either way
+    if constexpr (DH == 80)
+      if (ceil_div(a.S, 64) * a.heads * a.rows <= 256) return launch_qb<DH, 1, 128>(a, s);
+    return launch_qb<DH, 1, 64>(a, s);
+  }
   // 128-key blocks for 40-dim heads when at most two workgroups per CU exist
   // (batch 1 at 4,096 queries): the larger register set (216 VGPRs) costs no
   // occupancy there; on larger grids three 64-key workgroups per CU win
