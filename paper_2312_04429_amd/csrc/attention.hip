@@ -14,7 +14,8 @@
 // one 32-key MFMA step are the 2 x 4 keys it holds; V^T supplies the same 8
 // keys for its row d).  V arrives transposed from its projection, so both
 // tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps,
-// dims past d read as zero (d = 40 -> 64, 80 -> 96 for Q K^T).
+// dims past d read as zero (d = 40 -> 64, 80 -> 96 for Q K^T): Q's from
+// registers, K's from a zero pad of each LDS key row.
 #include "common.h"
 #include "attention.h"
 #include "trace.h"
@@ -23,6 +24,14 @@ namespace nv {
 namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
+
+// Halfs per LDS key row: an odd number of 16-byte chunks (conflict-free row
+// reads); a head dim off the 32 grid gets its row padded with zeros to the
+// next multiple of 32 plus one chunk, so every lane reads its Q K^T fragment
+// unconditionally (the pad meets Q's zeros past d).
+constexpr int krow(int dh) {
+  return dh % 32 ? (dh + 31) / 32 * 32 + 8 : ((dh / 8) % 2 ? dh : dh + 8);
+}
 
 // QB: 16-query column blocks per wave (2; 1 where the grid would otherwise
 // leave compute units idle, e.g. 1024 or 256 queries per head at batch 1).
@@ -35,8 +44,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
-  constexpr int KST = KCH % 2 ? KCH : KCH + 1; // odd chunk stride: conflict-free row reads
-  constexpr int KROW = KST * 8;                // halfs per LDS key row
+  constexpr bool KPAD = DH % 32 != 0;          // key rows padded with zeros to N32 * 32 dims
+  constexpr int KROW = krow(DH);               // halfs per LDS key row
   constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
   constexpr int KPT = (KCN + 255) / 256, VPT = (VCN + 255) / 256;
   static_assert(DH % 8 == 0, "head dim");
@@ -149,7 +158,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
       half8 fk[N32];
 #pragma unroll
       for (int ks = 0; ks < N32; ++ks)
-        fk[ks] = ks * 32 + kc * 8 < DH ? *(const half8*)(kr + ks * 32 + kc * 8) : half8{};
+        fk[ks] = (KPAD || ks * 32 + kc * 8 < DH) ? *(const half8*)(kr + ks * 32 + kc * 8)
+                                                 : half8{};
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         s[qb][h] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -234,6 +244,13 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   };
   if (ONES)
     for (int i = tid; i < 2 * KB; i += 256) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
+  if (KPAD) {  // zero pad of every key row in both buffers (the stash never writes it)
+    constexpr int PADC = (N32 * 32 - DH) / 8;
+    for (int i = tid; i < 2 * KB * PADC; i += 256) {
+      const int b = i / (KB * PADC), r = (i / PADC) % KB, c = i % PADC;
+      *(half8*)&sK[b][r * KROW + DH + c * 8] = half8{};
+    }
+  }
   fetch(0, rkA, rvA);
   if (1 < nkb) fetch(1, rkB, rvB);
   stash(0, 0, rkA, rvA);
@@ -271,9 +288,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 
 template <int DH, int QB, int KB>
 hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
-  constexpr int KCH = DH / 8, KST = KCH % 2 ? KCH : KCH + 1, DV = (DH + 15) / 16 * 16;
-  constexpr int VROW = KB + 8;
-  const size_t lds = (size_t)2 * (KB * KST * 8 + DV * VROW) * 2;
+  constexpr int DV = (DH + 15) / 16 * 16, VROW = KB + 8;
+  const size_t lds = (size_t)2 * (KB * krow(DH) + DV * VROW) * 2;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB>,
