@@ -96,9 +96,35 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   // the same multiply then accumulates the softmax denominator in O^T row DH.
   constexpr bool ONES = DV > DH;
 
-  const _Float16* kbase = a.k + (int64_t)row * a.L * a.ldk + head * DH;
-  const _Float16* vtbase = a.vt + (int64_t)head * DH * a.vt_ld + (int64_t)row * a.vt_row;
   const int nkb = (a.L + KB - 1) / KB;
+
+  // K and V^T tiles through buffer descriptors over the whole tensors (the
+  // launcher checks both stay under 2 GiB): each thread's byte offsets of
+  // block 0 are fixed, a block adds a uniform step.  Rows past L read the
+  // next row's keys or, past the tensor, zeros; their scores are masked and
+  // their V^T columns zeroed in the stash, so no per-load test is needed.
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<_Float16*>(a.k), (short)0, (int)((int64_t)a.rows * a.L * a.ldk * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<_Float16*>(a.vt), (short)0, (int)((int64_t)a.heads * DH * a.vt_ld * 2),
+      0x00020000);
+  constexpr uint32_t OOB = 0x80000000u;  // past both ranges: loads return zeros
+  uint32_t koff[KPT], voff[VPT];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int c = tid + i * 256;
+    koff[i] = c < KCN ? (uint32_t)((((int64_t)row * a.L + c / KCH) * a.ldk + head * DH +
+                                    (c % KCH) * 8) * 2)
+                      : OOB;
+  }
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int c = tid + i * 256;
+    voff[i] = c < VCN ? (uint32_t)((((int64_t)head * DH + c / (KB / 8)) * a.vt_ld +
+                                    (int64_t)row * a.vt_row + (c % (KB / 8)) * 8) * 2)
+                      : OOB;
+  }
+  const uint32_t kstep = (uint32_t)KB * a.ldk * 2, vstep = KB * 2;
 
   // Two register sets: block kb + 2 is requested while block kb is multiplied
   // and block kb + 1 waits in the other set (two blocks of latency hiding).
@@ -106,18 +132,13 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   auto fetch = [&](int kb, uint4(&rk)[KPT], uint4(&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const int c = tid + i * 256;
-      const int kr = c / KCH, ch = c % KCH;
-      const int j = kb * KB + kr;
-      rk[i] = (c < KCN && j < a.L) ? *(const uint4*)(kbase + (int64_t)j * a.ldk + ch * 8)
-                                   : make_uint4(0, 0, 0, 0);
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(krs, koff[i] + kb * kstep, 0, 0);
+      rk[i] = make_uint4(v[0], v[1], v[2], v[3]);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
-      const int c = tid + i * 256;
-      const int d = c / (KB / 8), j0 = kb * KB + (c % (KB / 8)) * 8;
-      rv[i] = (c < VCN && j0 < a.L) ? *(const uint4*)(vtbase + (int64_t)d * a.vt_ld + j0)
-                                    : make_uint4(0, 0, 0, 0);
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff[i] + kb * vstep, 0, 0);
+      rv[i] = make_uint4(v[0], v[1], v[2], v[3]);
     }
   };
   auto stash = [&](int buf, int kb, const uint4(&rk)[KPT], const uint4(&rv)[VPT]) {
@@ -298,6 +319,11 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
     attr_set = true;
   }
   if (a.vt_row < a.L || a.vt_row % 8 || a.vt_ld % 8 || a.vt_ld < (int64_t)a.rows * a.vt_row)
+    return hipErrorInvalidValue;
+  // the K / V^T buffer descriptors address at most 2 GiB, with the out-of-range
+  // offset 2^31 plus any block step staying below 2^32
+  if ((int64_t)a.rows * a.L * a.ldk * 2 >= 0x80000000ll ||
+      (int64_t)a.heads * DH * a.vt_ld * 2 >= 0x80000000ll)
     return hipErrorInvalidValue;
   dim3 grid((unsigned)(ceil_div(a.S, 64 * QB) * a.heads * a.rows));
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
