@@ -723,14 +723,15 @@ hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Ci
                           int C0, int rows, _Float16* out, hipStream_t s) {
   if (Cin > 16) return hipErrorInvalidValue;
   const size_t lds = ((size_t)C0 * Cin * 9 + C0) * 4;
-  if (lds > 65536) {
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 65536) {  // once, for the largest size any call may ask for
     static bool attr = false;
     if (!attr) {
       hipError_t e = hipFuncSetAttribute((const void*)conv_in_k<0>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
       if (e == hipSuccess)
         e = hipFuncSetAttribute((const void*)conv_in_k<4>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
       if (e != hipSuccess) return e;
       attr = true;
     }
