@@ -242,8 +242,8 @@ def build_lookup_inputs(wl, B, args, dev, torch, synth):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path's "
-              "multi-GPU sharding is described in DESIGN.md but not built.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): sharding the "
+              "cache rows and the samples over several GPUs is not built.", file=sys.stderr)
         sys.exit(2)
     import torch
 
