@@ -3,10 +3,10 @@
 // latent tokens and cross-attention to the text context (Sec. 2.1: text
 // conditioning enters the UNet through cross-attention).
 //
-// Work split: one workgroup = 128 queries of one (row, head); each wave owns
-// 32 queries (two 16-query column blocks).  Keys stream in blocks of 64
-// through two register sets (fetched two blocks ahead) and a double-buffered
-// LDS, one barrier per block.  The kernel computes the
+// Work split: one workgroup of four waves = 64 or 128 queries of one (row,
+// head); each wave owns one or two 16-query column blocks (QB).  Keys stream
+// in blocks of 64 or 128 (KB) through two register sets (fetched two blocks
+// ahead) and a double-buffered LDS, one barrier per block.  The kernel computes the
 // transposed score block S^T = K Q^T so that every accumulator entry of a
 // lane belongs to one query (column l % 16): the running max / sum and the
 // output rescale are per-lane scalars, and the probabilities P^T are already
