@@ -12,6 +12,7 @@ import math
 
 import numpy as np
 import pytest
+import torch
 
 import synth
 from oracle import ivf
@@ -128,3 +129,25 @@ def test_duplicate_centroids_ties_and_empty_lists():
     assert pr[0, 0] == 0 and i1[0] == 7
     c1, _, _, _ = ivf.build(X, [7, 8, 50, 120], 1)
     assert np.array_equal(c1[1], X[8])
+
+
+def test_round_like_matches_torch_rounding():
+    """The centroid storage rounding (float64 -> float32 -> bfloat16, nearest
+    even at each step) against torch's own conversions, on values built to sit
+    exactly on and one ulp either side of bfloat16 ties (both parities of the
+    kept bit), at both signs, in the subnormal range and next to the largest
+    finite bfloat16.  A truncating or ties-away rounding fails here."""
+    rng = np.random.default_rng(5)
+    hi = rng.integers(0, 0x7F7F, 4000, dtype=np.uint32)  # finite bf16 patterns below the max
+    lows = np.array([0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF], np.uint32)
+    u = (hi[:, None] << np.uint32(16)) | lows[None, :]
+    f32 = u.reshape(-1).view(np.float32)
+    vals = np.concatenate([f32, -f32]).astype(np.float64)
+    # float64 values between float32 neighbours (the first rounding matters too)
+    vals = np.concatenate([vals, vals * (1 + 2.0 ** -30), rng.standard_normal(4000) * 1e-39,
+                           np.array([3.3895313892515355e38, -3.3895313892515355e38])])
+    got = ivf._round_like(vals, np.uint16)
+    ref = torch.tensor(vals, dtype=torch.float64).to(torch.float32).to(torch.bfloat16)
+    np.testing.assert_array_equal(got, ref.view(torch.int16).numpy().view(np.uint16))
+    np.testing.assert_array_equal(ivf._round_like(vals, np.float32),
+                                  torch.tensor(vals).to(torch.float32).numpy())

@@ -109,7 +109,7 @@ def _t(a):
     return torch.tensor(np.asarray(a), dtype=F64)
 
 
-def _torch_unet(cfg, w, x, t, ctx):
+def _torch_unet(cfg, w, x, t, ctx, pooled=None):
     W = {k: _t(v) for k, v in w.items()}
     G, eg, el = cfg["gn_groups"], cfg["gn_eps"], cfg["ln_eps"]
     c0 = cfg["ch"][0]
@@ -118,6 +118,8 @@ def _torch_unet(cfg, w, x, t, ctx):
     temb = torch.cat([torch.cos(t * fr), torch.sin(t * fr)])
     temb = TF.linear(TF.silu(TF.linear(temb, W["time.l1.w"], W["time.l1.b"])), W["time.l2.w"],
                      W["time.l2.b"])
+    if pooled is not None:  # added as is to the embedding, before the ResBlocks' SiLU
+        temb = temb + _t(pooled)
     c_ = _t(ctx)
 
     def conv(h, n, stride=1):
@@ -198,6 +200,27 @@ def test_tiny_unet_matches_independent_torch_composition(over):
     got = U.UNet(cfg, w)(x, 741, ctx)
     ref = _torch_unet(cfg, w, x, 741.0, ctx)
     np.testing.assert_allclose(got, ref, rtol=1e-3, atol=2e-4)
+
+
+def test_sdxl_topology_with_pooled_vector_matches_independent_torch_composition():
+    """The SDXL-shaped rules on a narrow network: head count from head_dim (1, 2
+    and 4 heads of 64), transformer depth 0/2 per level and a depth-10 middle
+    block, and a pooled vector as wide as the time embedding added to it.  A
+    pooled vector added before time.l2 or after the ResBlocks' SiLU, a head
+    count taken from n_heads, or a dropped depth block fails the comparison."""
+    cfg = synth.unet_config("sdxl", H=8, W=8, ch=(64, 128, 256), ctx_len=6, ctx_dim=96,
+                            pooled_dim=256, depth=(0, 2, 2), mid_depth=10)
+    w = synth.make_weights(cfg, 0)
+    x = synth.make_latents(1, 4, cfg["H"], cfg["W"], 2002)[0]
+    ctx = synth.make_contexts(1, cfg["ctx_len"], cfg["ctx_dim"], 7)[0]
+    pooled = synth.make_pooled(1, cfg["pooled_dim"], 8)[0]
+    net = U.UNet(cfg, w)
+    got = net(x, 601, ctx, pooled)
+    ref = _torch_unet(cfg, w, x, 601.0, ctx, pooled)
+    np.testing.assert_allclose(got, ref, rtol=1e-3, atol=2e-4)
+    # the pooled vector reaches eps (its effect is far above the tolerance)
+    plain = _torch_unet(cfg, w, x, 601.0, ctx, None)
+    assert np.abs(ref - plain).max() > 50 * 2e-4
 
 
 def test_context_token_permutation_invariance():
