@@ -879,6 +879,9 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
 
 template <int MODE, int BM, int BN, int STAGES, bool LN>
 hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
+  if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
+      (int64_t)g.N * g.ldw * 2 >= 0x80000000ll)
+    return hipErrorInvalidValue;  // descriptors address less than 2 GiB (gemm_launch chunks)
   const size_t lds = (size_t)STAGES * (BM + BN) * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
@@ -1005,9 +1008,7 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
   return launch<MODE, 64, 64>(g, split_for(t64, 4), s);
 }
 
-}  // namespace
-
-hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
+hipError_t gemm_launch_one(const GemmArgs& gin, hipStream_t s) {
   GemmArgs g = gin;
   // byte extents of the A sources for the range descriptors
   if (g.conv) {
@@ -1027,6 +1028,56 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
              (!g.bias || al(g.bias, 16)) &&
              (!g.residual || ((g.ld_res % 4 == 0) && al(g.residual, 8)));
   return g.conv ? dispatch<1>(g, s) : dispatch<0>(g, s);
+}
+
+}  // namespace
+
+// The buffer descriptors address less than 2 GiB (the out-of-range offset is
+// 2^31), so a product whose A source reaches that runs as a sequence of row
+// chunks below it, each a product of its own on the same stream.  Chunks hold
+// whole units: one sample's output pixels for a convolution, and for a dense
+// product the rows that share a row-vector entry or a transposed-output
+// column block (both indexed per sample).  Weights of 2 GiB or more, or a
+// single unit that large, are rejected.
+hipError_t gemm_launch(const GemmArgs& g, hipStream_t s) {
+  constexpr uint64_t LIMIT = 0x80000000ull;
+  if ((uint64_t)g.N * (uint64_t)g.ldw * 2 >= LIMIT) return hipErrorInvalidValue;
+  int64_t unit = 1;
+  uint64_t ub1 = 0, ub2 = 0, src_u1 = 0, src_u2 = 0;  // bytes / halfs of source per unit
+  if (g.conv) {
+    unit = (int64_t)g.Ho * g.Wo;
+    if (unit <= 0 || g.M % unit) return hipErrorInvalidValue;
+    src_u1 = (uint64_t)g.Hin * g.Win * g.C1;
+    src_u2 = (uint64_t)g.Hin * g.Win * g.C2;
+  } else {
+    auto lcm = [](int64_t a, int64_t b) { return a / std::__gcd(a, b) * b; };
+    if (g.rowvec && g.rows_div > 1) unit = lcm(unit, g.rows_div);
+    if (g.vt && g.vt_div > 1) unit = lcm(unit, g.vt_div);
+    src_u1 = (uint64_t)unit * g.lda1;
+    src_u2 = g.src2 ? (uint64_t)unit * g.lda2 : 0;
+  }
+  ub1 = src_u1 * 2;
+  ub2 = src_u2 * 2;
+  const uint64_t ub = std::max(ub1, ub2);
+  const int64_t units = ceil_div(g.M, unit);
+  if (ub == 0 || (uint64_t)units * ub < LIMIT) return gemm_launch_one(g, s);
+  const int64_t per = (int64_t)((LIMIT - 1) / ub);  // units per chunk
+  if (per < 1) return hipErrorInvalidValue;
+  const size_t osz = g.out_f32 ? 4 : 2;
+  for (int64_t u0 = 0; u0 < units; u0 += per) {
+    const int64_t m0 = u0 * unit;
+    GemmArgs c = g;
+    c.M = std::min<int64_t>(g.M - m0, per * unit);
+    c.src1 = g.src1 + u0 * src_u1;
+    if (g.src2) c.src2 = g.src2 + u0 * src_u2;
+    c.out = (char*)g.out + (size_t)m0 * g.ldo * osz;
+    if (g.residual) c.residual = g.residual + m0 * g.ld_res;
+    if (g.rowvec) c.rowvec = g.rowvec + (m0 / g.rows_div) * g.ld_rowvec;
+    if (g.vt) c.vt = g.vt + (m0 / g.vt_div) * g.vt_stride;
+    const hipError_t e = gemm_launch_one(c, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace nv
