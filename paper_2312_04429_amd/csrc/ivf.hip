@@ -12,7 +12,7 @@
 //           (assign every row with the exact lookup, then the normalised float64
 //           mean of each non-empty list, rows in ascending order, rounded to
 //           float32 and on to the cache type); a final assignment; the rows
-//           sorted by list (stable radix sort: ascending rows within a list),
+//           sorted by list (a stable counting sort: ascending rows within a list),
 //           list offsets, and a copy of the rows in list order, so a probe
 //           reads one contiguous block.
 //   search: centroid scores per (query, list); the best nprobe lists per query
@@ -20,8 +20,6 @@
 //           canonically (rows staged through LDS with coalesced loads, one
 //           thread per row); per-(query, probe, chunk) best rows merged in a
 //           final pass; float32 similarity and the selector's K.
-#include <hipcub/hipcub.hpp>
-
 #include <algorithm>
 #include <cmath>
 #include <vector>
@@ -67,22 +65,101 @@ __global__ void __launch_bounds__(256) rows_to_f32_k(const void* __restrict__ sr
   }
 }
 
-__global__ void iota_k(int64_t* v, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
-    v[i] = i;
+// Stable counting sort of the rows by list (L <= 4096 lists): the rows are cut
+// into nb consecutive blocks of R rows; list_count_k counts each block's rows
+// per list, list_scan_k turns the counts into list offsets and, per (block,
+// list), the position of the block's first row of that list; list_scatter_k
+// walks each block's rows in ascending order, 64 at a time, and places row r
+// of list l at that position plus the number of earlier rows of l in the
+// block.  Ties keep row order, so every list holds its rows ascending.
+// A list id outside [0, L) cannot come from the assignment (a lookup over L >= 1
+// centroids always names one); it is clamped so no access leaves the arrays.
+constexpr int MAX_LISTS = 4096;
+constexpr int64_t SORT_MIN_ROWS = 4096;  // rows per block at least
+constexpr int64_t SORT_MAX_BLOCKS = 1024;
+
+__device__ inline int list_of(const int64_t* lists, int64_t r, int L) {
+  const int64_t l = lists[r];
+  return l < 0 ? 0 : (l >= L ? L - 1 : (int)l);
 }
 
-// offsets[l] = first position of list l in the sorted keys (binary search)
-__global__ void offsets_k(const int64_t* __restrict__ keys, int64_t n, int L,
-                          int64_t* __restrict__ off) {
-  const int l = blockIdx.x * blockDim.x + threadIdx.x;
-  if (l > L) return;
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) / 2;
-    if (keys[mid] < l) lo = mid + 1; else hi = mid;
+__global__ void __launch_bounds__(256) list_count_k(const int64_t* __restrict__ lists, int64_t n,
+                                                    int L, int64_t R,
+                                                    int32_t* __restrict__ counts) {
+  __shared__ int32_t h[MAX_LISTS];
+  for (int l = threadIdx.x; l < L; l += 256) h[l] = 0;
+  __syncthreads();
+  const int64_t r0 = (int64_t)blockIdx.x * R, r1 = min(n, r0 + R);
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) atomicAdd(&h[list_of(lists, r, L)], 1);
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += 256) counts[(int64_t)blockIdx.x * L + l] = h[l];
+}
+
+// One workgroup: column sums over the blocks (exclusive, in place), list
+// totals, their exclusive scan into off[0..L], then off added to every column.
+__global__ void __launch_bounds__(1024) list_scan_k(int32_t* __restrict__ counts, int nb, int L,
+                                                    int64_t* __restrict__ off) {
+  __shared__ int64_t tot[MAX_LISTS];
+  for (int l = threadIdx.x; l < L; l += 1024) {
+    int64_t run = 0;
+    for (int b = 0; b < nb; ++b) {
+      const int32_t c = counts[(int64_t)b * L + l];
+      counts[(int64_t)b * L + l] = (int32_t)run;
+      run += c;
+    }
+    tot[l] = run;
   }
-  off[l] = lo;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int l = 0; l < L; ++l) {
+      const int64_t c = tot[l];
+      tot[l] = run;
+      off[l] = run;
+      run += c;
+    }
+    off[L] = run;
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += 1024) {
+    const int64_t base = tot[l];
+    for (int b = 0; b < nb; ++b) counts[(int64_t)b * L + l] += (int32_t)base;
+  }
+}
+
+// One wave per block of rows: the next free position of each list in LDS; per
+// 64 rows, a lane's rank among earlier lanes of its list (readlane sweep), then
+// the last lane of each list advances that list's position.
+__global__ void __launch_bounds__(64) list_scatter_k(const int64_t* __restrict__ lists, int64_t n,
+                                                     int L, int64_t R,
+                                                     const int32_t* __restrict__ base,
+                                                     int64_t* __restrict__ perm) {
+  __shared__ int32_t next[MAX_LISTS];
+  const int lane = threadIdx.x;
+  for (int l = lane; l < L; l += 64) next[l] = base[(int64_t)blockIdx.x * L + l];
+  __syncthreads();
+  const int64_t r0 = (int64_t)blockIdx.x * R, r1 = min(n, r0 + R);
+  for (int64_t c = r0; c < r1; c += 64) {
+    const int64_t r = c + lane;
+    const bool live = r < r1;
+    const int l = live ? list_of(lists, r, L) : -1;
+    int rank = 0, same = 0;
+    for (int j = 0; j < 64; ++j) {
+      const int lj = __builtin_amdgcn_readlane(l, j);
+      const bool eq = live && lj == l;
+      rank += (eq && j < lane) ? 1 : 0;
+      same += eq ? 1 : 0;
+    }
+    const int pos = live ? next[l] + rank : 0;
+    __builtin_amdgcn_wave_barrier();
+    if (live) perm[pos] = r;
+    if (live && rank == same - 1) next[l] = pos + 1;
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+inline int64_t sort_rows_per_block(int64_t n) {
+  return std::max<int64_t>(SORT_MIN_ROWS, ceil_div(n, SORT_MAX_BLOCKS));
 }
 
 // sums[l][k] = sum over the rows of list l, in ascending row order, of row[k] (float64)
@@ -398,15 +475,9 @@ __global__ void __launch_bounds__(256) probe_final_k(const double* __restrict__ 
   }
 }
 
-inline int bits_for(int L) {
-  int b = 1;
-  while ((1 << b) < L) ++b;
-  return b;
-}
-
 struct BuildWs {
-  size_t qf, lk, idx_tmp, sim_tmp, k_tmp, keys, keys_sorted, vals, sums, sort_tmp, total;
-  size_t sort_bytes, lk_bytes;
+  size_t qf, lk, idx_tmp, sim_tmp, k_tmp, init_idx, sums, counts, total;
+  size_t lk_bytes;
 };
 
 inline BuildWs plan_build(int64_t n, int d, int L) {
@@ -418,21 +489,14 @@ inline BuildWs plan_build(int64_t n, int d, int L) {
     return at;
   };
   w.lk_bytes = nv_cache_lookup_workspace(ASSIGN_BATCH, L, d);
-  size_t sb = 0;
-  hipcub::DeviceRadixSort::SortPairs(nullptr, sb, (const int64_t*)nullptr, (int64_t*)nullptr,
-                                     (const int64_t*)nullptr, (int64_t*)nullptr, (int)n, 0,
-                                     bits_for(L));
-  w.sort_bytes = sb;
   w.qf = take((size_t)ASSIGN_BATCH * d * 4);
   w.lk = take(w.lk_bytes);
   w.idx_tmp = take((size_t)ASSIGN_BATCH * 8);
   w.sim_tmp = take((size_t)ASSIGN_BATCH * 4);
   w.k_tmp = take((size_t)ASSIGN_BATCH * 4);
-  w.keys = take((size_t)n * 8);
-  w.keys_sorted = take((size_t)n * 8);
-  w.vals = take((size_t)n * 8);
+  w.init_idx = take((size_t)std::max<int64_t>(L, 1) * 8);
   w.sums = take((size_t)L * d * 8);
-  w.sort_tmp = take(sb);
+  w.counts = take((size_t)ceil_div(n, sort_rows_per_block(n)) * L * 4);
   w.total = o;
   return w;
 }
@@ -470,12 +534,11 @@ extern "C" int32_t nv_ivf_build(const void* cache, int32_t c_dtype, int64_t n, i
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   const int bf = c_dtype == NV_BF16;
-  int64_t* keys_sorted = (int64_t*)(ws + w.keys_sorted);
-  int64_t* vals = (int64_t*)(ws + w.vals);
+  int64_t* init_idx = (int64_t*)(ws + w.init_idx);
   // initial centroids: the rows at init (host indices staged through the key buffer)
-  NV_HIP_TRY(hipMemcpyAsync(keys_sorted, init, (size_t)L * 8, hipMemcpyHostToDevice, s));
+  NV_HIP_TRY(hipMemcpyAsync(init_idx, init, (size_t)L * 8, hipMemcpyHostToDevice, s));
   hipLaunchKernelGGL(gather_rows_k, dim3((unsigned)std::min<int64_t>(ceil_div((int64_t)L * d, 256), 4096)),
-                     dim3(256), 0, s, cache, bf, d, (const int64_t*)keys_sorted, (int64_t)L, cents);
+                     dim3(256), 0, s, cache, bf, d, (const int64_t*)init_idx, (int64_t)L, cents);
   NV_LAUNCH_CHECK("gather_rows_k");
   const float thr_none[1] = {1e30f};
   const int32_t k_none[1] = {0};
@@ -494,16 +557,17 @@ extern "C" int32_t nv_ivf_build(const void* cache, int32_t c_dtype, int64_t n, i
     return NV_OK;
   };
   auto sort_lists = [&]() -> int32_t {
-    hipLaunchKernelGGL(iota_k, dim3((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)), dim3(256),
-                       0, s, vals, n);
-    NV_LAUNCH_CHECK("iota_k");
-    size_t sb = w.sort_bytes;
-    NV_HIP_TRY(hipcub::DeviceRadixSort::SortPairs(ws + w.sort_tmp, sb, (const int64_t*)lists,
-                                                  keys_sorted, (const int64_t*)vals, perm, (int)n,
-                                                  0, bits_for(L), s));
-    hipLaunchKernelGGL(offsets_k, dim3((unsigned)ceil_div(L + 1, 256)), dim3(256), 0, s,
-                       (const int64_t*)keys_sorted, n, L, offsets);
-    NV_LAUNCH_CHECK("offsets_k");
+    const int64_t R = sort_rows_per_block(n);
+    const int nb = (int)ceil_div(n, R);
+    int32_t* counts = (int32_t*)(ws + w.counts);
+    hipLaunchKernelGGL(list_count_k, dim3((unsigned)nb), dim3(256), 0, s, (const int64_t*)lists,
+                       n, L, R, counts);
+    NV_LAUNCH_CHECK("list_count_k");
+    hipLaunchKernelGGL(list_scan_k, dim3(1), dim3(1024), 0, s, counts, nb, L, offsets);
+    NV_LAUNCH_CHECK("list_scan_k");
+    hipLaunchKernelGGL(list_scatter_k, dim3((unsigned)nb), dim3(64), 0, s, (const int64_t*)lists,
+                       n, L, R, (const int32_t*)counts, perm);
+    NV_LAUNCH_CHECK("list_scatter_k");
     return NV_OK;
   };
   for (int it = 0; it < iters; ++it) {
