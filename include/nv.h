@@ -80,6 +80,26 @@ int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache, int3
                         int32_t J, int64_t* idx_out, float* sim_out, int32_t* k_out,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* Capacity of the scratch array behind nv_cache_lookup_static (64 MiB per GPU). */
+#define NV_LOOKUP_STATIC_BYTES ((size_t)64 << 20)
+
+/* nv_cache_lookup_static: nv_cache_lookup without a workspace, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  It allocates nothing: its
+ * scratch is a device array of NV_LOOKUP_STATIC_BYTES inside the library, one
+ * copy per GPU (the device current at the call), held until the process ends.
+ * Arguments, results and errors are those of nv_cache_lookup, plus
+ * NV_ERR_UNSUPPORTED (before any launch) when the lookup needs more scratch
+ * than the array holds; it needs at most nv_cache_lookup_workspace(m, n, d)
+ * bytes: with d = 768, 8 queries fit up to 85M rows and 256 queries up to
+ * 4.1M.  Every call on one GPU shares the array and leaves its scratch
+ * behind (the next call initialises what it reads): calls in stream order are
+ * safe, calls that overlap on one GPU (unordered streams) race. */
+int32_t nv_cache_lookup_static(const float* queries, int32_t m, const void* cache,
+                               int32_t c_dtype, int64_t n, int32_t d, const float* thresholds,
+                               const int32_t* k_values, int32_t J, int64_t* idx_out,
+                               float* sim_out, int32_t* k_out, void* stream);
+
 /* ------------------------------------------------------------------------ *
  * State fetch (Sec. 5.3 storage; Alg. 1 retrieval of the state after step K).
  *

@@ -13,6 +13,7 @@ LIB_PATH = os.environ.get("NV_LIB_PATH") or os.path.join(HERE, "libnv.so")
 NV_OK, NV_ERR_INVALID_ARG, NV_ERR_UNSUPPORTED = 0, -1, -2
 NV_ERR_OUT_OF_MEMORY, NV_ERR_HIP, NV_ERR_WORKSPACE = -3, -4, -5
 NV_F32, NV_BF16 = 0, 1
+NV_LOOKUP_STATIC_BYTES = 64 << 20
 NV_FAM_CONV, NV_FAM_LINEAR, NV_FAM_ATTN, NV_FAM_SCAN = 1, 2, 4, 8
 
 if not os.path.exists(LIB_PATH):
@@ -41,6 +42,7 @@ _sigs = {
     "nv_version": (C.c_char_p, []),
     "nv_cache_lookup_workspace": (SZ, [I32, I64, I32]),
     "nv_cache_lookup": (I32, [VP, I32, VP, I32, I64, I32, VP, VP, I32, VP, VP, VP, VP, SZ, VP]),
+    "nv_cache_lookup_static": (I32, [VP, I32, VP, I32, I64, I32, VP, VP, I32, VP, VP, VP, VP]),
     "nv_gather_states": (I32, [VP, I64, I32, VP, VP, I64, VP, VP, VP, I32, I64, VP, VP]),
     "nv_unet_param_count": (I64, [C.POINTER(nv_unet_config)]),
     "nv_unet_param_info": (I32, [C.POINTER(nv_unet_config), I64, C.c_char_p, I32,

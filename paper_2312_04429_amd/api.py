@@ -70,6 +70,35 @@ def nv_cache_lookup(queries, cache, thresholds, k_values, ws=None):
     return idx, sim, kk
 
 
+def nv_cache_lookup_static(queries, cache, thresholds, k_values, out=None):
+    """nv_cache_lookup on the library's own scratch (no workspace, no allocation by
+    the library).  out: optional (idx, sim, K) device tensors of m entries to fill."""
+    _need_cuda(queries, cache)
+    assert queries.dtype == torch.float32 and queries.is_contiguous()
+    assert cache.is_contiguous()
+    m, d = queries.shape
+    n = cache.shape[0]
+    if cache.dtype == torch.float32:
+        cdt = N.NV_F32
+    elif cache.dtype in BF16_DTYPES:
+        cdt = N.NV_BF16
+    else:
+        raise ValueError("cache must be float32 or bfloat16 (bits)")
+    thr = (C.c_float * len(thresholds))(*thresholds)
+    kv = (C.c_int32 * len(k_values))(*k_values)
+    dev = queries.device
+    if out is None:
+        out = (torch.empty(m, dtype=torch.int64, device=dev),
+               torch.empty(m, dtype=torch.float32, device=dev),
+               torch.empty(m, dtype=torch.int32, device=dev))
+    idx, sim, kk = out
+    st = N.lib.nv_cache_lookup_static(_p(queries), m, _p(cache) if n > 0 else None, cdt, n, d,
+                                      thr, kv, len(thresholds), _p(idx), _p(sim), _p(kk),
+                                      _stream())
+    N.check(st, "nv_cache_lookup_static")
+    return idx, sim, kk
+
+
 def nv_gather_states(store, slot_k, payload, n_rows, idx, k, noise, out=None):
     """store [n_store][n_slots][*latent] f32; returns out [B][*latent]; k rewritten in place."""
     _need_cuda(store, idx, k, noise)

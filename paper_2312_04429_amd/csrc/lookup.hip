@@ -21,6 +21,7 @@
 //      lowest index wins; its float32 rounding goes through the thresholds.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "trace.h"
@@ -762,12 +763,14 @@ extern "C" size_t nv_cache_lookup_workspace(int32_t m, int64_t n, int32_t d) {
   return rows_in_registers(d, true) ? std::max(wide, plan_ws(m, n, d, RR_TILE).total) : wide;
 }
 
-extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache,
-                                   int32_t c_dtype, int64_t n, int32_t d, const float* thresholds,
-                                   const int32_t* k_values, int32_t J, int64_t* idx_out,
-                                   float* sim_out, int32_t* k_out, void* workspace,
-                                   size_t workspace_bytes, void* stream) {
-  clear_error();
+namespace nv {
+namespace {
+
+// Argument checks of the lookup (before any launch); fills the threshold table.
+int32_t lookup_check(const float* queries, int32_t m, const void* cache, int32_t c_dtype,
+                     int64_t n, int32_t d, const float* thresholds, const int32_t* k_values,
+                     int32_t J, const int64_t* idx_out, const float* sim_out,
+                     const int32_t* k_out, Thresholds* th) {
   NV_CHECK_ARG(queries && idx_out && sim_out && k_out, "null query or output pointer");
   NV_CHECK_ARG(m >= 1 && m <= 4096, "m must be in [1, 4096]");
   NV_CHECK_ARG(n >= 0 && n < (int64_t(1) << 31), "n must be in [0, 2^31)");
@@ -775,30 +778,38 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
   NV_CHECK_ARG(c_dtype == NV_F32 || c_dtype == NV_BF16, "c_dtype must be NV_F32 or NV_BF16");
   NV_CHECK_ARG(n == 0 || cache, "null cache pointer with n > 0");
   NV_CHECK_ARG(thresholds && k_values && J >= 1 && J <= 16, "need 1..16 thresholds");
-  Thresholds th{};
-  th.J = J;
+  *th = Thresholds{};
+  th->J = J;
   for (int j = 0; j < J; ++j) {
     NV_CHECK_ARG(std::isfinite(thresholds[j]), "thresholds must be finite");
     NV_CHECK_ARG(j == 0 || thresholds[j] < thresholds[j - 1],
                  "thresholds must be strictly descending");
     NV_CHECK_ARG(k_values[j] >= 0, "k_values must be >= 0");
-    th.t[j] = thresholds[j];
-    th.k[j] = k_values[j];
+    th->t[j] = thresholds[j];
+    th->k[j] = k_values[j];
   }
   if (d % 8 != 0 || d > MAX_D) {
     set_error("d must be a multiple of 8 and at most 2048");
     return NV_ERR_UNSUPPORTED;
   }
+  return NV_OK;
+}
+
+// Bytes of scratch one lookup uses (its tile size follows the cache type and d).
+size_t lookup_scratch_bytes(int32_t m, int64_t n, int32_t d, int32_t c_dtype) {
+  const bool rr = rows_in_registers(d, c_dtype == NV_BF16);
+  return plan_ws(m, n, d, rr ? RR_TILE : TILE).total;
+}
+
+// The lookup's launches on checked arguments; w: at least lookup_scratch_bytes,
+// 256-byte aligned, any contents (every region is initialised by the kernels).
+int32_t lookup_run(const float* queries, int32_t m, const void* cache, int32_t c_dtype,
+                   int64_t n, int32_t d, const Thresholds& th, int64_t* idx_out,
+                   float* sim_out, int32_t* k_out, char* w, hipStream_t s) {
   const int bf = c_dtype == NV_BF16;
   const bool rr = rows_in_registers(d, bf);
   const int tr = rr ? RR_TILE : TILE;
   const WsPlan p = plan_ws(m, n, d, tr);
-  if (!workspace || workspace_bytes < p.total || ((uintptr_t)workspace & 255)) {
-    set_error("lookup workspace missing, misaligned or smaller than nv_cache_lookup_workspace()");
-    return NV_ERR_WORKSPACE;
-  }
-  hipStream_t s = (hipStream_t)stream;
-  char* w = (char*)workspace;
   const int mq_pad = (int)ceil_div(m, QB) * QB;
   const int dp = (int)align_up(d, 128);
   const int T = (int)ceil_div(n, (int64_t)tr);
@@ -856,6 +867,81 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
                      idx_out, sim_out, k_out);
   NV_LAUNCH_CHECK("lk_select");
   return NV_OK;
+}
+
+}  // namespace
+}  // namespace nv
+
+extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* cache,
+                                   int32_t c_dtype, int64_t n, int32_t d, const float* thresholds,
+                                   const int32_t* k_values, int32_t J, int64_t* idx_out,
+                                   float* sim_out, int32_t* k_out, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  clear_error();
+  Thresholds th;
+  const int32_t st = lookup_check(queries, m, cache, c_dtype, n, d, thresholds, k_values, J,
+                                  idx_out, sim_out, k_out, &th);
+  if (st != NV_OK) return st;
+  if (!workspace || workspace_bytes < lookup_scratch_bytes(m, n, d, c_dtype) ||
+      ((uintptr_t)workspace & 255)) {
+    set_error("lookup workspace missing, misaligned or smaller than nv_cache_lookup_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  return lookup_run(queries, m, cache, c_dtype, n, d, th, idx_out, sim_out, k_out,
+                    (char*)workspace, (hipStream_t)stream);
+}
+
+// ---------------------------------------------------------------------------
+// The lookup without a caller workspace, for callers that cannot allocate:
+// its scratch is the file-scope device array below, one copy per GPU, held
+// until the process ends.  Host code never uses the array's name as an
+// address: on a device's first call its address is taken with
+// hipGetSymbolAddress (that device current) and kept per device.
+namespace nv {
+namespace {
+__device__ __align__(256) unsigned char lookup_scratch[NV_LOOKUP_STATIC_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[MAX_DEVICES] = {};
+
+int32_t lookup_scratch_ptr(char** out) {
+  int dev = -1;
+  NV_HIP_TRY(hipGetDevice(&dev));
+  NV_CHECK_ARG(dev >= 0 && dev < MAX_DEVICES, "device ordinal beyond the library's table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    NV_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(lookup_scratch)));
+    NV_CHECK_ARG(p != nullptr && ((uintptr_t)p & 255) == 0, "scratch address not 256-byte aligned");
+    g_scratch[dev] = p;
+  }
+  *out = (char*)g_scratch[dev];
+  return NV_OK;
+}
+}  // namespace
+}  // namespace nv
+
+extern "C" int32_t nv_cache_lookup_static(const float* queries, int32_t m, const void* cache,
+                                          int32_t c_dtype, int64_t n, int32_t d,
+                                          const float* thresholds, const int32_t* k_values,
+                                          int32_t J, int64_t* idx_out, float* sim_out,
+                                          int32_t* k_out, void* stream) {
+  clear_error();
+  Thresholds th;
+  int32_t st = lookup_check(queries, m, cache, c_dtype, n, d, thresholds, k_values, J, idx_out,
+                            sim_out, k_out, &th);
+  if (st != NV_OK) return st;
+  if (lookup_scratch_bytes(m, n, d, c_dtype) > NV_LOOKUP_STATIC_BYTES) {
+    set_error("lookup needs more scratch than the library's static array "
+              "(nv_cache_lookup_workspace(m, n, d) > NV_LOOKUP_STATIC_BYTES)");
+    return NV_ERR_UNSUPPORTED;
+  }
+  char* w = nullptr;
+  st = lookup_scratch_ptr(&w);
+  if (st != NV_OK) return st;
+  return lookup_run(queries, m, cache, c_dtype, n, d, th, idx_out, sim_out, k_out, w,
+                    (hipStream_t)stream);
 }
 
 // ---------------------------------------------------------------------------

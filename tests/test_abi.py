@@ -139,3 +139,27 @@ def test_pool_entry_points_validate_before_launch():
                                      None, d, 1 << 30, None) == N.NV_ERR_INVALID_ARG
     assert lib.nv_denoise_store_pool(None, C.byref(s), d, k, 65, d, d, None, 7.5, d, 2, 2, sk,
                                      dst, d, 1 << 30, None) == N.NV_ERR_INVALID_ARG
+
+
+def test_static_lookup_validation_before_launch():
+    """nv_cache_lookup_static rejects bad arguments, and lookups needing more
+    scratch than its 64 MiB array, before touching a device."""
+    from paper_2312_04429_amd import _native as N
+    lib = N.lib
+    thr = (C.c_float * 2)(0.9, 0.75)
+    kv = (C.c_int32 * 2)(10, 5)
+    dummy = C.c_void_p(0x10000)
+
+    def call(q=dummy, m=4, n=100, d=64, dt=N.NV_BF16, J=2):
+        return lib.nv_cache_lookup_static(q, m, dummy, dt, n, d, thr, kv, J, dummy, dummy, dummy,
+                                          None)
+    assert call(q=None) == N.NV_ERR_INVALID_ARG
+    assert call(m=0) == N.NV_ERR_INVALID_ARG
+    assert call(J=0) == N.NV_ERR_INVALID_ARG
+    assert call(d=60) == N.NV_ERR_UNSUPPORTED
+    # 256 queries over 5M rows of 768 bf16 dims need about 80 MiB of scratch
+    assert lib.nv_cache_lookup_workspace(256, 5_000_000, 768) > N.NV_LOOKUP_STATIC_BYTES
+    assert call(m=256, n=5_000_000, d=768) == N.NV_ERR_UNSUPPORTED
+    # the limits quoted with the declaration
+    assert lib.nv_cache_lookup_workspace(8, 85_000_000, 768) <= N.NV_LOOKUP_STATIC_BYTES
+    assert lib.nv_cache_lookup_workspace(256, 4_100_000, 768) <= N.NV_LOOKUP_STATIC_BYTES
