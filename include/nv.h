@@ -480,6 +480,13 @@ int32_t nv_trace_enable(int32_t family_mask, int32_t max_launches);
 int32_t nv_trace_disable(void);
 int32_t nv_trace_read(int32_t family, int64_t* launches, double* ms, double* flops,
                       double* bytes);
+/* Record i (0-based, in launch order) of the current trace: its family, shape
+ * (HOST int64 [4]: for matrix products M, N, K and the tile code
+ * BM * 10000 + BN * 10 + splits; for attention S, L, heads * dh and
+ * dh * 10000 + QB * 1000 + KB; for scans m, n, d, 0), kernel time in ms
+ * (waits for the launch) and algorithmic FLOPs.  NV_ERR_INVALID_ARG when i is
+ * out of range. */
+int32_t nv_trace_get(int32_t i, int32_t* family, int64_t* shape, double* ms, double* flops);
 
 /* ------------------------------------------------------------------------ *
  * Matrix-core throughput probe (measurement support, not part of the path).

@@ -16,7 +16,8 @@ Importing the package loads libnv.so and fails if it has not been built.
 from .api import (NvIVF, NvLCBFU, NvUNet, nv_cache_insert, nv_cache_move_rows, nv_gather_pool,
                   nv_match_gate, nv_ocsvm_train, nv_table_update, nv_cache_lookup, nv_cache_lookup_static, nv_cache_lookup_workspace, nv_gather_states,
                   nv_op_attention, nv_op_conv3x3, nv_op_linear, nv_probe_peaks, nv_trace_disable,
-                  nv_trace_enable, nv_trace_read, nv_unet_param_count, nv_unet_param_info, workspace)
+                  nv_trace_enable, nv_trace_read, nv_trace_records, nv_unet_param_count,
+                  nv_unet_param_info, workspace)
 
 from ._native import NV_FAM_ATTN as FAM_ATTN, NV_FAM_CONV as FAM_CONV
 from ._native import NV_FAM_LINEAR as FAM_LINEAR, NV_FAM_SCAN as FAM_SCAN
@@ -25,4 +26,4 @@ __all__ = ["FAM_ATTN", "FAM_CONV", "FAM_LINEAR", "FAM_SCAN", "NvIVF", "NvLCBFU",
            "nv_cache_move_rows", "nv_gather_pool", "nv_match_gate", "nv_ocsvm_train",
            "nv_table_update", "nv_cache_insert", "nv_cache_lookup", "nv_cache_lookup_static", "nv_cache_lookup_workspace", "nv_gather_states",
            "nv_op_attention", "nv_op_conv3x3", "nv_op_linear", "nv_probe_peaks", "nv_trace_disable", "nv_trace_enable",
-           "nv_trace_read", "nv_unet_param_count", "nv_unet_param_info", "workspace"]
+           "nv_trace_read", "nv_trace_records", "nv_unet_param_count", "nv_unet_param_info", "workspace"]

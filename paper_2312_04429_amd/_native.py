@@ -78,6 +78,7 @@ _sigs = {
                           VP]),
     "nv_trace_enable": (I32, [I32, I32]),
     "nv_trace_disable": (I32, []),
+    "nv_trace_get": (I32, [I32, VP, VP, VP, VP]),
     "nv_trace_read": (I32, [I32, C.POINTER(I64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                             C.POINTER(C.c_double)]),
     "nv_probe_mfma": (I32, [I32, I32, I32, VP, VP]),

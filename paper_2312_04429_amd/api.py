@@ -512,6 +512,22 @@ def nv_trace_disable():
     N.lib.nv_trace_disable()
 
 
+def nv_trace_records():
+    """Every launch of the current trace: list of (family, (m, n, k, variant), ms, flops)."""
+    n = C.c_int64()
+    ms, fl, by = C.c_double(), C.c_double(), C.c_double()
+    N.check(N.lib.nv_trace_read(-1 & 0x7FFFFFFF, C.byref(n), C.byref(ms), C.byref(fl), C.byref(by)),
+            "nv_trace_read")
+    out = []
+    fam = C.c_int32()
+    shape = (C.c_int64 * 4)()
+    for i in range(n.value):
+        N.check(N.lib.nv_trace_get(i, C.byref(fam), shape, C.byref(ms), C.byref(fl)),
+                "nv_trace_get")
+        out.append((fam.value, tuple(shape), ms.value, fl.value))
+    return out
+
+
 def nv_trace_read(family):
     """(launches, ms, flops, bytes) summed over the recorded launches of `family`."""
     n = C.c_int64()

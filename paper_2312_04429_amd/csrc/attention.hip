@@ -328,7 +328,9 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(ceil_div(a.S, 64 * QB) * a.heads * a.rows));
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
-  const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes);
+  const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes,
+                                 TraceShape{a.S, a.L, (int64_t)a.heads * a.dh,
+                                            DH * 10000 + QB * 1000 + KB});
   hipExtLaunchKernelGGL((attn_f16<DH, QB, KB>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
                         a);
   return hipGetLastError();

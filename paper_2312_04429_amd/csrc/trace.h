@@ -10,5 +10,11 @@ namespace nv {
 struct TraceEv {
   hipEvent_t a = nullptr, b = nullptr;
 };
-TraceEv trace_begin(int family, double flops, double bytes);
+// Shape of a traced launch: matrix products (M, N, K, tile code BM*10000 +
+// BN*10 + splits), attention (S, L, heads*dh, head dim*10000 + QB*1000 + KB),
+// scans (m, n, d, 0).
+struct TraceShape {
+  int64_t m = 0, n = 0, k = 0, variant = 0;
+};
+TraceEv trace_begin(int family, double flops, double bytes, const TraceShape& shape = {});
 }  // namespace nv

@@ -14,6 +14,7 @@ struct Rec {
   hipEvent_t a, b;
   int family;
   double flops, bytes;
+  TraceShape shape;
 };
 
 struct Tracer {
@@ -26,12 +27,12 @@ struct Tracer {
 
 }  // namespace
 
-TraceEv trace_begin(int family, double flops, double bytes) {
+TraceEv trace_begin(int family, double flops, double bytes, const TraceShape& shape) {
   TraceEv ev;
   if (!(T.mask & family)) return ev;
   std::lock_guard<std::mutex> lk(T.mu);
   if (T.recs.size() >= T.cap) return ev;
-  Rec r{T.pool[2 * T.recs.size()], T.pool[2 * T.recs.size() + 1], family, flops, bytes};
+  Rec r{T.pool[2 * T.recs.size()], T.pool[2 * T.recs.size() + 1], family, flops, bytes, shape};
   T.recs.push_back(r);
   ev.a = r.a;
   ev.b = r.b;
@@ -85,5 +86,25 @@ extern "C" int32_t nv_trace_read(int32_t family, int64_t* launches, double* ms, 
   *ms = t;
   *flops = f;
   *bytes = b;
+  return NV_OK;
+}
+
+extern "C" int32_t nv_trace_get(int32_t i, int32_t* family, int64_t* shape, double* ms,
+                                double* flops) {
+  clear_error();
+  NV_CHECK_ARG(family && shape && ms && flops, "null output pointer");
+  std::lock_guard<std::mutex> lk(T.mu);
+  NV_CHECK_ARG(i >= 0 && (size_t)i < T.recs.size(), "record index out of range");
+  const Rec& r = T.recs[i];
+  NV_HIP_TRY(hipEventSynchronize(r.b));
+  float e = 0.f;
+  NV_HIP_TRY(hipEventElapsedTime(&e, r.a, r.b));
+  *family = r.family;
+  shape[0] = r.shape.m;
+  shape[1] = r.shape.n;
+  shape[2] = r.shape.k;
+  shape[3] = r.shape.variant;
+  *ms = e;
+  *flops = r.flops;
   return NV_OK;
 }
