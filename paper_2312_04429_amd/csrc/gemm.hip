@@ -538,8 +538,9 @@ __device__ __forceinline__ void mma_tile(const _Float16* __restrict__ a,
   }
 }
 
-template <int MODE, int BM, int BN, int STAGES, bool LN>
+template <int MODE, int BM, int BN, int STAGES, bool LN, int U>
 __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
+  static_assert(U >= 1 && STAGES >= 2 * U, "ring must hold two groups of U tiles");
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 16, FN = WN / 16;
   constexpr int AJ = BM / 32, BJ = BN / 32;  // 8-row groups per wave per tile (A, B)
@@ -548,7 +549,8 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16* ring = (_Float16*)smem;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases in SGPRs
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 15, kc = lane >> 4;
   const int ntn = (g.N + BN - 1) / BN;
@@ -634,9 +636,16 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   auto issue = [&](int buf) {
     _Float16* A = ring + buf * TILE_H;
     _Float16* Bt = A + BM * 64;
-    const __amdgpu_buffer_rsrc_t rsa = t_first ? rs1 : rs2;
+    // the source is uniform: branch on it (made visibly uniform), so each
+    // descriptor stays in SGPRs (a selected one would sit in VGPRs and need a
+    // readfirstlane loop around every load)
+    if (__builtin_amdgcn_readfirstlane((int)t_first) != 0) {
 #pragma unroll
-    for (int j = 0; j < AJ; ++j) lds_dma16(rsa, aoff[j], A + (j * 4 + wave) * 512);
+      for (int j = 0; j < AJ; ++j) lds_dma16(rs1, aoff[j], A + (j * 4 + wave) * 512);
+    } else {
+#pragma unroll
+      for (int j = 0; j < AJ; ++j) lds_dma16(rs2, aoff[j], A + (j * 4 + wave) * 512);
+    }
 #pragma unroll
     for (int j = 0; j < BJ; ++j) lds_dma16(rsw, boff[j], Bt + (j * 4 + wave) * 512);
     t_k0 += 64;
@@ -669,11 +678,12 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // Prologue: tiles kt0 .. kt0 + STAGES - 2.  Requests past kt1 fetch tiles
-  // that are never multiplied (in range or zero-filled), which keeps the
-  // per-wave count of loads in flight fixed for the waits below.
+  // Prologue: tiles kt0 .. kt0 + STAGES - U - 1.  Requests past kt1 fetch
+  // tiles that are never multiplied (in range or zero-filled), which keeps the
+  // per-wave count of loads in flight fixed for the waits below.  Each pass of
+  // the main loop multiplies U tiles behind one barrier.
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) issue(s);
+  for (int s = 0; s < STAGES - U; ++s) issue(s);
   // Folded LayerNorm: TPR threads per A row each sum CPT of the row's eight
   // 16-byte chunks per k tile, shifted by the row's first value (k = 0, in
   // chunk slot r & 7) so that the one-pass variance does not cancel: the
@@ -683,15 +693,20 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   half2v st_shift = {(_Float16)0.f, (_Float16)0.f};
   const half2v st_one = {(_Float16)1.f, (_Float16)1.f};
   float st_s1 = 0.f, st_s2 = 0.f;
-  for (int kt = kt0; kt < kt1; ++kt) {
-    wait_vmcnt<(STAGES - 2) * OPS>();  // this wave's loads of tile kt have landed
-    ring_barrier();                    // everyone's have; buffer (kt - 1) is free
-    issue((kt - kt0 + STAGES - 1) % STAGES);
-    const _Float16* A = ring + ((kt - kt0) % STAGES) * TILE_H;
+  for (int kt = kt0; kt < kt1; kt += U) {
+    wait_vmcnt<(STAGES - 2 * U) * OPS>();  // this wave's loads of tiles kt .. kt+U-1 have landed
+    ring_barrier();                        // everyone's have; the previous U buffers are free
+#pragma unroll
+    for (int u = 0; u < U; ++u) issue((kt - kt0 + STAGES - U + u) % STAGES);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+    const int ktu = kt + u;
+    if (U > 1 && ktu >= kt1) break;
+    const _Float16* A = ring + ((ktu - kt0) % STAGES) * TILE_H;
     mma_tile<FM, FN>(A, A + BM * 64, wm * WM, wn * WN, li, kc, acc);
     if (LN) {
       const _Float16* ar = A + st_row * 64;
-      if (kt == 0) st_shift = half2v{ar[(st_row & 7) * 8], ar[(st_row & 7) * 8]};
+      if (ktu == 0) st_shift = half2v{ar[(st_row & 7) * 8], ar[(st_row & 7) * 8]};
 #pragma unroll
       for (int c = 0; c < CPT; ++c) {
         const half8 h = *(const half8*)(ar + (st_slot + c) * 8);
@@ -702,6 +717,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
           st_s2 = __builtin_amdgcn_fdot2(d, d, st_s2, false);
         }
       }
+    }
     }
   }
   wait_vmcnt<0>();  // drain the requests past the last tile before the workgroup ends
@@ -861,12 +877,15 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   const int nk = (g.K + BK - 1) / BK;
   const int kps = (nk + splits - 1) / splits;
   splits = (nk + kps - 1) / kps;
+  if (splits > 1 && (!g.partial || (size_t)splits * g.M * g.N * 4 > g.partial_bytes))
+    return hipErrorInvalidValue;  // split-K partials must fit the scratch
   dim3 grid((unsigned)(ceil_div(g.M, BM) * ceil_div(g.N, BN)), 1, (unsigned)splits);
   const int fam = MODE == 1 ? NV_FAM_CONV : NV_FAM_LINEAR;
   const double flops = 2.0 * (double)g.M * g.N * g.K;
   const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
-  const TraceEv ev = trace_begin(fam, flops, bytes);
+  const TraceEv ev =
+      trace_begin(fam, flops, bytes, TraceShape{g.M, g.N, g.K, BM * 10000 + BN * 10 + splits});
   hipExtLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), (uint32_t)lds, s, ev.a,
                         ev.b, 0u, g, kps);
   if (splits > 1) {
@@ -877,7 +896,7 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int MODE, int BM, int BN, int STAGES, bool LN>
+template <int MODE, int BM, int BN, int STAGES, bool LN, int U = 1>
 hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
       (int64_t)g.N * g.ldw * 2 >= 0x80000000ll)
@@ -885,7 +904,7 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   const size_t lds = (size_t)STAGES * (BM + BN) * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES, LN>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES, LN, U>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -893,13 +912,16 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   const int nk = g.K / 64;
   const int kps = (nk + splits - 1) / splits;
   splits = (nk + kps - 1) / kps;
+  if (splits > 1 && (!g.partial || (size_t)splits * g.M * g.N * 4 > g.partial_bytes))
+    return hipErrorInvalidValue;  // split-K partials must fit the scratch
   dim3 grid((unsigned)(ceil_div(g.M, BM) * ceil_div(g.N, BN)), 1, (unsigned)splits);
   const int fam = MODE == 1 ? NV_FAM_CONV : NV_FAM_LINEAR;
   const double flops = 2.0 * (double)g.M * g.N * g.K;
   const double bytes = (double)g.bytes1 + g.bytes2 + (double)g.N * g.K * 2 +
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
-  const TraceEv ev = trace_begin(fam, flops, bytes);
-  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN>), grid, dim3(256), (uint32_t)lds, s,
+  const TraceEv ev =
+      trace_begin(fam, flops, bytes, TraceShape{g.M, g.N, g.K, BM * 10000 + BN * 10 + splits});
+  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN, U>), grid, dim3(256), (uint32_t)lds, s,
                         ev.a, ev.b, 0u, g, kps);
   if (splits > 1) {
     const int64_t total = g.M * (int64_t)(g.N / 4);
@@ -910,11 +932,11 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
 }
 
 // A folded LayerNorm needs every k tile of a row in one workgroup: no split.
-template <int MODE, int BM, int BN, int STAGES>
+template <int MODE, int BM, int BN, int STAGES, int U = 1>
 hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
   if constexpr (MODE == 0)
-    if (g.ln_c1) return launch_s_t<0, BM, BN, STAGES, true>(g, 1, s);
-  return launch_s_t<MODE, BM, BN, STAGES, false>(g, splits, s);
+    if (g.ln_c1) return launch_s_t<0, BM, BN, STAGES, true, U>(g, 1, s);
+  return launch_s_t<MODE, BM, BN, STAGES, false, U>(g, splits, s);
 }
 
 // Streamed kernel when every 64-deep k tile lies inside one source and tap.
