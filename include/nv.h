@@ -416,6 +416,18 @@ int32_t nv_denoise_store_pool(nv_unet* net, const nv_schedule* sched, float* lat
                               const int32_t* slot_k, const int32_t* dst, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/* How the denoise entry points enqueue their steps.  By default each step (the
+ * UNet on the active rows, guidance, the DDIM update) is captured once into a
+ * HIP graph per active row count and replayed: the same kernels in the same
+ * order, at about half the dispatch cost per kernel.  The captured graphs
+ * belong to the handle and are rebuilt when the workspace, the batch size, the
+ * guidance, eta, the noise pointer or N change between calls; while launch
+ * tracing is on, steps are launched kernel by kernel.  enable = 0 launches
+ * every kernel directly (results are bit-identical either way).  Not
+ * thread-safe with concurrent calls on the handle.  NV_ERR_INVALID_ARG for a
+ * null handle. */
+int32_t nv_unet_set_graphs(nv_unet* net, int32_t enable);
+
 /* One UNet evaluation per row for teacher-forced checks: sample b at step
  * index step_idx[b] (HOST int32 [B], 0 <= step_idx < N, timestep t_i of the
  * grid) gives eps_uncond[b], eps_cond[b] (device f32 [B][out_ch][H][W]). */

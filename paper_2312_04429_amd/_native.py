@@ -74,6 +74,7 @@ _sigs = {
     "nv_lcbfu_insert": (I32, [VP, I32, VP, VP, VP, VP, VP, VP, VP, VP]),
     "nv_lcbfu_info": (I32, [VP, VP]),
     "nv_lcbfu_export": (I32, [VP, VP, VP, VP]),
+    "nv_unet_set_graphs": (I32, [VP, I32]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
     "nv_trace_enable": (I32, [I32, I32]),

@@ -349,6 +349,10 @@ class NvUNet:
         except Exception:
             pass
 
+    def set_graphs(self, enable):
+        """Replay denoise steps from captured HIP graphs (default) or launch every kernel."""
+        N.check(N.lib.nv_unet_set_graphs(self._h, int(bool(enable))), "nv_unet_set_graphs")
+
     def workspace_bytes(self, B):
         n = int(N.lib.nv_denoise_workspace(self._h, B))
         if n == 0:

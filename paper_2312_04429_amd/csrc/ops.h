@@ -8,13 +8,17 @@ namespace nv {
 
 constexpr int MAX_SAMPLES = 64;
 
-// Per-iteration sampler state passed by value: sample b (in the batch's
-// K-ascending order) is at grid step kstep[b] + j; perm maps that order back
-// to the caller's sample index.
+// Sampler state of a call: sample b (in the batch's K-ascending order) starts
+// at grid step kstep[b]; perm maps that order back to the caller's sample
+// index.  The kernels of a step read the current grid step of sample b from
+// dev[b] and its caller index from dev[MAX_SAMPLES + b] (device memory, so a
+// captured step replays unchanged): steps_init_launch fills dev from kstep
+// and perm at the start of a call, steps_advance_launch moves every sample on
+// by one grid step after each step.
 struct StepArgs {
   int32_t kstep[MAX_SAMPLES];
   int32_t perm[MAX_SAMPLES];
-  int32_t j;
+  int32_t* dev;  // device int32 [2][MAX_SAMPLES]
 };
 
 struct GnArgs {
@@ -48,5 +52,7 @@ hipError_t ctx_rows_launch(const StepArgs& st, const float* cond, const float* u
                            int64_t per_sample, int rows, _Float16* out, hipStream_t s);
 hipError_t permute_launch(const StepArgs& st, const float* src, float* dst, int64_t per_sample,
                           int samples, int to_sorted, hipStream_t s);
+hipError_t steps_init_launch(const StepArgs& st, hipStream_t s);
+hipError_t steps_advance_launch(int32_t* dev, hipStream_t s);
 
 }  // namespace nv

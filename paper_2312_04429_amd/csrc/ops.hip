@@ -313,13 +313,13 @@ __global__ void schedule_k(int T, int N, double b0, double b1, int32_t* ts, floa
 }
 
 // Sinusoidal embedding [cos(t f_k), sin(t f_k)] of the timestep of each row.
-// Rows 2b, 2b+1 belong to sample b at grid step kstep[b] + j.
-__global__ void temb_sin_k(StepArgs st, const int32_t* __restrict__ ts, int C0, int rows,
-                           _Float16* __restrict__ out) {
+// Rows 2b, 2b+1 belong to sample b at grid step step[b].
+__global__ void temb_sin_k(const int32_t* __restrict__ step, const int32_t* __restrict__ ts, int C0,
+                           int rows, _Float16* __restrict__ out) {
   const int r = blockIdx.x;
   if (r >= rows) return;
   const int b = r >> 1;
-  const float t = (float)ts[st.kstep[b] + st.j];
+  const float t = (float)ts[step[b]];
   const int half = C0 / 2;
   for (int k = threadIdx.x; k < half; k += blockDim.x) {
     const float f = expf(-logf(10000.0f) * (float)k / (float)half);
@@ -376,7 +376,8 @@ __global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
 // samplers; eta = 0 without z is the deterministic update).  z: the caller's
 // standard normal draws [samples][N][C][HW], indexed by the caller's sample
 // order and the grid step, or null.
-__global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __restrict__ eps,
+__global__ void __launch_bounds__(256) cfg_ddim_k(const int32_t* __restrict__ dev,
+                                                  const float* __restrict__ eps,
                                                   float* __restrict__ x, int C, int HW,
                                                   int samples, float guidance,
                                                   const float* __restrict__ a_t,
@@ -388,7 +389,7 @@ __global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __re
   const int b = (int)(i / ((int64_t)C * HW));
   const int rem = (int)(i % ((int64_t)C * HW));
   const int c = rem / HW, p = rem % HW;
-  const int step = st.kstep[b] + st.j;
+  const int step = dev[b];
   const float at = a_t[step], ap = a_prev[step];
   const float eu = eps[((int64_t)(2 * b) * HW + p) * C + c];
   const float ec = eps[((int64_t)(2 * b + 1) * HW + p) * C + c];
@@ -399,10 +400,26 @@ __global__ void __launch_bounds__(256) cfg_ddim_k(StepArgs st, const float* __re
   float sigma = 0.0f, zv = 0.0f;
   if (z) {
     sigma = eta * sqrtf((1.0f - ap) / (1.0f - at)) * sqrtf(1.0f - at / ap);
-    zv = z[((int64_t)st.perm[b] * N + step) * ((int64_t)C * HW) + rem];
+    zv = z[((int64_t)dev[MAX_SAMPLES + b] * N + step) * ((int64_t)C * HW) + rem];
   }
   const float v = sqrtf(ap) * x0 + sqrtf(fmaxf(1.0f - ap - sigma * sigma, 0.0f)) * e;
   x[i] = v + sigma * zv;
+}
+
+// dev[b] = kstep[b], dev[MAX_SAMPLES + b] = perm[b] (start of a call).
+__global__ void steps_init_k(StepArgs st) {
+  const int b = threadIdx.x;
+  if (b < MAX_SAMPLES) {
+    st.dev[b] = st.kstep[b];
+    st.dev[MAX_SAMPLES + b] = st.perm[b];
+  }
+}
+
+// Every sample one grid step on (end of a step; samples past the active
+// prefix are never read again).
+__global__ void steps_advance_k(int32_t* dev) {
+  const int b = threadIdx.x;
+  if (b < MAX_SAMPLES) dev[b] += 1;
 }
 
 // eps rows [rows][HW][C] float32 -> eps_u / eps_c [samples][C][HW].
@@ -715,7 +732,8 @@ hipError_t schedule_launch(int T, int N, double b0, double b1, int32_t* ts, floa
 
 hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int rows, _Float16* out,
                            hipStream_t s) {
-  hipLaunchKernelGGL(temb_sin_k, dim3(rows), dim3(128), 0, s, st, ts, C0, rows, out);
+  hipLaunchKernelGGL(temb_sin_k, dim3(rows), dim3(128), 0, s, (const int32_t*)st.dev, ts, C0, rows,
+                     out);
   return hipGetLastError();
 }
 
@@ -750,8 +768,9 @@ hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C
                            int samples, float guidance, const float* a_t, const float* a_prev,
                            float eta, const float* z, int N, hipStream_t s) {
   const int64_t total = (int64_t)samples * C * HW;
-  hipLaunchKernelGGL(cfg_ddim_k, dim3(blocks_for(total)), dim3(256), 0, s, st, eps, x, C, HW,
-                     samples, guidance, a_t, a_prev, eta, z, N);
+  hipLaunchKernelGGL(cfg_ddim_k, dim3(blocks_for(total)), dim3(256), 0, s,
+                     (const int32_t*)st.dev, eps, x, C, HW, samples, guidance, a_t, a_prev, eta, z,
+                     N);
   return hipGetLastError();
 }
 
@@ -767,6 +786,16 @@ hipError_t ctx_rows_launch(const StepArgs& st, const float* cond, const float* u
                            int64_t per_sample, int rows, _Float16* out, hipStream_t s) {
   hipLaunchKernelGGL(ctx_rows_k, dim3(blocks_for(rows * per_sample)), dim3(256), 0, s, st, cond,
                      uncond, per_sample, rows, out);
+  return hipGetLastError();
+}
+
+hipError_t steps_init_launch(const StepArgs& st, hipStream_t s) {
+  hipLaunchKernelGGL(steps_init_k, dim3(1), dim3(MAX_SAMPLES), 0, s, st);
+  return hipGetLastError();
+}
+
+hipError_t steps_advance_launch(int32_t* dev, hipStream_t s) {
+  hipLaunchKernelGGL(steps_advance_k, dim3(1), dim3(MAX_SAMPLES), 0, s, dev);
   return hipGetLastError();
 }
 

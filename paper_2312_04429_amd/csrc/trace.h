@@ -17,4 +17,7 @@ struct TraceShape {
   int64_t m = 0, n = 0, k = 0, variant = 0;
 };
 TraceEv trace_begin(int family, double flops, double bytes, const TraceShape& shape = {});
+// True while some family is being traced (launches then carry events and are
+// not captured into graphs).
+bool trace_active();
 }  // namespace nv

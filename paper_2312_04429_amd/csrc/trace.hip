@@ -39,6 +39,11 @@ TraceEv trace_begin(int family, double flops, double bytes, const TraceShape& sh
   return ev;
 }
 
+bool trace_active() {
+  std::lock_guard<std::mutex> lk(T.mu);
+  return T.mask != 0;
+}
+
 }  // namespace nv
 
 using namespace nv;

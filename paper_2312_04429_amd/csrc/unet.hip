@@ -25,6 +25,7 @@
 #include "common.h"
 #include "gemm.h"
 #include "ops.h"
+#include "trace.h"
 
 namespace nv {
 
@@ -289,6 +290,21 @@ struct Plan {
   // fixed regions
   size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0;
   size_t gnpart = 0, splitk = 0;
+  size_t stepdev = 0;  // int32 [2][MAX_SAMPLES]: current grid step and caller index per sample
+};
+
+// What a captured denoise step depends on besides the active rows: the plan
+// (its buffer offsets), the workspace and the update's constants.
+struct GraphKey {
+  const Plan* plan = nullptr;
+  const char* ws = nullptr;
+  float guidance = 0.f, eta = 0.f;
+  const float* z = nullptr;
+  int N = 0;
+  bool operator==(const GraphKey& o) const {
+    return plan == o.plan && ws == o.ws && guidance == o.guidance && eta == o.eta && z == o.z &&
+           N == o.N;
+  }
 };
 
 }  // namespace
@@ -304,6 +320,17 @@ struct nv_unet {
   int temb_total = 0;                       // sum of ResBlock widths
   std::map<std::string, int> temb_off;      // ResBlock name -> column offset
   std::map<int, std::unique_ptr<nv::Plan>> plans;
+  // Captured denoise steps (HIP graphs), one per active row count, valid for
+  // gkey; replaying one costs about half the dispatch time of launching its
+  // kernels one by one.
+  bool use_graphs = true;
+  hipStream_t capture_stream = nullptr;
+  nv::GraphKey gkey;
+  std::map<int, hipGraphExec_t> graphs;
+  void drop_graphs() {
+    for (auto& kv : graphs) (void)hipGraphExecDestroy(kv.second);
+    graphs.clear();
+  }
 };
 
 namespace nv {
@@ -708,6 +735,7 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
   int maxG = c.gn_groups;
   P->gnpart = B.fixed((size_t)Rmax * ceil_div(HW0, 8) * maxG * 2 * 4);
   P->splitk = B.fixed(SPLITK_BYTES);
+  P->stepdev = B.fixed((size_t)2 * MAX_SAMPLES * 4);
   // per-call context K|V regions, one per transformer block
   std::map<std::string, size_t> kv_regions;
   std::map<std::string, int> kv_width;
@@ -1195,6 +1223,8 @@ extern "C" int32_t nv_unet_create(const nv_unet_config* cfg, const float* weight
 
 extern "C" void nv_unet_destroy(nv_unet* net) {
   if (!net) return;
+  net->drop_graphs();
+  if (net->capture_stream) (void)hipStreamDestroy(net->capture_stream);
   if (net->d16) (void)hipFree(net->d16);
   if (net->d32) (void)hipFree(net->d32);
   delete net;
@@ -1276,11 +1306,13 @@ static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* laten
   }
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
+  sa.dev = (int32_t*)(ws + P->stepdev);
   const int HW = c.H * c.W;
   const int64_t lat = (int64_t)c.in_ch * HW;
   NV_HIP_TRY(schedule_launch(sched->T, N, sched->beta_start, sched->beta_end,
                              (int32_t*)(ws + P->ts), (float*)(ws + P->at), (float*)(ws + P->ap),
                              s));
+  NV_HIP_TRY(steps_init_launch(sa, s));
   NV_HIP_TRY(permute_launch(sa, latent, (float*)(ws + P->x_work), lat, B, 1, s));
   NV_HIP_TRY(ctx_rows_launch(sa, cond, uncond, (int64_t)c.ctx_len * c.ctx_dim, 2 * B,
                              (_Float16*)(ws + P->ctx), s));
@@ -1304,17 +1336,64 @@ static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* laten
   };
   for (int a = 0; a < B; ++a) NV_HIP_TRY(take(a, sa.kstep[a]));  // the states given
   NV_HIP_TRY(run_ops(P->pre, rc));
+  // One step for the first A samples: the UNet on their 2A rows, guidance and
+  // the DDIM update, then every sample's grid step moves on.  Enqueued on
+  // stream `on`.
+  const float eta = sto ? sto->eta : 0.0f;
+  const float* z = sto ? sto->z : nullptr;
+  auto step_ops = [&](int A, hipStream_t on) -> hipError_t {
+    RunCtx r = rc;
+    r.R = 2 * A;
+    r.s = on;
+    hipError_t e = run_ops(P->step, r);
+    if (e == hipSuccess)
+      e = cfg_ddim_launch(r.st, (const float*)(ws + P->eps), (float*)(ws + P->x_work), c.out_ch,
+                          HW, A, guidance, (const float*)(ws + P->at), (const float*)(ws + P->ap),
+                          eta, z, N, on);
+    if (e == hipSuccess) e = steps_advance_launch(sa.dev, on);
+    return e;
+  };
+  // Replayed from a graph captured on first use (per active row count, for
+  // this plan, workspace and update), unless launches are being traced.
+  const GraphKey key{P, ws, guidance, eta, z, N};
+  const bool graphs = net->use_graphs && !trace_active();
+  if (graphs && !(key == net->gkey)) {
+    net->drop_graphs();
+    net->gkey = key;
+  }
+  auto graph_for = [&](int A) -> hipGraphExec_t {
+    auto it = net->graphs.find(A);
+    if (it != net->graphs.end()) return it->second;
+    if (!net->capture_stream &&
+        hipStreamCreateWithFlags(&net->capture_stream, hipStreamNonBlocking) != hipSuccess)
+      return nullptr;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ex = nullptr;
+    if (hipStreamBeginCapture(net->capture_stream, hipStreamCaptureModeRelaxed) != hipSuccess)
+      return nullptr;
+    const hipError_t e = step_ops(A, net->capture_stream);
+    const hipError_t ee = hipStreamEndCapture(net->capture_stream, &g);
+    if (e == hipSuccess && ee == hipSuccess && g &&
+        hipGraphInstantiate(&ex, g, nullptr, nullptr, 0) == hipSuccess) {
+      net->graphs[A] = ex;
+    } else {
+      ex = nullptr;
+    }
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();  // a failed capture leaves no sticky error behind
+    return ex;
+  };
   for (int j = 0;; ++j) {
     int A = 0;
     while (A < B && sa.kstep[A] + j < N) ++A;
     if (A == 0) break;
-    rc.R = 2 * A;
-    rc.st.j = j;
-    NV_HIP_TRY(run_ops(P->step, rc));
-    NV_HIP_TRY(cfg_ddim_launch(rc.st, (const float*)(ws + P->eps), (float*)(ws + P->x_work),
-                               c.out_ch, HW, A, guidance, (const float*)(ws + P->at),
-                               (const float*)(ws + P->ap), sto ? sto->eta : 0.0f,
-                               sto ? sto->z : nullptr, N, s));
+    hipGraphExec_t ex = graphs && net->use_graphs ? graph_for(A) : nullptr;
+    if (ex) {
+      NV_HIP_TRY(hipGraphLaunch(ex, s));
+    } else {
+      if (graphs) net->use_graphs = false;  // capture failed: launch eagerly from now on
+      NV_HIP_TRY(step_ops(A, s));
+    }
     for (int a = 0; a < A; ++a) NV_HIP_TRY(take(a, sa.kstep[a] + j + 1));
   }
   NV_HIP_TRY(permute_launch(sa, (const float*)(ws + P->x_work), latent, lat, B, 0, s));
@@ -1432,9 +1511,11 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
   }
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
+  sa.dev = (int32_t*)(ws + P->stepdev);
   NV_HIP_TRY(schedule_launch(sched->T, sched->N, sched->beta_start, sched->beta_end,
                              (int32_t*)(ws + P->ts), (float*)(ws + P->at), (float*)(ws + P->ap),
                              s));
+  NV_HIP_TRY(steps_init_launch(sa, s));
   NV_HIP_TRY(ctx_rows_launch(sa, cond, uncond, (int64_t)c.ctx_len * c.ctx_dim, 2 * B,
                              (_Float16*)(ws + P->ctx), s));
   if (c.pooled_dim > 0)
@@ -1444,6 +1525,15 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
   NV_HIP_TRY(run_ops(P->step, rc));
   NV_HIP_TRY(eps_split_launch((const float*)(ws + P->eps), c.out_ch, c.H * c.W, B, eps_uncond,
                               eps_cond, s));
+  return NV_OK;
+}
+
+extern "C" int32_t nv_unet_set_graphs(nv_unet* net, int32_t enable) {
+  clear_error();
+  NV_CHECK_ARG(net, "null handle");
+  net->use_graphs = enable != 0;
+  net->drop_graphs();
+  net->gkey = GraphKey{};
   return NV_OK;
 }
 
