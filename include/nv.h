@@ -416,17 +416,20 @@ int32_t nv_denoise_store_pool(nv_unet* net, const nv_schedule* sched, float* lat
                               const int32_t* slot_k, const int32_t* dst, void* workspace,
                               size_t workspace_bytes, void* stream);
 
-/* How the denoise entry points enqueue their steps.  By default each step (the
- * UNet on the active rows, guidance, the DDIM update) is captured once into a
- * HIP graph per active row count and replayed: the same kernels in the same
- * order, at about half the dispatch cost per kernel.  The captured graphs
- * belong to the handle and are rebuilt when the workspace, the batch size, the
- * guidance, eta, the noise pointer or N change between calls; while launch
- * tracing is on, steps are launched kernel by kernel.  enable = 0 launches
- * every kernel directly (results are bit-identical either way).  Not
- * thread-safe with concurrent calls on the handle.  NV_ERR_INVALID_ARG for a
- * null handle. */
-int32_t nv_unet_set_graphs(nv_unet* net, int32_t enable);
+/* Execution options of a handle (flags, default NV_UNET_GRAPHS); the results
+ * are bit-identical under every setting.
+ *   NV_UNET_GRAPHS: the denoise entry points capture each step (the UNet on
+ *     the active rows, guidance, the DDIM update) once into a HIP graph per
+ *     active row count and replay it: the same kernels in the same order with
+ *     one host call per step instead of one per kernel.  The graphs belong to
+ *     the handle and are rebuilt when the workspace, the batch size, the
+ *     guidance, eta, the noise pointer or N change between calls; while launch
+ *     tracing is on, steps are launched kernel by kernel.
+ * Setting options drops the captured graphs.  Not thread-safe with
+ * concurrent calls on the handle.  NV_ERR_INVALID_ARG for a null handle or
+ * unknown flags. */
+enum { NV_UNET_GRAPHS = 1 };
+int32_t nv_unet_set_options(nv_unet* net, int32_t flags);
 
 /* One UNet evaluation per row for teacher-forced checks: sample b at step
  * index step_idx[b] (HOST int32 [B], 0 <= step_idx < N, timestep t_i of the

@@ -15,6 +15,7 @@ NV_ERR_OUT_OF_MEMORY, NV_ERR_HIP, NV_ERR_WORKSPACE = -3, -4, -5
 NV_F32, NV_BF16 = 0, 1
 NV_LOOKUP_STATIC_BYTES = 64 << 20
 NV_FAM_CONV, NV_FAM_LINEAR, NV_FAM_ATTN, NV_FAM_SCAN = 1, 2, 4, 8
+NV_UNET_GRAPHS = 1
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2312_04429_amd.build`")
@@ -74,7 +75,7 @@ _sigs = {
     "nv_lcbfu_insert": (I32, [VP, I32, VP, VP, VP, VP, VP, VP, VP, VP]),
     "nv_lcbfu_info": (I32, [VP, VP]),
     "nv_lcbfu_export": (I32, [VP, VP, VP, VP]),
-    "nv_unet_set_graphs": (I32, [VP, I32]),
+    "nv_unet_set_options": (I32, [VP, I32]),
     "nv_unet_eps": (I32, [VP, C.POINTER(nv_schedule), VP, VP, I32, VP, VP, VP, VP, VP, VP, SZ,
                           VP]),
     "nv_trace_enable": (I32, [I32, I32]),

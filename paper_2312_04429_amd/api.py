@@ -349,9 +349,11 @@ class NvUNet:
         except Exception:
             pass
 
-    def set_graphs(self, enable):
-        """Replay denoise steps from captured HIP graphs (default) or launch every kernel."""
-        N.check(N.lib.nv_unet_set_graphs(self._h, int(bool(enable))), "nv_unet_set_graphs")
+    def set_options(self, graphs=True):
+        """nv_unet_set_options: replay denoise steps from captured HIP graphs (default)
+        or launch every kernel from the host."""
+        N.check(N.lib.nv_unet_set_options(self._h, N.NV_UNET_GRAPHS if graphs else 0),
+                "nv_unet_set_options")
 
     def workspace_bytes(self, B):
         n = int(N.lib.nv_denoise_workspace(self._h, B))

@@ -1528,10 +1528,11 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
   return NV_OK;
 }
 
-extern "C" int32_t nv_unet_set_graphs(nv_unet* net, int32_t enable) {
+extern "C" int32_t nv_unet_set_options(nv_unet* net, int32_t flags) {
   clear_error();
   NV_CHECK_ARG(net, "null handle");
-  net->use_graphs = enable != 0;
+  NV_CHECK_ARG((flags & ~NV_UNET_GRAPHS) == 0, "unknown option flags");
+  net->use_graphs = (flags & NV_UNET_GRAPHS) != 0;
   net->drop_graphs();
   net->gkey = GraphKey{};
   return NV_OK;

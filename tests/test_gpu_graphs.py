@@ -1,5 +1,6 @@
 """Denoise steps replayed from captured HIP graphs against the same steps
-launched kernel by kernel (nv_unet_set_graphs(net, 0)): bit-identical x_0.
+launched kernel by kernel (nv_unet_set_options without NV_UNET_GRAPHS):
+bit-identical x_0.
 
 The replays run several times per handle with other GPU work and
 synchronisations between them, across calls that change the active row count
@@ -23,7 +24,7 @@ def t(a):
 
 
 def _run(net, x, ks, cond, unc, sched, graphs, guidance=7.5, eta=None, noise=None):
-    net.set_graphs(graphs)
+    net.set_options(graphs=graphs)
     lat = t(x.copy())
     if eta is None:
         net.nv_denoise(lat, ks, t(cond), t(unc), guidance=guidance, sched=sched)
@@ -74,7 +75,7 @@ def test_graph_replay_matches_eager_tiny():
     store_e = torch.zeros((5, 2, 4, cfg["H"], cfg["W"]), device="cuda")
     store_g = torch.zeros_like(store_e)
     for graphs, store in ((False, store_e), (True, store_g)):
-        net.set_graphs(graphs)
+        net.set_options(graphs=graphs)
         lat = t(x.copy())
         net.nv_denoise_store(lat, ks, t(cond), t(unc), store, [5, 10], [0, 1, 2, 3, 4],
                              sched=sched)
@@ -104,3 +105,4 @@ def test_graph_replay_matches_eager_sd15():
     np.testing.assert_array_equal(_run(net, x, [47, 45], cond, unc, sched, True), ref2)
     assert np.isfinite(ref2).all()
     net.close()
+
