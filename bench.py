@@ -32,7 +32,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="sd15_b1",
-                    help="sd15_b1 (default), sd15_b8_mixed, sdxl_b2, retrieval_heavy, "
+                    help="sd15_b1 (default), sd15_b8_mixed, sdxl_b2, retrieval_heavy, retrieval_gated, "
                          "sd15_lcbfu (a request stream through the LCBFU-maintained cache)")
     ap.add_argument("--k", type=int, default=None,
                     help="sd15_b1: place the query in this K's similarity band; "
@@ -54,6 +54,12 @@ def parse():
                     help="with --scan-only: also build an IVF index (L lists from seeded row "
                          "samples, ITERS Lloyd steps) and time its search at NPROBE probes, "
                          "with recall against the exact lookup")
+    ap.add_argument("--gate", type=float, default=None, metavar="P_FRESH",
+                    help="with --scan-only: replace this fraction of the queries with fresh "
+                         "draws (uniform on the sphere, far from every cached prompt), train "
+                         "the match predictor on sampled cache rows and time the lookup with "
+                         "the predictor in front (only predicted matches searched) beside the "
+                         "plain lookup over the same queries")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the event tracing of kernel launches (for counter passes)")
@@ -203,7 +209,8 @@ def build_lookup_inputs(wl, B, args, dev, torch, synth):
     """Cache, queries and the indices of the queries that feed the denoise."""
     n, d = wl["n_cache"], wl["d"]
     if n > 2_000_000:  # too large for the host generator: drawn on the device, same recipe
-        d_cache = synth.make_cache_device(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"], dev)
+        d_cache = synth.make_cache_device(n, d, wl["clusters"], wl["sigma"], wl["cache_seed"], dev,
+                                          cone=wl.get("cone", 0.0))
         cache = None
         rows_f32 = lambda r: synth.from_bf16_bits(
             d_cache[torch.from_numpy(np.asarray(r, dtype=np.int64)).to(dev)]
@@ -222,7 +229,8 @@ def build_lookup_inputs(wl, B, args, dev, torch, synth):
         planted = rng.choice(n, m // 2, replace=False)
         near = synth.make_queries_at_sims(rows_f32(planted), rng.uniform(0.95, 0.999, m // 2),
                                           wl["query_seed"])
-        mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev).cpu().numpy()
+        mu = synth.cluster_centres_device(wl["clusters"], d, wl["cache_seed"], dev,
+                                          wl.get("cone", 0.0)).cpu().numpy()
         far = synth.cluster_queries_from(mu, m - m // 2, wl["sigma"], wl["query_seed"] + 1)
         q = np.empty((m, d), dtype=np.float32)
         q[0::2], q[1::2] = near, far
@@ -362,6 +370,8 @@ def main():
         step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    # float16 activations have a finite range: the last step's x_0 must be finite
+    finite = bool(torch.isfinite(x).all().item())
     kern = trace_kernels(step, args, P, torch, B)
     ms = dt * 1e3 / args.steps
     ks_last = ks_seen[-1]
@@ -393,6 +403,7 @@ def main():
         "unet_steps_per_s": ups, "unet_step_ms": 1e3 / ups,
         "unet_step_tflop": fl_step / 1e12,
         "mfma_frac_whole_step": ups * fl_step / MFMA_PEAK_F16,
+        "x0_finite": finite,
         "kernels": kern,
     }
     add_roofline(out, kern, args, P, dev)
@@ -721,7 +732,66 @@ def scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
     out["hbm_frac_scan_kernel_of_measured"] = kby / (kms * 1e-3) / 1e9 / pk["hbm_read_gbps"]
     if args.ivf:
         out["ivf"] = ivf_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m)
+    if args.gate is not None:
+        out["gate"] = gate_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m)
     print(json.dumps(out))
+
+
+def gate_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):
+    """The lookup with the match predictor in front (Alg. 1, Sec. 5.2) on a query
+    batch where a fraction of the requests are fresh prompts: warm time of the
+    gated lookup (score, compact, search the predicted matches, scatter) against
+    the plain lookup over the same batch, the number searched, and how often the
+    gate turned away a query the lookup would have served (a false negative)."""
+    n, d = d_cache.shape
+    rng = np.random.default_rng(wl["query_seed"] + 11)
+    fresh = np.sort(rng.choice(m, int(round(args.gate * m)), replace=False))
+    q = d_q.clone()
+    if len(fresh):
+        q[torch.from_numpy(fresh).to(dev)] = torch.from_numpy(
+            synth_fresh(len(fresh), d, wl["query_seed"] + 12)).to(dev)
+    n_train = min(n, 200_000)
+    rows = torch.from_numpy(np.sort(rng.choice(n, n_train, replace=False))).to(dev)
+    host_rows = d_cache[rows].view(torch.int16).cpu().numpy().view(np.uint16)
+    print(f"[bench] training the match predictor on {n_train} cache rows",
+          file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    w, rho = P.nv_ocsvm_train(host_rows, 0.001, rng.permutation(2 * n_train) % n_train)
+    train_s = time.perf_counter() - t0
+    del host_rows
+    d_w = torch.from_numpy(w).to(dev)
+    gb = P.nv_cache_lookup_gated_workspace(m, n, d)
+    gown, gaddr = P.workspace(gb, dev)
+    gws = (gown, gaddr, gb)
+
+    def timed(fn):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            r = fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t1) * 1e3 / args.steps, r
+    plain_ms, (pi, _, pk) = timed(lambda: P.nv_cache_lookup(q, d_cache, thr, kv, ws=lws))
+    gated_ms, (gi, _, gk, _, searched) = timed(
+        lambda: P.nv_cache_lookup_gated(q, d_cache, thr, kv, d_w, rho, 0.0, ws=gws))
+    pi, pk, gi, gk = (a.cpu().numpy() for a in (pi, pk, gi, gk))
+    gated_out = gi < 0
+    agree = (gi == pi) & (gk == pk)
+    return {"fresh_fraction": args.gate, "queries": int(m), "searched": int(searched),
+            "nu": 0.001, "tau": 0.0, "train_rows": n_train, "train_s": train_s,
+            "plain_lookup_ms": plain_ms, "gated_lookup_ms": gated_ms,
+            "saved_ms": plain_ms - gated_ms,
+            "served_by_plain": int((pk > 0).sum()), "served_by_gated": int((gk > 0).sum()),
+            "false_negatives": int((gated_out & (pk > 0)).sum()),
+            "searched_queries_agree": bool(agree[~gated_out].all()),
+            "timing": "host wall clock per call (the gated call waits for its count)"}
+
+
+def synth_fresh(count, d, seed):
+    import synth
+    return synth.make_prompt_stream(count, d, seed, p_new=1.0)
 
 
 def ivf_leg(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, m):

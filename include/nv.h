@@ -291,6 +291,26 @@ int32_t nv_match_gate(const float* queries, int32_t m, int32_t d, const double* 
                       double tau, double* score_out, int64_t* idx, float* sim, int32_t* k,
                       void* stream);
 
+/* nv_cache_lookup_gated: Alg. 1 with the predictor in front of the search.
+ * Each query's decision value s = w.q - rho is computed as by nv_match_gate;
+ * the queries with s >= tau are compacted (ascending order) and searched by
+ * the exact lookup, the others get the "no suitable cache" result (idx -1,
+ * sim -inf, K 0) without touching the cache.  Arguments and results as
+ * nv_cache_lookup (idx_out, sim_out, k_out for every query) and
+ * nv_match_gate (w, rho, tau; score_out device float64 [m] or NULL), plus
+ * *n_searched (HOST) = the number of queries searched.  Synchronous on
+ * `stream` (that number sizes the search).  workspace >=
+ * nv_cache_lookup_gated_workspace(m, n, d), 256-byte aligned.  Errors: those
+ * of nv_cache_lookup, NV_ERR_INVALID_ARG for null w / n_searched, a
+ * non-finite rho or a NaN tau. */
+size_t nv_cache_lookup_gated_workspace(int32_t m, int64_t n, int32_t d);
+int32_t nv_cache_lookup_gated(const float* queries, int32_t m, const void* cache,
+                              int32_t c_dtype, int64_t n, int32_t d, const float* thresholds,
+                              const int32_t* k_values, int32_t J, const double* w, double rho,
+                              double tau, int64_t* idx_out, float* sim_out, int32_t* k_out,
+                              double* score_out, int32_t* n_searched, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ *
  * Latent-diffusion UNet (Sec. 2.1: UNet backbone, text conditioning through
  * cross-attention, operating on latents).  Topology rule:

@@ -67,6 +67,9 @@ _sigs = {
     "nv_ivf_search_workspace": (SZ, [I32, I32, I32, I64]),
     "nv_ivf_search": (I32, [VP, I32, I32, VP, I32, VP, I32, VP, VP, I64, I32, VP, VP, I32, VP,
                             VP, VP, VP, VP, SZ, VP]),
+    "nv_cache_lookup_gated_workspace": (SZ, [I32, I64, I32]),
+    "nv_cache_lookup_gated": (I32, [VP, I32, VP, I32, I64, I32, VP, VP, I32, VP, C.c_double,
+                                    C.c_double, VP, VP, VP, VP, VP, VP, SZ, VP]),
     "nv_ocsvm_train": (I32, [VP, I32, I64, I32, C.c_double, C.c_double, VP, I64, VP, VP]),
     "nv_match_gate": (I32, [VP, I32, I32, VP, C.c_double, C.c_double, VP, VP, VP, VP, VP]),
     "nv_lcbfu_create": (I32, [I32, VP, I64, I64, C.POINTER(VP)]),

@@ -247,6 +247,47 @@ def nv_match_gate(queries, w, rho, tau=0.0, idx=None, sim=None, k=None, score=Tr
     return out
 
 
+def nv_cache_lookup_gated(queries, cache, thresholds, k_values, w, rho, tau=0.0, ws=None):
+    """The lookup with the match predictor in front (Alg. 1): only queries with
+    w.q - rho >= tau are searched.  Returns (idx, sim, K, score) on the device and
+    the number of queries searched."""
+    _need_cuda(queries, cache, w)
+    assert queries.dtype == torch.float32 and queries.is_contiguous() and cache.is_contiguous()
+    assert w.dtype == torch.float64 and w.numel() == queries.shape[1]
+    m, d = queries.shape
+    n = cache.shape[0]
+    if cache.dtype == torch.float32:
+        cdt = N.NV_F32
+    elif cache.dtype in BF16_DTYPES:
+        cdt = N.NV_BF16
+    else:
+        raise ValueError("cache must be float32 or bfloat16 (bits)")
+    thr = (C.c_float * len(thresholds))(*thresholds)
+    kv = (C.c_int32 * len(k_values))(*k_values)
+    dev = queries.device
+    idx = torch.empty(m, dtype=torch.int64, device=dev)
+    sim = torch.empty(m, dtype=torch.float32, device=dev)
+    kk = torch.empty(m, dtype=torch.int32, device=dev)
+    score = torch.empty(m, dtype=torch.float64, device=dev)
+    need = int(N.lib.nv_cache_lookup_gated_workspace(m, n, d))
+    if ws is None:
+        _own, addr = workspace(need, dev)
+        wbytes = need
+    else:
+        _own, addr, wbytes = ws
+    searched = C.c_int32()
+    st = N.lib.nv_cache_lookup_gated(_p(queries), m, _p(cache) if n > 0 else None, cdt, n, d, thr,
+                                     kv, len(thresholds), _p(w), float(rho), float(tau), _p(idx),
+                                     _p(sim), _p(kk), _p(score), C.byref(searched),
+                                     C.c_void_p(addr), wbytes, _stream())
+    N.check(st, "nv_cache_lookup_gated")
+    return idx, sim, kk, score, searched.value
+
+
+def nv_cache_lookup_gated_workspace(m, n, d):
+    return int(N.lib.nv_cache_lookup_gated_workspace(m, n, d))
+
+
 class NvLCBFU:
     """Host LCBFU maintainer (native); arrays in and out are host numpy arrays."""
 

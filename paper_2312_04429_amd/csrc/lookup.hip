@@ -892,6 +892,167 @@ extern "C" int32_t nv_cache_lookup(const float* queries, int32_t m, const void* 
 }
 
 // ---------------------------------------------------------------------------
+// Alg. 1 with the match predictor in front of the search (Sec. 5.2): the
+// decision values come first (nv_match_gate); the queries predicted to match
+// are compacted into a contiguous block and only they are searched; the others
+// get the "no suitable cache" result without touching the cache.
+namespace nv {
+namespace {
+constexpr int GATE_T = 1024;
+
+// One workgroup; thread t owns queries [t*per, (t+1)*per), per = ceil(m / GATE_T):
+// list[0 .. count) = the queries with score >= tau in ascending order (an
+// exclusive prefix sum over the threads' counts gives each its first slot);
+// every other query gets idx -1, sim -inf, K 0.
+__global__ void __launch_bounds__(GATE_T) gate_compact_k(const double* __restrict__ score, int m,
+                                                         double tau, int32_t* __restrict__ list,
+                                                         int32_t* __restrict__ count,
+                                                         int64_t* __restrict__ idx,
+                                                         float* __restrict__ sim,
+                                                         int32_t* __restrict__ kk) {
+  __shared__ int32_t sc[GATE_T];
+  const int t = threadIdx.x;
+  const int per = (m + GATE_T - 1) / GATE_T;
+  const int j0 = t * per;
+  int c = 0;
+  for (int u = 0; u < per; ++u) {
+    const int j = j0 + u;
+    if (j < m && score[j] >= tau) ++c;
+  }
+  sc[t] = c;
+  __syncthreads();
+  for (int o = 1; o < GATE_T; o <<= 1) {  // inclusive scan (integers: any order is exact)
+    const int v = t >= o ? sc[t - o] : 0;
+    __syncthreads();
+    sc[t] += v;
+    __syncthreads();
+  }
+  int at = sc[t] - c;
+  for (int u = 0; u < per; ++u) {
+    const int j = j0 + u;
+    if (j >= m) break;
+    if (score[j] >= tau) {
+      list[at++] = j;
+    } else {
+      idx[j] = -1;
+      sim[j] = -INFINITY;
+      kk[j] = 0;
+    }
+  }
+  if (t == GATE_T - 1) *count = sc[t];
+}
+
+__global__ void __launch_bounds__(256) gate_gather_k(const float* __restrict__ q, int d,
+                                                     const int32_t* __restrict__ list, int mc,
+                                                     float* __restrict__ qc) {
+  const int64_t total = (int64_t)mc * d;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t j = e / d;
+    qc[e] = q[(int64_t)list[j] * d + (e - j * d)];
+  }
+}
+
+__global__ void __launch_bounds__(256) gate_scatter_k(const int32_t* __restrict__ list, int mc,
+                                                      const int64_t* __restrict__ ci,
+                                                      const float* __restrict__ cs,
+                                                      const int32_t* __restrict__ ck,
+                                                      int64_t* __restrict__ idx,
+                                                      float* __restrict__ sim,
+                                                      int32_t* __restrict__ kk) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= mc) return;
+  const int q = list[j];
+  idx[q] = ci[j];
+  sim[q] = cs[j];
+  kk[q] = ck[j];
+}
+
+struct GatedPlan {
+  size_t score, list, count, qc, ci, cs, ck, lk, lk_bytes, total;
+};
+
+GatedPlan gated_plan(int32_t m, int64_t n, int32_t d) {
+  GatedPlan p{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + std::max<size_t>(bytes, 1), 256);
+    return at;
+  };
+  p.score = take((size_t)m * 8);
+  p.list = take((size_t)m * 4);
+  p.count = take(4);
+  p.qc = take((size_t)m * d * 4);
+  p.ci = take((size_t)m * 8);
+  p.cs = take((size_t)m * 4);
+  p.ck = take((size_t)m * 4);
+  p.lk_bytes = nv_cache_lookup_workspace(m, n, d);
+  p.lk = take(p.lk_bytes);
+  p.total = o;
+  return p;
+}
+}  // namespace
+}  // namespace nv
+
+extern "C" size_t nv_cache_lookup_gated_workspace(int32_t m, int64_t n, int32_t d) {
+  if (m <= 0 || n < 0 || d <= 0) return 0;
+  return gated_plan(m, n, d).total;
+}
+
+extern "C" int32_t nv_cache_lookup_gated(const float* queries, int32_t m, const void* cache,
+                                         int32_t c_dtype, int64_t n, int32_t d,
+                                         const float* thresholds, const int32_t* k_values,
+                                         int32_t J, const double* w, double rho, double tau,
+                                         int64_t* idx_out, float* sim_out, int32_t* k_out,
+                                         double* score_out, int32_t* n_searched, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  clear_error();
+  Thresholds th;
+  int32_t st = lookup_check(queries, m, cache, c_dtype, n, d, thresholds, k_values, J, idx_out,
+                            sim_out, k_out, &th);
+  if (st != NV_OK) return st;
+  NV_CHECK_ARG(w && n_searched, "null predictor weights or n_searched");
+  NV_CHECK_ARG(std::isfinite(rho) && !std::isnan(tau), "rho must be finite, tau not NaN");
+  const GatedPlan p = gated_plan(m, n, d);
+  if (!workspace || workspace_bytes < p.total || ((uintptr_t)workspace & 255)) {
+    set_error("gated lookup workspace missing, misaligned or smaller than "
+              "nv_cache_lookup_gated_workspace()");
+    return NV_ERR_WORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  double* score = score_out ? score_out : (double*)(ws + p.score);
+  int32_t* list = (int32_t*)(ws + p.list);
+  int32_t* cnt_dev = (int32_t*)(ws + p.count);
+  st = nv_match_gate(queries, m, d, w, rho, tau, score, nullptr, nullptr, nullptr, stream);
+  if (st != NV_OK) return st;
+  hipLaunchKernelGGL(gate_compact_k, dim3(1), dim3(GATE_T), 0, s, (const double*)score, (int)m,
+                     tau, list, cnt_dev, idx_out, sim_out, k_out);
+  NV_LAUNCH_CHECK("gate_compact_k");
+  int32_t mc = 0;
+  NV_HIP_TRY(hipMemcpyAsync(&mc, cnt_dev, 4, hipMemcpyDeviceToHost, s));
+  NV_HIP_TRY(hipStreamSynchronize(s));
+  *n_searched = mc;
+  if (mc == 0) return NV_OK;
+  float* qc = (float*)(ws + p.qc);
+  const unsigned gb = (unsigned)std::min<int64_t>(ceil_div((int64_t)mc * d, 256), 4096);
+  hipLaunchKernelGGL(gate_gather_k, dim3(gb), dim3(256), 0, s, queries, (int)d,
+                     (const int32_t*)list, mc, qc);
+  NV_LAUNCH_CHECK("gate_gather_k");
+  int64_t* ci = (int64_t*)(ws + p.ci);
+  float* cs = (float*)(ws + p.cs);
+  int32_t* ck = (int32_t*)(ws + p.ck);
+  st = lookup_run(qc, mc, cache, c_dtype, n, d, th, ci, cs, ck, ws + p.lk, s);
+  if (st != NV_OK) return st;
+  hipLaunchKernelGGL(gate_scatter_k, dim3((unsigned)ceil_div(mc, 256)), dim3(256), 0, s,
+                     (const int32_t*)list, mc, (const int64_t*)ci, (const float*)cs,
+                     (const int32_t*)ck, idx_out, sim_out, k_out);
+  NV_LAUNCH_CHECK("gate_scatter_k");
+  return NV_OK;
+}
+
+// ---------------------------------------------------------------------------
 // The lookup without a caller workspace, for callers that cannot allocate:
 // its scratch is the file-scope device array below, one copy per GPU, held
 // until the process ends.  Host code never uses the array's name as an

@@ -114,4 +114,14 @@ WORKLOADS = {
         cache_seed=31, query_seed=32, n_queries=256, thresholds=THRESHOLDS_PAPER,
         N=50, guidance=7.5, weight_seed=0, batch=16, cond_seed=3, uncond_seed=4,
     ),
+    # The retrieval-heavy recipe with its cluster centres inside a cone (cosine 0.5
+    # to a common axis: centres at cosine 0.25, distinct cached prompts at about
+    # 0.09 on average, the anisotropy of text-encoder embeddings), for the match
+    # predictor in front of the lookup: in-domain requests as above, off-domain
+    # ones uniform on the sphere.
+    "retrieval_gated": dict(
+        unet="sd15", n_cache=10_000_000, d=768, cache_dtype="bf16", clusters=10_000, sigma=0.05,
+        cone=0.5, cache_seed=33, query_seed=34, n_queries=256, thresholds=THRESHOLDS_PAPER,
+        N=50, guidance=7.5, weight_seed=0, batch=16, cond_seed=3, uncond_seed=4,
+    ),
 }

@@ -28,10 +28,25 @@ def from_bf16_bits(b):
     return (b.astype(np.uint32) << 16).view(np.float32)
 
 
-def cluster_centres(clusters, d, seed):
+def _into_cone(mu, axis, cone):
+    """Unit centres at cosine `cone` to the unit `axis`: cone * axis + sqrt(1 - cone^2)
+    times the normalised component of mu orthogonal to the axis."""
+    mu = mu - (mu @ axis)[:, None] * axis[None, :]
+    mu /= np.linalg.norm(mu, axis=1, keepdims=True)
+    return cone * axis[None, :] + np.sqrt(1.0 - cone * cone) * mu
+
+
+def cluster_centres(clusters, d, seed, cone=0.0):
+    """Unit centres, uniform on the sphere; with cone > 0, inside a cone around a
+    seeded axis (every centre at cosine `cone` to it), the anisotropy of text-encoder
+    embedding spaces, where a linear one-class model can tell in-domain prompts from
+    off-domain ones."""
     rng = np.random.default_rng([seed, 0])
     mu = rng.standard_normal((clusters, d))
     mu /= np.linalg.norm(mu, axis=1, keepdims=True)
+    if cone > 0.0:
+        axis = np.random.default_rng([seed, 9]).standard_normal(d)
+        mu = _into_cone(mu, axis / np.linalg.norm(axis), cone)
     return mu.astype(np.float32)
 
 
@@ -46,15 +61,16 @@ def _chunk_rows(mu, sigma, seed, chunk_index, rows):
     return x
 
 
-def make_cache(n, d, clusters, sigma, seed, dtype="bf16", dup_pairs=(), threads=16):
+def make_cache(n, d, clusters, sigma, seed, dtype="bf16", dup_pairs=(), threads=16, cone=0.0):
     """Cache of n unit-norm embeddings.
 
     dtype "f32" -> float32 [n][d]; "bf16" -> uint16 bit patterns [n][d].
     dup_pairs: (i, j) pairs; row j is overwritten with an exact copy of row i.
+    cone: centres inside a cone (cluster_centres).
     Chunks have their own streams, so the values do not depend on `threads`.
     """
     from concurrent.futures import ThreadPoolExecutor
-    mu = cluster_centres(clusters, d, seed)
+    mu = cluster_centres(clusters, d, seed, cone)
     out = np.empty((n, d), dtype=np.float32 if dtype == "f32" else np.uint16)
 
     def fill(c):
@@ -157,21 +173,28 @@ def make_k_values(b, choices, seed):
     return rng.choice(np.asarray(choices, dtype=np.int32), size=b)
 
 
-def _device_centres(g, clusters, d, device):
+def _device_centres(g, clusters, d, device, cone=0.0):
     import torch
     mu = torch.randn(clusters, d, generator=g, device=device, dtype=torch.float32)
-    return mu / mu.norm(dim=1, keepdim=True)
+    mu = mu / mu.norm(dim=1, keepdim=True)
+    if cone > 0.0:  # the axis is the generator's next draw
+        axis = torch.randn(d, generator=g, device=device, dtype=torch.float32)
+        axis /= axis.norm()
+        mu = mu - (mu @ axis)[:, None] * axis[None, :]
+        mu /= mu.norm(dim=1, keepdim=True)
+        mu = cone * axis[None, :] + float(np.sqrt(1.0 - cone * cone)) * mu
+    return mu
 
 
-def cluster_centres_device(clusters, d, seed, device):
+def cluster_centres_device(clusters, d, seed, device, cone=0.0):
     """The centres make_cache_device draws first from its generator (float32 [clusters][d])."""
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
-    return _device_centres(g, clusters, d, device)
+    return _device_centres(g, clusters, d, device, cone)
 
 
-def make_cache_device(n, d, clusters, sigma, seed, device, chunk=1 << 20):
+def make_cache_device(n, d, clusters, sigma, seed, device, chunk=1 << 20, cone=0.0):
     """The same cluster recipe drawn with torch's seeded generator on `device`, for caches
     too large to generate on the host (10M x 768).  Returns a torch.bfloat16 [n][d]
     tensor (round to nearest even); values depend only on (seed, n, d, clusters, sigma,
@@ -179,7 +202,7 @@ def make_cache_device(n, d, clusters, sigma, seed, device, chunk=1 << 20):
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
-    mu = _device_centres(g, clusters, d, device)
+    mu = _device_centres(g, clusters, d, device, cone)
     out = torch.empty((n, d), dtype=torch.bfloat16, device=device)
     for start in range(0, n, chunk):
         rows = min(chunk, n - start)

@@ -163,3 +163,32 @@ def test_static_lookup_validation_before_launch():
     # the limits quoted with the declaration
     assert lib.nv_cache_lookup_workspace(8, 85_000_000, 768) <= N.NV_LOOKUP_STATIC_BYTES
     assert lib.nv_cache_lookup_workspace(256, 4_100_000, 768) <= N.NV_LOOKUP_STATIC_BYTES
+
+
+def test_gated_lookup_validation_before_launch():
+    """nv_cache_lookup_gated checks the lookup's arguments, the predictor's and
+    the workspace before any launch."""
+    from paper_2312_04429_amd import _native as N
+    lib = N.lib
+    thr = (C.c_float * 2)(0.9, 0.75)
+    kv = (C.c_int32 * 2)(10, 5)
+    dummy = C.c_void_p(0x10000)
+    searched = C.c_int32(-7)
+    need = lib.nv_cache_lookup_gated_workspace(4, 100, 64)
+    assert need >= lib.nv_cache_lookup_workspace(4, 100, 64) + 4 * 64 * 4
+
+    def call(q=dummy, m=4, d=64, w=dummy, rho=0.5, tau=0.0, ns=C.byref(searched), ws=dummy,
+             wb=need):
+        return lib.nv_cache_lookup_gated(q, m, dummy, N.NV_BF16, 100, d, thr, kv, 2, w, rho, tau,
+                                         dummy, dummy, dummy, None, ns, ws, wb, None)
+    assert call(q=None) == N.NV_ERR_INVALID_ARG
+    assert call(m=4097) == N.NV_ERR_INVALID_ARG
+    assert call(w=None) == N.NV_ERR_INVALID_ARG
+    assert call(ns=None) == N.NV_ERR_INVALID_ARG
+    assert call(rho=float("inf")) == N.NV_ERR_INVALID_ARG
+    assert call(tau=float("nan")) == N.NV_ERR_INVALID_ARG
+    assert call(d=60) == N.NV_ERR_UNSUPPORTED
+    assert call(wb=need - 1) == N.NV_ERR_WORKSPACE
+    assert call(ws=C.c_void_p(0x10008)) == N.NV_ERR_WORKSPACE
+    assert searched.value == -7  # untouched on every error
+    assert lib.nv_cache_lookup_gated_workspace(0, 100, 64) == 0
