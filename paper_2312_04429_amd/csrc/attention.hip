@@ -15,7 +15,9 @@
 // keys for its row d).  V arrives transposed from its projection, so both
 // tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps,
 // dims past d read as zero (d = 40 -> 64, 80 -> 96 for Q K^T): Q's from
-// registers, K's from a zero pad of each LDS key row.
+// registers, K's from a zero pad of each LDS key row.  The accumulators of
+// Q K^T start at minus the query's reference max, so the scores leave the
+// multiply already shifted for the exponential.
 #include "common.h"
 #include "attention.h"
 #include "trace.h"
@@ -145,7 +147,16 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * 256;
-      if (c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
+      if (KCN % 256 == 0 || c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
+    }
+    if ((kb + 1) * KB <= a.L) {  // uniform: every key of the block is real
+#pragma unroll
+      for (int i = 0; i < VPT; ++i) {
+        const int c = tid + i * 256;
+        if (VCN % 256 == 0 || c < VCN)
+          *(uint4*)&sVt[buf][(c / (KB / 8)) * VROW + (c % (KB / 8)) * 8] = rv[i];
+      }
+      return;
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -171,7 +182,14 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     if (kb + 2 < nkb) fetch(kb + 2, Fk, Fv);
     const _Float16* K_ = sK[cur];
     const _Float16* V_ = sVt[cur];
-    // S^T for 4 key quarters x QB query blocks; lane holds keys h*16 + 4*kc + r.
+    // Scores relative to the reference max come straight out of the multiply:
+    // the accumulators start at -base (base = the query's reference max, 0
+    // before the first block).
+    float base[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) base[qb] = mrun[qb] == -INFINITY ? 0.f : mrun[qb];
+    // S^T - base for NH key quarters x QB query blocks; lane holds keys
+    // h*16 + 4*kc + r.
     floatx4 s[QB][NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
@@ -183,7 +201,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
                                                  : half8{};
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        s[qb][h] = floatx4{0.f, 0.f, 0.f, 0.f};
+        s[qb][h] = floatx4{-base[qb], -base[qb], -base[qb], -base[qb]};
 #pragma unroll
         for (int ks = 0; ks < N32; ++ks)
           s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
@@ -202,7 +220,8 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     // Online softmax with a lazily moved reference: while no score of the wave
     // exceeds its query's reference max by more than 2^RESCALE_LOG2 (p stays
     // <= 256, exact enough in float16), the reference stays and nothing is
-    // rescaled; otherwise every lane moves to its new max and rescales.
+    // rescaled; otherwise every lane moves to its new max, rescales, and
+    // shifts this block's relative scores by the move.
     constexpr float RESCALE_LOG2 = 8.0f;
     float mloc[QB];
     bool grow = false;
@@ -215,18 +234,22 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
         for (int r = 0; r < 4; ++r) m = fmaxf(m, s[qb][h][r]);
       m = fmaxf(m, __shfl_xor(m, 16, 64));
       m = fmaxf(m, __shfl_xor(m, 32, 64));
-      mloc[qb] = m;
-      grow |= !(m <= mrun[qb] + RESCALE_LOG2);  // also true while mrun is -inf
+      mloc[qb] = m;  // relative to base
+      grow |= !(m <= RESCALE_LOG2) || mrun[qb] == -INFINITY;
     }
     if (__ballot(grow)) {  // uniform: the whole wave moves its references
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        const float mnew = fmaxf(mrun[qb], mloc[qb]);
+        // new reference base + delta = max(reference, block max)
+        const float delta = mrun[qb] == -INFINITY ? mloc[qb] : fmaxf(mloc[qb], 0.f);
+        const float mnew = base[qb] + delta;
         const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
         mrun[qb] = mnew;
         lrun[qb] *= alpha;
 #pragma unroll
         for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) s[qb][h] -= delta;
       }
     }
     half8 fp[QB][NS];
@@ -237,7 +260,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
       for (int h = 0; h < NH; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[qb][h][r] - mrun[qb]);
+          const float p = __builtin_amdgcn_exp2f(s[qb][h][r]);
           if (!ONES) psum += p;
           fp[qb][h >> 1][(h & 1) * 4 + r] = (_Float16)p;
         }
