@@ -330,20 +330,24 @@ __global__ void temb_sin_k(const int32_t* __restrict__ step, const int32_t* __re
 }
 
 // conv_in in float32 from the float32 latent x [samples][Cin][H][W]; output
-// [rows][H*W][C0] float16, rows 2b and 2b+1 read sample b.  One workgroup per
-// 64 output pixels of a row: the 3x3xCin input patch of each pixel is gathered
-// once into registers and the weights sit in LDS.
+// [rows][H*W][C0] float16, rows 2b and 2b+1 read sample b.  Workgroup
+// (blockIdx.x = 64 output pixels of a row, blockIdx.y = 32 output channels):
+// wave w produces channels 8 w .. 8 w + 7 of the block for its lane's pixel
+// (3x3xCin patch gathered into registers, weights read from LDS as
+// broadcasts) and stores them as one 16-byte vector.  C0 % 32 == 0.
 template <int CIN>
 __global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
                                                  const float* __restrict__ w,
                                                  const float* __restrict__ bias, int Cin_rt, int H,
                                                  int W, int C0, int rows,
                                                  _Float16* __restrict__ out) {
-  const int Cin = CIN > 0 ? CIN : Cin_rt;  // CIN > 0: patch stays in registers
-  extern __shared__ float sw[];  // [C0][Cin*9] weights then [C0] bias
+  const int Cin = CIN > 0 ? CIN : Cin_rt;  // CIN > 0: patch size known at compile time
+  constexpr int NKMAX = (CIN > 0 ? CIN : 16) * 9;
+  __shared__ float sw[32 * NKMAX + 32];    // this block's 32 channels, then their bias
   const int nk = Cin * 9;
-  for (int i = threadIdx.x; i < C0 * nk; i += 256) sw[i] = w[i];
-  for (int i = threadIdx.x; i < C0; i += 256) sw[C0 * nk + i] = bias[i];
+  const int c0 = blockIdx.y * 32;
+  for (int i = threadIdx.x; i < 32 * nk; i += 256) sw[i] = w[(int64_t)c0 * nk + i];
+  if (threadIdx.x < 32) sw[32 * nk + threadIdx.x] = bias[c0 + threadIdx.x];
   __syncthreads();
   const int HW = H * W;
   const int pblocks = (HW + 63) / 64;
@@ -352,22 +356,26 @@ __global__ void __launch_bounds__(256) conv_in_k(const float* __restrict__ x,
   if (r >= rows || p >= HW) return;
   const int y = p / W, xx = p % W;
   const float* xs = x + (int64_t)(r >> 1) * Cin * HW;
-  float patch[(CIN > 0 ? CIN : 16) * 9];
+  float patch[NKMAX];
 #pragma unroll
-  for (int ci = 0; ci < Cin; ++ci)
-#pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const int iy = y + t / 3 - 1, ix = xx + t % 3 - 1;
-      patch[ci * 9 + t] = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? xs[(int64_t)ci * HW + iy * W + ix] : 0.f;
-    }
-  // the 4 waves split the output channels
-  for (int co = threadIdx.x >> 6; co < C0; co += 4) {
-    const float* wr = sw + co * nk;
-    float acc = sw[C0 * nk + co];
-#pragma unroll
-    for (int k = 0; k < nk; ++k) acc = fmaf(wr[k], patch[k], acc);
-    out[((int64_t)r * HW + p) * C0 + co] = (_Float16)acc;
+  for (int k = 0; k < NKMAX; ++k) {
+    const int ci = k / 9, t = k % 9;
+    const int iy = y + t / 3 - 1, ix = xx + t % 3 - 1;
+    patch[k] = (k < nk && iy >= 0 && iy < H && ix >= 0 && ix < W)
+                   ? xs[(int64_t)ci * HW + iy * W + ix] : 0.f;
   }
+  const int wv = threadIdx.x >> 6;
+  half8 h;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const float* wr = sw + (wv * 8 + c) * nk;
+    float a = sw[32 * nk + wv * 8 + c];
+#pragma unroll
+    for (int k = 0; k < NKMAX; ++k)
+      if (CIN > 0 || k < nk) a = fmaf(wr[k], patch[k], a);
+    h[c] = (_Float16)a;
+  }
+  *(half8*)(out + ((int64_t)r * HW + p) * C0 + c0 + wv * 8) = h;
 }
 
 // eps = eps_u + s (eps_c - eps_u); x0 = (x - sqrt(1-a_t) eps) / sqrt(a_t);
@@ -739,28 +747,12 @@ hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int ro
 
 hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Cin, int H, int W,
                           int C0, int rows, _Float16* out, hipStream_t s) {
-  if (Cin > 16) return hipErrorInvalidValue;
-  const size_t lds = ((size_t)C0 * Cin * 9 + C0) * 4;
-  if (lds > 160 * 1024) return hipErrorInvalidValue;
-  if (lds > 65536) {  // once, for the largest size any call may ask for
-    static bool attr = false;
-    if (!attr) {
-      hipError_t e = hipFuncSetAttribute((const void*)conv_in_k<0>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e == hipSuccess)
-        e = hipFuncSetAttribute((const void*)conv_in_k<4>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e != hipSuccess) return e;
-      attr = true;
-    }
-  }
-  const int pblocks = (H * W + 63) / 64;
+  if (Cin > 16 || C0 % 32 != 0) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(rows * ((H * W + 63) / 64)), (unsigned)(C0 / 32));
   if (Cin == 4)
-    hipLaunchKernelGGL(conv_in_k<4>, dim3((unsigned)(rows * pblocks)), dim3(256), lds, s, x, w, b,
-                       Cin, H, W, C0, rows, out);
+    hipLaunchKernelGGL(conv_in_k<4>, grid, dim3(256), 0, s, x, w, b, Cin, H, W, C0, rows, out);
   else
-    hipLaunchKernelGGL(conv_in_k<0>, dim3((unsigned)(rows * pblocks)), dim3(256), lds, s, x, w, b,
-                       Cin, H, W, C0, rows, out);
+    hipLaunchKernelGGL(conv_in_k<0>, grid, dim3(256), 0, s, x, w, b, Cin, H, W, C0, rows, out);
   return hipGetLastError();
 }
 
