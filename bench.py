@@ -61,6 +61,9 @@ def parse():
                          "the predictor in front (only predicted matches searched) beside the "
                          "plain lookup over the same queries")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="launch each denoise step's kernels one by one instead of replaying a "
+                         "captured graph (for counter collection, which samples per dispatch)")
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the event tracing of kernel launches (for counter passes)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -292,6 +295,8 @@ def main():
         return scan_only(args, wl, P, torch, dev, d_q, d_cache, thr, kv, lws, q.shape[0])
     weights = synth.make_weights(cfg, wl["weight_seed"])
     net = P.NvUNet(cfg, weights)
+    if args.no_graphs:
+        net.set_options(graphs=False)
     cond = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["cond_seed"])
     unc = synth.make_contexts(B, cfg["ctx_len"], cfg["ctx_dim"], wl["uncond_seed"])
     d_cond, d_unc = t(cond), t(unc)
