@@ -27,18 +27,6 @@ namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
-// Max over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one query's 16-lane rows)
-// with gfx950's row swaps, which run on the VALU (a shuffle goes through LDS):
-// permlane16_swap of x with itself leaves rows (0, 0, 2, 2) in one result and
-// (1, 1, 3, 3) in the other, permlane32_swap halves (lo, lo) and (hi, hi).
-__device__ inline float rows_max(float x) {
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                                  false);
-  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false,
-                                                  false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
 
 // Halfs per LDS key row: an odd number of 16-byte chunks (conflict-free row
 // reads); a head dim off the 32 grid gets its row padded with zeros to the

@@ -61,6 +61,20 @@ __device__ inline int xcd_remap(int b, int total) {
   return x * base + (x < rem ? x : rem) + local;
 }
 
+// Max over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane rows of
+// a wave) with gfx950's row swaps, which run on the VALU (a shuffle goes
+// through LDS): permlane16_swap of x with itself leaves rows (0, 0, 2, 2) in
+// one result and (1, 1, 3, 3) in the other, permlane32_swap halves (lo, lo)
+// and (hi, hi).
+__device__ inline float rows_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false,
+                                                  false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -433,8 +433,7 @@ __global__ void __launch_bounds__(256, 2) lk_scan_bf16(const uint16_t* __restric
       v = (full || rl + r < rows) ? fmaxf(v, acc0[r]) : v;
       v = (full || rl + 16 + r < rows) ? fmaxf(v, acc1[r]) : v;
     }
-    v = fmaxf(v, __shfl_xor(v, 16, 64));
-    v = fmaxf(v, __shfl_xor(v, 32, 64));
+    v = rows_max(v);
     float* M = sM + (i & 1) * 4 * QB;
     if (kc == 0) M[wave * QB + li] = v;
     // This wave's part of block i + 1 has landed once only block i + 2's
