@@ -986,7 +986,13 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
     // otherwise (graph-timed on the batched SD-1.5 and SDXL shapes; the batch-1
     // feed-forward products, 320 to 1280 tiles of 128 x 128, run 8 to 22 % faster
     // at 64 x 128)
-    const bool big = (g.N >= 2560 && t128 >= 1536) || g.K >= 8192 || g.N <= 320;
+    // (and, measured on the SDXL level-2 and batch-8 shapes, 128 x 128 for at least
+    // 4096 rows when wide with K >= 1280 or deep with N >= 1280: q|k|v 4096x3840x1280
+    // 76.6 -> 55.6 us, 4096x1280x5120 85.1 -> 74.0 us; the 640-channel
+    // convolutions and 16384-row products below 2560 columns stay at 64 x 128)
+    const bool big = (g.N >= 2560 && t128 >= 1536) || g.K >= 8192 || g.N <= 320 ||
+                     (g.M >= 4096 && g.N >= 2560 && g.K >= 1280) ||
+                     (g.M >= 4096 && g.N >= 1280 && g.K >= 4096);
     return big ? launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s)
                : launch_s<MODE, 64, 128, 2>(g, 1, s);
   }
