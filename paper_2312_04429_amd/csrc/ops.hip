@@ -14,7 +14,7 @@ namespace {
 __device__ inline float silu(float x) { return x / (1.0f + __expf(-x)); }
 
 __device__ inline float block_sum_256(float v, float* red) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  v = wave_sum(v);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
@@ -256,7 +256,7 @@ __global__ void __launch_bounds__(256) layernorm_k(const _Float16* __restrict__ 
       }
     }
   }
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  s = wave_sum(s);
   const float mean = s / (float)C;
   float q = 0.f;
 #pragma unroll
@@ -270,7 +270,7 @@ __global__ void __launch_bounds__(256) layernorm_k(const _Float16* __restrict__ 
       }
     }
   }
-  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  q = wave_sum(q);
   const float rstd = rsqrtf(q / (float)C + eps);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -482,8 +482,7 @@ constexpr int GN1_T = 1024;
 constexpr int GN1_NV = 32;  // pixels per thread at most (more would spill)
 
 __device__ inline float block_sum_1024(float v, float* red) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  v = wave_sum(v);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
