@@ -74,7 +74,9 @@ def parse():
 
 def unet_flops_per_row(cfg):
     """Algorithmic matrix FLOPs (2*M*N*K of every conv, linear and attention product)
-    of one UNet evaluation on one row."""
+    of one denoising step's UNet evaluation on one row.  The cross-attention K / V
+    projections of the text context are left out: they depend on the context only, so
+    the denoise computes them once per call, not per step."""
     import synth
     fl = 0
     c0 = cfg["ch"][0]
@@ -99,7 +101,6 @@ def unet_flops_per_row(cfg):
         for _ in range(depth):
             f += 2 * s * 3 * c * c + 2 * 2 * s * s * c + 2 * s * c * c           # self-attn
             f += 2 * s * c * c + 2 * 2 * s * cfg["ctx_len"] * c + 2 * s * c * c  # cross q, attn, o
-            f += 2 * 2 * cfg["ctx_len"] * cfg["ctx_dim"] * c                   # context k, v
             f += 2 * s * 8 * c * c + 2 * s * 4 * c * c                          # GEGLU FF
         return f
 
