@@ -13,9 +13,9 @@
 // in the B-operand layout of O^T = V^T P^T (the 8 keys a lane contributes to
 // one 32-key MFMA step are the 2 x 4 keys it holds; V^T supplies the same 8
 // keys for its row d).  V arrives transposed from its projection, so both
-// tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps,
-// dims past d read as zero (d = 40 -> 64, 80 -> 96 for Q K^T): Q's from
-// registers, K's from a zero pad of each LDS key row.  The accumulators of
+// tiles move as 16-byte rows.  The head dimension runs in 32-wide MFMA steps
+// (d = 40 -> 64, 80 -> 96 for Q K^T) with Q's dims past d zero in registers,
+// so whatever K values meet them add nothing.  The accumulators of
 // Q K^T start at minus the query's reference max, so the scores leave the
 // multiply already shifted for the exponential.
 #include "common.h"
@@ -29,12 +29,10 @@ constexpr float LOG2E = 1.4426950408889634f;
 
 
 // Halfs per LDS key row: an odd number of 16-byte chunks (conflict-free row
-// reads); a head dim off the 32 grid gets its row padded with zeros to the
-// next multiple of 32 plus one chunk, so every lane reads its Q K^T fragment
-// unconditionally (the pad meets Q's zeros past d).
-constexpr int krow(int dh) {
-  return dh % 32 ? (dh + 31) / 32 * 32 + 8 : ((dh / 8) % 2 ? dh : dh + 8);
-}
+// reads).  Past d a lane of the last 32-wide step reads the row's chunk at that
+// step's start instead (real keys, in range); Q's fragment is zero there, so
+// those products add nothing.
+constexpr int krow(int dh) { return (dh / 8) % 2 ? dh : dh + 8; }
 
 // QB: 16-query column blocks per wave (2; 1 where the grid would otherwise
 // leave compute units idle, e.g. 1024 or 256 queries per head at batch 1).
@@ -47,7 +45,6 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
-  constexpr bool KPAD = DH % 32 != 0;          // key rows padded with zeros to N32 * 32 dims
   constexpr int KROW = krow(DH);               // halfs per LDS key row
   constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
   constexpr int KPT = (KCN + 255) / 256, VPT = (VCN + 255) / 256;
@@ -198,8 +195,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
       half8 fk[N32];
 #pragma unroll
       for (int ks = 0; ks < N32; ++ks)
-        fk[ks] = (KPAD || ks * 32 + kc * 8 < DH) ? *(const half8*)(kr + ks * 32 + kc * 8)
-                                                 : half8{};
+        fk[ks] = *(const half8*)(kr + (ks * 32 + kc * 8 < DH ? ks * 32 + kc * 8 : ks * 32));
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         s[qb][h] = floatx4{-base[qb], -base[qb], -base[qb], -base[qb]};
@@ -288,13 +284,6 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   };
   if (ONES)
     for (int i = tid; i < 2 * KB; i += 256) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
-  if (KPAD) {  // zero pad of every key row in both buffers (the stash never writes it)
-    constexpr int PADC = (N32 * 32 - DH) / 8;
-    for (int i = tid; i < 2 * KB * PADC; i += 256) {
-      const int b = i / (KB * PADC), r = (i / PADC) % KB, c = i % PADC;
-      *(half8*)&sK[b][r * KROW + DH + c * 8] = half8{};
-    }
-  }
   fetch(0, rkA, rvA);
   if (1 < nkb) fetch(1, rkB, rvB);
   stash(0, 0, rkA, rvA);
