@@ -30,7 +30,8 @@ pytestmark = pytest.mark.gpu
                                                (1, 200, 333, 8, 40), (1, 512, 1000, 8, 40),
                                                (2, 2048, 333, 8, 40), (3, 4096, 200, 8, 40),
                                                (16, 256, 256, 8, 160), (16, 256, 77, 8, 160),
-                                               (16, 1024, 77, 8, 80)])
+                                               (16, 1024, 77, 8, 80), (2, 4096, 4096, 8, 40),
+                                               (1, 2000, 1000, 16, 40), (2, 2048, 128, 8, 40)])
 def test_attention(rows, S, L, heads, dh):
     print(f"op attention rows={rows} S={S} L={L} heads={heads} dh={dh}", flush=True)
     C = heads * dh
@@ -71,6 +72,8 @@ PEAK_CASES = [  # (rows, S, L, heads, dh): form
     (1, 256, 700, 8, 40),    # 1 x 64
     (2, 2048, 700, 8, 40),   # 2 x 128
     (3, 4096, 700, 8, 40),   # 2 x 64
+    (2, 2048, 704, 8, 40),   # 2 x 128
+    (1, 4000, 1000, 8, 40),  # 2 x 128, ragged queries and last key block
     (1, 300, 700, 8, 64),    # 1 x 64
     (2, 2048, 700, 8, 64),   # 2 x 64
     (1, 2100, 700, 8, 80),   # 1 x 64 (264 workgroups of 64 queries)
