@@ -41,6 +41,11 @@ hipError_t schedule_launch(int T, int N, double b0, double b1, int32_t* ts, floa
                            float* a_prev, hipStream_t s);
 hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int rows, _Float16* out,
                            hipStream_t s);
+// sinusoidal embeddings of the timesteps of grid steps 0 .. N-1, one row each
+hipError_t temb_sin_steps_launch(const int32_t* ts, int C0, int N, _Float16* out, hipStream_t s);
+// out row r <- table row (grid step of sample r / 2), float32, width % 4 == 0
+hipError_t step_rows_launch(const StepArgs& st, const float* table, int width, int rows,
+                            float* out, hipStream_t s);
 hipError_t conv_in_launch(const float* x, const float* w, const float* b, int Cin, int H, int W,
                           int C0, int rows, _Float16* out, hipStream_t s);
 hipError_t cfg_ddim_launch(const StepArgs& st, const float* eps, float* x, int C, int HW,

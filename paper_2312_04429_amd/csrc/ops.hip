@@ -318,8 +318,8 @@ __global__ void temb_sin_k(const int32_t* __restrict__ step, const int32_t* __re
                            int rows, _Float16* __restrict__ out) {
   const int r = blockIdx.x;
   if (r >= rows) return;
-  const int b = r >> 1;
-  const float t = (float)ts[step[b]];
+  // row r: sample r / 2 at its current grid step, or (step == null) grid step r
+  const float t = (float)ts[step ? step[r >> 1] : r];
   const int half = C0 / 2;
   for (int k = threadIdx.x; k < half; k += blockDim.x) {
     const float f = expf(-logf(10000.0f) * (float)k / (float)half);
@@ -741,6 +741,30 @@ hipError_t temb_sin_launch(const StepArgs& st, const int32_t* ts, int C0, int ro
                            hipStream_t s) {
   hipLaunchKernelGGL(temb_sin_k, dim3(rows), dim3(128), 0, s, (const int32_t*)st.dev, ts, C0, rows,
                      out);
+  return hipGetLastError();
+}
+
+hipError_t temb_sin_steps_launch(const int32_t* ts, int C0, int N, _Float16* out, hipStream_t s) {
+  hipLaunchKernelGGL(temb_sin_k, dim3(N), dim3(128), 0, s, (const int32_t*)nullptr, ts, C0, N, out);
+  return hipGetLastError();
+}
+
+// Row r of out <- row dev[r / 2] (the grid step of sample r / 2) of a table of
+// per-step rows; width % 4 == 0.
+__global__ void step_rows_k(const int32_t* __restrict__ step, const float4* __restrict__ table,
+                            int w4, int rows, float4* __restrict__ out) {
+  const int r = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows || i >= w4) return;
+  out[(int64_t)r * w4 + i] = table[(int64_t)step[r >> 1] * w4 + i];
+}
+
+hipError_t step_rows_launch(const StepArgs& st, const float* table, int width, int rows,
+                            float* out, hipStream_t s) {
+  if (width % 4 != 0) return hipErrorInvalidValue;
+  const int w4 = width / 4;
+  hipLaunchKernelGGL(step_rows_k, dim3((unsigned)ceil_div(w4, 256), (unsigned)rows), dim3(256), 0, s,
+                     (const int32_t*)st.dev, (const float4*)table, w4, rows, (float4*)out);
   return hipGetLastError();
 }
 

@@ -228,6 +228,7 @@ struct RunCtx {
   StepArgs st;
   float* partial;    // split-K scratch
   size_t partial_bytes;
+  int nsteps = 0;    // grid steps N of the call's schedule
 };
 
 inline hipError_t gemm_run(GemmArgs g, const RunCtx& c) {
@@ -291,7 +292,11 @@ struct Plan {
   size_t x_work = 0, eps = 0, ts = 0, at = 0, ap = 0, ctx = 0, pooled = 0, tproj = 0;
   size_t gnpart = 0, splitk = 0;
   size_t stepdev = 0;  // int32 [2][MAX_SAMPLES]: current grid step and caller index per sample
+  size_t ttab = 0;     // float32 [MAX_GRID_STEPS][temb_total]: ResBlock time projections per grid step
 };
+
+// A schedule has N <= T / 2 <= 512 grid steps.
+constexpr int MAX_GRID_STEPS = 512;
 
 // What a captured denoise step depends on besides the active rows: the plan
 // (its buffer offsets), the workspace and the update's constants.
@@ -753,8 +758,57 @@ std::unique_ptr<Plan> build_plan(nv_unet* net, int Rmax) {
   }
   auto& ops = P->step;
 
-  // time embedding -> SiLU(temb) -> every ResBlock's projection
-  {
+  // time embedding -> SiLU(temb) -> every ResBlock's projection.  Without a
+  // pooled vector the projections depend only on the grid step, so each call
+  // computes them once for its N grid steps (P->ttab) and a step copies the
+  // rows of its samples' grid steps; with one, every step computes them for
+  // its rows.
+  if (c.pooled_dim == 0 && net->temb_total % 4 == 0) {
+    const int N = net->temb_total;
+    P->ttab = B.fixed((size_t)MAX_GRID_STEPS * N * 4);
+    const size_t so = B.fixed((size_t)MAX_GRID_STEPS * C0 * 2);
+    const size_t o1 = B.fixed((size_t)MAX_GRID_STEPS * td * 2);
+    const size_t o2 = B.fixed((size_t)MAX_GRID_STEPS * td * 2);
+    const size_t tso = P->ts, tt = P->ttab;
+    const _Float16* w1 = B.W16("time.l1.w");
+    const float* b1 = B.W32("time.l1.b");
+    const _Float16* w2 = B.W16("time.l2.w");
+    const float* b2 = B.W32("time.l2.b");
+    const _Float16* wa = B.W16("temb_all.w");
+    const float* ba = B.W32("temb_all.b");
+    P->pre.push_back([=](const RunCtx& x) {
+      const int M = x.nsteps;
+      if (M < 1 || M > MAX_GRID_STEPS) return hipErrorInvalidValue;
+      hipError_t e = temb_sin_steps_launch((const int32_t*)(x.ws + tso), C0, M,
+                                           (_Float16*)(x.ws + so), x.s);
+      if (e != hipSuccess) return e;
+      GemmArgs g = dense_args(td, C0, w1, b1);
+      g.M = M;
+      g.src1 = (const _Float16*)(x.ws + so);
+      g.silu = 1;
+      g.out = x.ws + o1;
+      g.ldo = td;
+      if ((e = gemm_run(g, x)) != hipSuccess) return e;
+      g = dense_args(td, td, w2, b2);
+      g.M = M;
+      g.src1 = (const _Float16*)(x.ws + o1);
+      g.silu = 1;
+      g.out = x.ws + o2;
+      g.ldo = td;
+      if ((e = gemm_run(g, x)) != hipSuccess) return e;
+      g = dense_args(N, td, wa, ba);
+      g.M = M;
+      g.src1 = (const _Float16*)(x.ws + o2);
+      g.out = x.ws + tt;
+      g.ldo = N;
+      g.out_f32 = 1;
+      return gemm_run(g, x);
+    });
+    const size_t o = P->tproj;
+    ops.push_back([=](const RunCtx& x) {
+      return step_rows_launch(x.st, (const float*)(x.ws + tt), N, x.R, (float*)(x.ws + o), x.s);
+    });
+  } else {
     Ten s0 = B.alloc(1, C0);
     const size_t so = s0.off, tso = P->ts;
     ops.push_back([=](const RunCtx& x) {
@@ -1320,6 +1374,7 @@ static int32_t denoise_impl(nv_unet* net, const nv_schedule* sched, float* laten
     NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
   RunCtx rc{ws, 2 * B, s, (const float*)(ws + P->x_work), sa, (float*)(ws + P->splitk),
             SPLITK_BYTES};
+  rc.nsteps = N;
   // copy every sorted sample a whose step count equals a slot's K
   auto take = [&](int a, int done) -> hipError_t {
     if (!snap) return hipSuccess;
@@ -1521,6 +1576,7 @@ extern "C" int32_t nv_unet_eps(nv_unet* net, const nv_schedule* sched, const flo
   if (c.pooled_dim > 0)
     NV_HIP_TRY(permute_launch(sa, pooled, (float*)(ws + P->pooled), c.pooled_dim, B, 1, s));
   RunCtx rc{ws, 2 * B, s, x, sa, (float*)(ws + P->splitk), SPLITK_BYTES};
+  rc.nsteps = sched->N;
   NV_HIP_TRY(run_ops(P->pre, rc));
   NV_HIP_TRY(run_ops(P->step, rc));
   NV_HIP_TRY(eps_split_launch((const float*)(ws + P->eps), c.out_ch, c.H * c.W, B, eps_uncond,
