@@ -1003,7 +1003,10 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   // (graph-timed 47 against 64 us at 32 x 32 with 1280 input channels)
   if (MODE == 1 && t128 >= 32 && t128 <= 128 && nk >= 80)
     return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 700), s);
-  const bool split = nk >= 40 || t64 < 128;
+  // split K past 40 k tiles, or below about 100 tiles (graph-timed alone:
+  // 2048 x 640 x 2560 22.2 -> 19.6 us and 512 x 1280 x 2560 17.9 -> 15.9 us
+  // unsplit, 128 x 3840 x 1280 10.8 -> 9.5 us)
+  const bool split = nk > 40 || t64 < 100;
   return launch_s<MODE, 64, 64, GEMM_S64>(g, split ? split_to(t64, 700) : 1, s);
 }
 
