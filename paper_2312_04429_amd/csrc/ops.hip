@@ -6,6 +6,8 @@
 #include <cmath>
 
 #include "common.h"
+
+#include <type_traits>
 #include "ops.h"
 
 namespace nv {
@@ -498,57 +500,149 @@ __device__ inline float h_lo(uint32_t u) {
 __device__ inline float h_hi(uint32_t u) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
 }
+__device__ inline uint32_t h_pack(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+}
 
-template <int NV>
-__global__ void __launch_bounds__(GN1_T) gn_group_k(GnArgs a) {
-  __shared__ float red[GN1_T / 64];
-  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
-  const int row = blockIdx.x / a.G, g = blockIdx.x % a.G;
-  const int t = threadIdx.x;
-  const bool on = t < P * vpp;
-  const int v = on ? t % vpp : 0, p0 = on ? t / vpp : 0;
-  const int c = g * cg + 2 * v;
-  const bool first = c < a.C1;
-  const int ld = first ? a.C1 : a.C2;
-  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
-                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
-  uint32_t x[NV];
+// W packed channel pairs (2W float16 values) at p, one 4-, 8- or 16-byte access
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+template <int W>
+__device__ inline void ld_pairs(const _Float16* p, uint32_t (&d)[W]) {
+  if constexpr (W == 1) {
+    d[0] = *(const uint32_t*)p;
+  } else if constexpr (W == 2) {
+    const u32x2v v = *(const u32x2v*)p;
+    d[0] = v[0];
+    d[1] = v[1];
+  } else {
+    static_assert(W == 4, "pairs per access");
+    const u32x4 v = *(const u32x4*)p;
+    d[0] = v[0]; d[1] = v[1]; d[2] = v[2]; d[3] = v[3];
+  }
+}
+template <int W>
+__device__ inline void st_pairs(_Float16* p, const uint32_t (&d)[W]) {
+  if constexpr (W == 1) {
+    *(uint32_t*)p = d[0];
+  } else if constexpr (W == 2) {
+    *(u32x2v*)p = u32x2v{d[0], d[1]};
+  } else {
+    *(u32x4*)p = u32x4{d[0], d[1], d[2], d[3]};
+  }
+}
+
+// Thread layout shared by the one-workgroup GroupNorm kernels: thread t owns
+// VW consecutive channels (VW / 2 packed pairs, one vector access) of the
+// group, vector t % vpp (vpp = cg / VW), for pixels t / vpp + j * P.
+template <int VW>
+struct GnLane {
+  int vpp, P, c, ld;
+  bool on;
+  int p0;
+  const _Float16* src;
+  __device__ GnLane(const GnArgs& a, int row, int g, int lo) {
+    const int C = a.C1 + a.C2, cg = C / a.G;
+    vpp = cg / VW;
+    P = GN1_T / vpp;
+    const int t = threadIdx.x;
+    on = t < P * vpp;
+    const int v = on ? t % vpp : 0;
+    p0 = lo + (on ? t / vpp : 0);
+    c = g * cg + VW * v;
+    const bool first = c < a.C1;
+    ld = first ? a.C1 : a.C2;
+    src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
+                : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
+  }
+};
+
+// load rounds j < NV of pixels below hi (others zero)
+template <int NV, int W>
+__device__ inline void gn_load(const GnLane<2 * W>& L, int hi, uint32_t (&x)[NV][W]) {
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    const int p = p0 + j * P;
-    x[j] = (on && p < a.HW) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
+    const int p = L.p0 + j * L.P;
+    if (L.on && p < hi) {
+      ld_pairs<W>(L.src + (int64_t)p * L.ld, x[j]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < W; ++e) x[j][e] = 0u;
+    }
   }
+}
+
+// normalise, affine, optional SiLU and store rounds j < NV of pixels below hi
+template <int NV, int W>
+__device__ inline void gn_store(const GnArgs& a, const GnLane<2 * W>& L, int row, int hi,
+                                float mean, float rstd, const uint32_t (&x)[NV][W]) {
+  const int C = a.C1 + a.C2;
+  float k[2 * W], f[2 * W];
+#pragma unroll
+  for (int e = 0; e < 2 * W; ++e) {
+    k[e] = rstd * a.gamma[L.c + e];
+    f[e] = a.beta[L.c + e] - mean * k[e];
+  }
+  _Float16* dst = a.out + (int64_t)row * a.HW * C + L.c;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int p = L.p0 + j * L.P;
+    if (p >= hi) continue;
+    uint32_t y[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+      float y0 = fmaf(h_lo(x[j][e]), k[2 * e], f[2 * e]);
+      float y1 = fmaf(h_hi(x[j][e]), k[2 * e + 1], f[2 * e + 1]);
+      if (a.silu) {
+        y0 = silu(y0);
+        y1 = silu(y1);
+      }
+      y[e] = h_pack(y0, y1);
+    }
+    st_pairs<W>(dst + (int64_t)p * C, y);
+  }
+}
+
+template <int NV, int W>
+__device__ inline float gn_sum(const uint32_t (&x)[NV][W]) {
   float s1 = 0.f;
 #pragma unroll
-  for (int j = 0; j < NV; ++j) s1 += h_lo(x[j]) + h_hi(x[j]);  // absent pixels are zero
-  const float n = (float)a.HW * (float)cg;
-  const float mean = block_sum_1024(s1, red) / n;
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int e = 0; e < W; ++e) s1 += h_lo(x[j][e]) + h_hi(x[j][e]);  // absent pixels are zero
+  return s1;
+}
+
+template <int NV, int W>
+__device__ inline float gn_sqdev(const GnLane<2 * W>& L, int hi, float mean,
+                                 const uint32_t (&x)[NV][W]) {
   float s2 = 0.f;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    if (on && p0 + j * P < a.HW) {
-      const float d0 = h_lo(x[j]) - mean, d1 = h_hi(x[j]) - mean;
-      s2 += d0 * d0 + d1 * d1;
-    }
-  }
-  const float rstd = rsqrtf(block_sum_1024(s2, red) / n + a.eps);
-  if (!on) return;
-  const float k0 = rstd * a.gamma[c], k1 = rstd * a.gamma[c + 1];
-  const float f0 = a.beta[c] - mean * k0, f1 = a.beta[c + 1] - mean * k1;
-  _Float16* dst = a.out + (int64_t)row * a.HW * C + c;
+    if (L.on && L.p0 + j * L.P < hi) {
 #pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int p = p0 + j * P;
-    if (p >= a.HW) continue;
-    float y0 = fmaf(h_lo(x[j]), k0, f0), y1 = fmaf(h_hi(x[j]), k1, f1);
-    if (a.silu) {
-      y0 = silu(y0);
-      y1 = silu(y1);
+      for (int e = 0; e < W; ++e) {
+        const float d0 = h_lo(x[j][e]) - mean, d1 = h_hi(x[j][e]) - mean;
+        s2 += d0 * d0 + d1 * d1;
+      }
     }
-    *(uint32_t*)(dst + (int64_t)p * C) =
-        (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y0) |
-        ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y1) << 16);
   }
+  return s2;
+}
+
+template <int NV, int W>
+__global__ void __launch_bounds__(GN1_T) gn_group_k(GnArgs a) {
+  __shared__ float red[GN1_T / 64];
+  const int C = a.C1 + a.C2, cg = C / a.G;
+  const int row = blockIdx.x / a.G, g = blockIdx.x % a.G;
+  const GnLane<2 * W> L(a, row, g, 0);
+  uint32_t x[NV][W];
+  gn_load<NV, W>(L, a.HW, x);
+  const float n = (float)a.HW * (float)cg;
+  const float mean = block_sum_1024(gn_sum<NV, W>(x), red) / n;
+  const float rstd = rsqrtf(block_sum_1024(gn_sqdev<NV, W>(L, a.HW, mean, x), red) / n + a.eps);
+  if (!L.on) return;
+  gn_store<NV, W>(a, L, row, a.HW, mean, rstd, x);
 }
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
@@ -563,10 +657,10 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
 // deviations from it (two exact passes over registers).  gn_split_apply_k:
 // merges the S partials of its pair in range order (pairwise update, float64),
 // then normalises its range (+ affine, SiLU).
-template <int NV>
+template <int NV, int W>
 __global__ void __launch_bounds__(GN1_T) gn_part_k(GnArgs a, int S) {
   __shared__ float red[GN1_T / 64];
-  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
+  const int C = a.C1 + a.C2, cg = C / a.G;
   const int pair = blockIdx.x / S, sp = blockIdx.x % S;
   const int row = pair / a.G, g = pair % a.G;
   const int HWs = (a.HW + S - 1) / S;
@@ -576,63 +670,31 @@ __global__ void __launch_bounds__(GN1_T) gn_part_k(GnArgs a, int S) {
     if (threadIdx.x == 0) out[0] = out[1] = 0.f;
     return;
   }
-  const int t = threadIdx.x;
-  const bool on = t < P * vpp;
-  const int v = on ? t % vpp : 0, p0 = lo + (on ? t / vpp : 0);
-  const int c = g * cg + 2 * v;
-  const bool first = c < a.C1;
-  const int ld = first ? a.C1 : a.C2;
-  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
-                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
-  uint32_t x[NV];
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int p = p0 + j * P;
-    x[j] = (on && p < hi) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
-  }
-  float s1 = 0.f;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) s1 += h_lo(x[j]) + h_hi(x[j]);
+  const GnLane<2 * W> L(a, row, g, lo);
+  uint32_t x[NV][W];
+  gn_load<NV, W>(L, hi, x);
   const float n = (float)(hi - lo) * (float)cg;
-  const float mean = block_sum_1024(s1, red) / n;
-  float s2 = 0.f;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    if (on && p0 + j * P < hi) {
-      const float d0 = h_lo(x[j]) - mean, d1 = h_hi(x[j]) - mean;
-      s2 += d0 * d0 + d1 * d1;
-    }
-  }
-  const float m2 = block_sum_1024(s2, red);
-  if (t == 0) {
+  const float mean = block_sum_1024(gn_sum<NV, W>(x), red) / n;
+  const float m2 = block_sum_1024(gn_sqdev<NV, W>(L, hi, mean, x), red);
+  if (threadIdx.x == 0) {
     out[0] = mean;
     out[1] = m2;
   }
 }
 
-template <int NV>
+template <int NV, int W>
 __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
   __shared__ float st[2];
-  const int C = a.C1 + a.C2, cg = C / a.G, vpp = cg / 2, P = GN1_T / vpp;
+  const int cg = (a.C1 + a.C2) / a.G;
   const int pair = blockIdx.x / S, sp = blockIdx.x % S;
   const int row = pair / a.G, g = pair % a.G;
   const int HWs = (a.HW + S - 1) / S;
   const int lo = sp * HWs, hi = min(a.HW, lo + HWs);
-  const int t = threadIdx.x;
-  const bool on = t < P * vpp && lo < hi;
-  const int v = on ? t % vpp : 0, p0 = lo + (on ? t / vpp : 0);
-  const int c = g * cg + 2 * v;
-  const bool first = c < a.C1;
-  const int ld = first ? a.C1 : a.C2;
-  const _Float16* src = first ? a.src1 + (int64_t)row * a.HW * a.C1 + c
-                              : a.src2 + (int64_t)row * a.HW * a.C2 + (c - a.C1);
-  uint32_t x[NV];  // issued first: their latency overlaps the merge below
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int p = p0 + j * P;
-    x[j] = (on && p < hi) ? *(const uint32_t*)(src + (int64_t)p * ld) : 0u;
-  }
-  if (t == 0) {
+  GnLane<2 * W> L(a, row, g, lo);
+  L.on = L.on && lo < hi;
+  uint32_t x[NV][W];  // issued first: their latency overlaps the merge below
+  gn_load<NV, W>(L, hi, x);
+  if (threadIdx.x == 0) {
     double n = 0.0, mean = 0.0, m2 = 0.0;
     for (int q = 0; q < S; ++q) {
       const int qlo = q * HWs, qhi = min(a.HW, qlo + HWs);
@@ -643,28 +705,36 @@ __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
     st[1] = rsqrtf((float)(m2 / n) + a.eps);
   }
   __syncthreads();
-  if (!on) return;
-  const float mean = st[0], rstd = st[1];
-  const float k0 = rstd * a.gamma[c], k1 = rstd * a.gamma[c + 1];
-  const float f0 = a.beta[c] - mean * k0, f1 = a.beta[c + 1] - mean * k1;
-  _Float16* dst = a.out + (int64_t)row * a.HW * C + c;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int p = p0 + j * P;
-    if (p >= hi) continue;
-    float y0 = fmaf(h_lo(x[j]), k0, f0), y1 = fmaf(h_hi(x[j]), k1, f1);
-    if (a.silu) {
-      y0 = silu(y0);
-      y1 = silu(y1);
-    }
-    *(uint32_t*)(dst + (int64_t)p * C) =
-        (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y0) |
-        ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y1) << 16);
-  }
+  if (!L.on) return;
+  gn_store<NV, W>(a, L, row, hi, st[0], st[1], x);
 }
 
 constexpr int GN_SPLIT_MAX = 8;
 constexpr int GN_SPLIT_TARGET = 256;  // pairs below which the split form is considered
+
+// Launch the one-workgroup kernels with W packed pairs per access and the
+// smallest register array (NV rounds, NV * W <= 32 dwords) that holds nv rounds.
+template <int W>
+hipError_t gn_one(const GnArgs& a, int rows, int nv, int S, hipStream_t s) {
+  const int pairs = rows * a.G;
+  const dim3 blk(GN1_T);
+  auto go = [&](auto nvc) {
+    constexpr int NV = decltype(nvc)::value;
+    if (S > 1) {
+      const dim3 grid((unsigned)(pairs * S));
+      hipLaunchKernelGGL((gn_part_k<NV, W>), grid, blk, 0, s, a, S);
+      hipLaunchKernelGGL((gn_split_apply_k<NV, W>), grid, blk, 0, s, a, S);
+    } else {
+      hipLaunchKernelGGL((gn_group_k<NV, W>), dim3((unsigned)pairs), blk, 0, s, a);
+    }
+    return hipGetLastError();
+  };
+  if (nv <= 4) return go(std::integral_constant<int, 4>{});
+  if (nv <= 8 && W >= 2) return go(std::integral_constant<int, 8>{});
+  if (nv <= 16 && W <= 2) return go(std::integral_constant<int, 16>{});
+  if (nv <= 32 && W == 1) return go(std::integral_constant<int, 32>{});
+  return hipErrorInvalidValue;
+}
 
 hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
   const int C = a.C1 + a.C2;
@@ -672,43 +742,33 @@ hipError_t gn_launch(const GnArgs& a, int rows, hipStream_t s) {
     return hipErrorInvalidValue;
   const int cg = C / a.G;
   const int pairs = rows * a.G;
-  // the split form pays a second launch: worth it only where one workgroup per pair
-  // would walk more than 16 pixel rounds (or not fit at all)
-  const bool long_pairs = cg % 2 == 0 && cg / 2 <= GN1_T &&
-                          ceil_div(a.HW, GN1_T / (cg / 2)) > 16;
-  if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / 2 <= GN1_T && pairs < GN_SPLIT_TARGET &&
-      a.part_chunks >= GN_SPLIT_MAX && long_pairs) {
-    const int S = std::min(GN_SPLIT_MAX, std::max(2, 2 * GN_SPLIT_TARGET / pairs));
-    const int P = GN1_T / (cg / 2);
-    const int nv = (int)ceil_div(ceil_div(a.HW, S), P);
-    if (nv <= GN1_NV) {
-      const dim3 grid((unsigned)(pairs * S)), blk(GN1_T);
-      if (nv <= 4) {
-        hipLaunchKernelGGL(gn_part_k<4>, grid, blk, 0, s, a, S);
-        hipLaunchKernelGGL(gn_split_apply_k<4>, grid, blk, 0, s, a, S);
-      } else if (nv <= 16) {
-        hipLaunchKernelGGL(gn_part_k<16>, grid, blk, 0, s, a, S);
-        hipLaunchKernelGGL(gn_split_apply_k<16>, grid, blk, 0, s, a, S);
-      } else {
-        hipLaunchKernelGGL(gn_part_k<GN1_NV>, grid, blk, 0, s, a, S);
-        hipLaunchKernelGGL(gn_split_apply_k<GN1_NV>, grid, blk, 0, s, a, S);
-      }
-      return hipGetLastError();
+  // widest access (2, 4 or 8 channels) that every source, the group size and
+  // the pointers allow; the rounds a thread holds shrink in proportion
+  const uintptr_t al = (uintptr_t)a.src1 | (uintptr_t)a.src2 | (uintptr_t)a.out;
+  int vw = 2;
+  for (int w : {8, 4})
+    if (cg % w == 0 && a.C1 % w == 0 && a.C2 % w == 0 && al % (2 * w) == 0) {
+      vw = w;
+      break;
     }
-  }
-  if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / 2 <= GN1_T) {
-    const int P = GN1_T / (cg / 2);                  // pixels per round
-    const int nv = (int)ceil_div(a.HW, P);           // rounds
-    if (nv <= GN1_NV) {
-      const dim3 grid((unsigned)(rows * a.G)), blk(GN1_T);
-      if (nv <= 4)
-        hipLaunchKernelGGL(gn_group_k<4>, grid, blk, 0, s, a);
-      else if (nv <= 16)
-        hipLaunchKernelGGL(gn_group_k<16>, grid, blk, 0, s, a);
-      else
-        hipLaunchKernelGGL(gn_group_k<GN1_NV>, grid, blk, 0, s, a);
-      return hipGetLastError();
+  auto fits = [&](int64_t nv) { return nv <= (vw == 8 ? 8 : vw == 4 ? 16 : 32); };
+  auto one = [&](int nv, int S) {
+    return vw == 8 ? gn_one<4>(a, rows, nv, S, s)
+         : vw == 4 ? gn_one<2>(a, rows, nv, S, s)
+                   : gn_one<1>(a, rows, nv, S, s);
+  };
+  if (cg % 2 == 0 && a.C1 % 2 == 0 && cg / vw <= GN1_T) {
+    const int P = GN1_T / (cg / vw);  // pixels per round
+    // the split form pays a second launch: worth it only where one workgroup
+    // per pair would walk more than 16 two-channel rounds
+    const bool long_pairs = cg / 2 <= GN1_T && ceil_div(a.HW, GN1_T / (cg / 2)) > 16;
+    if (pairs < GN_SPLIT_TARGET && a.part_chunks >= GN_SPLIT_MAX && long_pairs) {
+      const int S = std::min(GN_SPLIT_MAX, std::max(2, 2 * GN_SPLIT_TARGET / pairs));
+      const int64_t nv = ceil_div(ceil_div(a.HW, S), P);
+      if (fits(nv)) return one((int)nv, S);
     }
+    const int64_t nv = ceil_div(a.HW, P);  // rounds
+    if (fits(nv)) return one((int)nv, 1);
   }
   const GnShape sh = gn_shape(C);
   const int nchunks = (int)ceil_div(a.HW, sh.P);
