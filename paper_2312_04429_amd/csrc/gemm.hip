@@ -538,12 +538,14 @@ __device__ __forceinline__ void mma_tile(const _Float16* __restrict__ a,
   }
 }
 
-template <int MODE, int BM, int BN, int STAGES, bool LN, int U>
-__global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
+// NW waves: 2 x 2 wave tiles (4) or 2 x 4 (8, half the columns per wave).
+template <int MODE, int BM, int BN, int STAGES, bool LN, int U, int NW>
+__global__ void __launch_bounds__(NW * 64) gemm_s(GemmArgs g, int kt_per_split) {
   static_assert(U >= 1 && STAGES >= 2 * U, "ring must hold two groups of U tiles");
-  constexpr int WM = BM / 2, WN = BN / 2;
+  static_assert(NW == 4 || NW == 8, "waves per workgroup");
+  constexpr int WM = BM / 2, WN = BN / (NW / 2);
   constexpr int FM = WM / 16, FN = WN / 16;
-  constexpr int AJ = BM / 32, BJ = BN / 32;  // 8-row groups per wave per tile (A, B)
+  constexpr int AJ = BM / (8 * NW), BJ = BN / (8 * NW);  // 8-row groups per wave per tile
   constexpr int OPS = AJ + BJ;               // loads per wave per tile
   constexpr int TILE_H = (BM + BN) * 64;     // halfs per ring buffer
   extern __shared__ __align__(16) unsigned char smem[];
@@ -551,7 +553,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases in SGPRs
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   const int li = lane & 15, kc = lane >> 4;
   const int ntn = (g.N + BN - 1) / BN;
   const int mtn = (int)((g.M + BM - 1) / BM);
@@ -561,7 +563,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   const int nk = g.K / 64;
   const int kt0 = blockIdx.z * kt_per_split;
   const int kt1 = min(nk, kt0 + kt_per_split);
-  // loader geometry: group j of this wave covers rows (j * 4 + wave) * 8 ..+8;
+  // loader geometry: group j of this wave covers rows (j * NW + wave) * 8 ..+8;
   // lane l loads row +l/8, chunk slot l%8, i.e. k chunk (l%8) ^ (l/8)
   const int lrow = lane >> 3;
   const int cch = (lane & 7) ^ lrow;
@@ -573,7 +575,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   int a_b[AJ], a_oy[AJ], a_ox[AJ];
 #pragma unroll
   for (int j = 0; j < AJ; ++j) {
-    a_m[j] = m0 + (j * 4 + wave) * 8 + lrow;
+    a_m[j] = m0 + (j * NW + wave) * 8 + lrow;
     a_b[j] = a_oy[j] = a_ox[j] = 0;
     if (MODE == 1 && a_m[j] < g.M) {
       const int hw = g.Ho * g.Wo;
@@ -629,7 +631,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   a_offsets();
 #pragma unroll
   for (int j = 0; j < BJ; ++j) {
-    const int n = n0 + (j * 4 + wave) * 8 + lrow;
+    const int n = n0 + (j * NW + wave) * 8 + lrow;
     boff[j] = (n < g.N) ? (uint32_t)(((int64_t)n * g.ldw + t_k0 + cch * 8) * 2) : OOB;
   }
   // request the next tile in k order into ring buffer `buf`, then advance
@@ -641,13 +643,13 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
     // readfirstlane loop around every load)
     if (__builtin_amdgcn_readfirstlane((int)t_first) != 0) {
 #pragma unroll
-      for (int j = 0; j < AJ; ++j) lds_dma16(rs1, aoff[j], A + (j * 4 + wave) * 512);
+      for (int j = 0; j < AJ; ++j) lds_dma16(rs1, aoff[j], A + (j * NW + wave) * 512);
     } else {
 #pragma unroll
-      for (int j = 0; j < AJ; ++j) lds_dma16(rs2, aoff[j], A + (j * 4 + wave) * 512);
+      for (int j = 0; j < AJ; ++j) lds_dma16(rs2, aoff[j], A + (j * NW + wave) * 512);
     }
 #pragma unroll
-    for (int j = 0; j < BJ; ++j) lds_dma16(rsw, boff[j], Bt + (j * 4 + wave) * 512);
+    for (int j = 0; j < BJ; ++j) lds_dma16(rsw, boff[j], Bt + (j * NW + wave) * 512);
     t_k0 += 64;
 #pragma unroll
     for (int j = 0; j < BJ; ++j) boff[j] += 128;
@@ -688,7 +690,7 @@ __global__ void __launch_bounds__(256) gemm_s(GemmArgs g, int kt_per_split) {
   // 16-byte chunks per k tile, shifted by the row's first value (k = 0, in
   // chunk slot r & 7) so that the one-pass variance does not cancel: the
   // shifted pair d (float16) enters sum d and sum d^2 through float32 dot2.
-  constexpr int TPR = 256 / BM, CPT = 8 / TPR;
+  constexpr int TPR = NW * 64 / BM, CPT = 8 / TPR;
   const int st_row = tid / TPR, st_slot = (tid % TPR) * CPT;
   half2v st_shift = {(_Float16)0.f, (_Float16)0.f};
   const half2v st_one = {(_Float16)1.f, (_Float16)1.f};
@@ -896,7 +898,7 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int MODE, int BM, int BN, int STAGES, bool LN, int U = 1>
+template <int MODE, int BM, int BN, int STAGES, bool LN, int U = 1, int NW = 4>
 hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
       (int64_t)g.N * g.ldw * 2 >= 0x80000000ll)
@@ -904,7 +906,7 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
   const size_t lds = (size_t)STAGES * (BM + BN) * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES, LN, U>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_s<MODE, BM, BN, STAGES, LN, U, NW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -921,8 +923,8 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
                        (double)g.M * (g.geglu ? g.N / 2 : g.N) * (g.out_f32 ? 4 : 2);
   const TraceEv ev =
       trace_begin(fam, flops, bytes, TraceShape{g.M, g.N, g.K, BM * 10000 + BN * 10 + splits});
-  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN, U>), grid, dim3(256), (uint32_t)lds, s,
-                        ev.a, ev.b, 0u, g, kps);
+  hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN, U, NW>), grid, dim3(NW * 64),
+                        (uint32_t)lds, s, ev.a, ev.b, 0u, g, kps);
   if (splits > 1) {
     const int64_t total = g.M * (int64_t)(g.N / 4);
     const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
@@ -932,11 +934,11 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
 }
 
 // A folded LayerNorm needs every k tile of a row in one workgroup: no split.
-template <int MODE, int BM, int BN, int STAGES, int U = 1>
+template <int MODE, int BM, int BN, int STAGES, int U = 1, int NW = 4>
 hipError_t launch_s(const GemmArgs& g, int splits, hipStream_t s) {
   if constexpr (MODE == 0)
-    if (g.ln_c1) return launch_s_t<0, BM, BN, STAGES, true, U>(g, 1, s);
-  return launch_s_t<MODE, BM, BN, STAGES, false, U>(g, splits, s);
+    if (g.ln_c1) return launch_s_t<0, BM, BN, STAGES, true, U, NW>(g, 1, s);
+  return launch_s_t<MODE, BM, BN, STAGES, false, U, NW>(g, splits, s);
 }
 
 // Streamed kernel when every 64-deep k tile lies inside one source and tap.
@@ -990,10 +992,17 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
     // 4096 rows when wide with K >= 1280 or deep with N >= 1280: q|k|v 4096x3840x1280
     // 76.6 -> 55.6 us, 4096x1280x5120 85.1 -> 74.0 us; the 640-channel
     // convolutions and 16384-row products below 2560 columns stay at 64 x 128)
+    // 128 x 128 tiles run eight waves (2 x 4 wave tiles of 64 x 32): half the
+    // accumulators per wave, two waves per SIMD from one workgroup (graph-timed:
+    // 16384 x 5120 x 640 182 -> 168 us, 65536 x 2560 x 320 258 -> 226 us, the
+    // 320-channel convolution over 65536 pixels 161 -> 148 us); dense products
+    // over at least 8192 rows and 960 columns take them too (8192 x 960 x 320
+    // 17.0 -> 14.3 us, 8192 x 2560 x 320 32.7 -> 30.2 us against 64 x 128)
     const bool big = (g.N >= 2560 && t128 >= 1536) || g.K >= 8192 || g.N <= 320 ||
                      (g.M >= 4096 && g.N >= 2560 && g.K >= 1280) ||
-                     (g.M >= 4096 && g.N >= 1280 && g.K >= 4096);
-    return big ? launch_s<MODE, 128, 128, GEMM_S128>(g, 1, s)
+                     (g.M >= 4096 && g.N >= 1280 && g.K >= 4096) ||
+                     (MODE == 0 && g.M >= 8192 && g.N >= 960);
+    return big ? launch_s<MODE, 128, 128, GEMM_S128, 1, 8>(g, 1, s)
                : launch_s<MODE, 64, 128, 2>(g, 1, s);
   }
   if (t128 >= 128 && nk >= 128)

@@ -3,7 +3,8 @@ kernel) against the oracle's float32 layers on the same float16-valued
 inputs.  Shapes cover every tile configuration of both kernels (register
 staged for K or channel counts off the 64 grid; streamed 64x64 with and
 without split-K (including one workgroup per CU over a long K, and at most
-128 rows with ragged N over a long K), 64x128, 128x128 for large grids and for
+128 rows with ragged N over a long K), 64x128, 128x128 with eight waves for
+large grids (dense and convolution, ragged rows and columns) and with four for
 long K with split),
 ragged M / N / K edges, stride 2 and the fused nearest x2 upsample."""
 import numpy as np
@@ -23,7 +24,8 @@ def _h(a):
                                    (128, 1280, 11520), (8192, 640, 320), (4096, 4096, 512),
                                    (513, 2560, 1280), (130, 96, 136), (2048, 1024, 8192),
                                    (8200, 700, 192), (4100, 4000, 512), (512, 1280, 1280),
-                                   (500, 1000, 768), (100, 1000, 4096)])
+                                   (500, 1000, 768), (100, 1000, 4096), (8192, 960, 320),
+                                   (8200, 1000, 320), (4096, 2560, 1280)])
 def test_linear(M, N, K):
     import paper_2312_04429_amd as P
     print(f"op linear M={M} N={N} K={K}", flush=True)
@@ -68,7 +70,7 @@ def test_split_k_repeatable():
     (2, 32, 32, 640, 640, 2, 0), (2, 8, 8, 1280, 1280, 1, 0), (2, 16, 16, 96, 32, 1, 1),
     (3, 8, 8, 640, 640, 1, 1), (2, 8, 6, 64, 40, 2, 0), (2, 64, 64, 64, 1024, 1, 0),
     (2, 32, 32, 1024, 1024, 1, 0), (2, 64, 64, 64, 640, 1, 0), (2, 32, 32, 128, 256, 1, 0),
-    (1, 8, 8, 640, 1000, 1, 0)])
+    (1, 8, 8, 640, 1000, 1, 0), (4, 64, 64, 64, 320, 1, 0), (4, 32, 32, 64, 320, 1, 1)])
 def test_conv3x3(B, H, W, Cin, Cout, stride, up):
     import paper_2312_04429_amd as P
     print(f"op conv B={B} {H}x{W} {Cin}->{Cout} s{stride} up{up}", flush=True)
