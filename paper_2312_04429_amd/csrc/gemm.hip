@@ -1016,6 +1016,9 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   // 2048 x 640 x 2560 22.2 -> 19.6 us and 512 x 1280 x 2560 17.9 -> 15.9 us
   // unsplit, 128 x 3840 x 1280 10.8 -> 9.5 us)
   const bool split = nk > 40 || t64 < 100;
+  // wide products just under the large-grid bound (batch-1 level-1 q|k|v,
+  // 2048 x 1920 x 640: 15.2 -> 12.2 us graph-timed) take 64 x 128 tiles
+  if (!split && t64 >= 768 && g.N >= 1920) return launch_s<MODE, 64, 128, 2>(g, 1, s);
   return launch_s<MODE, 64, 64, GEMM_S64>(g, split ? split_to(t64, 700) : 1, s);
 }
 
