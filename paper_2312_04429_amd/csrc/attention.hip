@@ -38,8 +38,9 @@ constexpr int krow(int dh) { return (dh / 8) % 2 ? dh : dh + 8; }
 // leave compute units idle, e.g. 1024 or 256 queries per head at batch 1).
 // KB: keys per block (64, or 128, which halves the barriers and max
 // reductions per key at the price of registers).
-template <int DH, int QB, int KB>
-__global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
+template <int DH, int QB, int KB, int NW = 4>
+__global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
+  constexpr int NT = NW * 64;  // threads; NW waves of QB query blocks share each K / V^T block
   constexpr int VROW = KB + 8;                 // halfs per LDS V^T row
   constexpr int NH = KB / 16, NS = KB / 32;    // 16-key quarters, 32-key PV steps
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
@@ -47,7 +48,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
   constexpr int KROW = krow(DH);               // halfs per LDS key row
   constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
-  constexpr int KPT = (KCN + 255) / 256, VPT = (VCN + 255) / 256;
+  constexpr int KPT = (KCN + NT - 1) / NT, VPT = (VCN + NT - 1) / NT;
   static_assert(DH % 8 == 0, "head dim");
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                       // [2]
@@ -57,10 +58,10 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   const int li = lane & 15, kc = lane >> 4;
   // 1-D grid; an XCD owns a contiguous range of (row, head, query block) ids so
   // the query blocks of one head share its K / V through that XCD's L2
-  const int nqb = (a.S + 64 * QB - 1) / (64 * QB);
+  const int nqb = (a.S + NW * 16 * QB - 1) / (NW * 16 * QB);
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int qblk = id % nqb, head = (id / nqb) % a.heads, row = id / (nqb * a.heads);
-  const int q0 = qblk * (64 * QB) + wave * (16 * QB);
+  const int q0 = qblk * (NW * 16 * QB) + wave * (16 * QB);
 
   // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8,
   // zero past DH, scaled by scale * log2(e) so the scores come out of the
@@ -112,14 +113,14 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   uint32_t koff[KPT], voff[VPT];
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
-    const int c = tid + i * 256;
+    const int c = tid + i * NT;
     koff[i] = c < KCN ? (uint32_t)((((int64_t)row * a.L + c / KCH) * a.ldk + head * DH +
                                     (c % KCH) * 8) * 2)
                       : OOB;
   }
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
-    const int c = tid + i * 256;
+    const int c = tid + i * NT;
     voff[i] = c < VCN ? (uint32_t)((((int64_t)head * DH + c / (KB / 8)) * a.vt_ld +
                                     (int64_t)row * a.vt_row + (c % (KB / 8)) * 8) * 2)
                       : OOB;
@@ -144,13 +145,13 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   auto stash = [&](int buf, int kb, const uint4(&rk)[KPT], const uint4(&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       if (KCN % 256 == 0 || c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
     }
     if ((kb + 1) * KB <= a.L) {  // uniform: every key of the block is real
 #pragma unroll
       for (int i = 0; i < VPT; ++i) {
-        const int c = tid + i * 256;
+        const int c = tid + i * NT;
         if (VCN % 256 == 0 || c < VCN)
           *(uint4*)&sVt[buf][(c / (KB / 8)) * VROW + (c % (KB / 8)) * 8] = rv[i];
       }
@@ -158,7 +159,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       if (c < VCN) {
         const int d = c / (KB / 8), k8 = (c % (KB / 8)) * 8;
         half8 v = *(const half8*)&rv[i];
@@ -283,7 +284,7 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
     __syncthreads();
   };
   if (ONES)
-    for (int i = tid; i < 2 * KB; i += 256) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
+    for (int i = tid; i < 2 * KB; i += NT) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
   fetch(0, rkA, rvA);
   if (1 < nkb) fetch(1, rkB, rvB);
   stash(0, 0, rkA, rvA);
@@ -319,13 +320,13 @@ __global__ void __launch_bounds__(256) attn_f16(AttnArgs a) {
   }
 }
 
-template <int DH, int QB, int KB>
+template <int DH, int QB, int KB, int NW = 4>
 hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   constexpr int DV = (DH + 15) / 16 * 16, VROW = KB + 8;
   const size_t lds = (size_t)2 * (KB * krow(DH) + DV * VROW) * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB, NW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -337,14 +338,14 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   if ((int64_t)a.rows * a.L * a.ldk * 2 >= 0x80000000ll ||
       (int64_t)a.heads * DH * a.vt_ld * 2 >= 0x80000000ll)
     return hipErrorInvalidValue;
-  dim3 grid((unsigned)(ceil_div(a.S, 64 * QB) * a.heads * a.rows));
+  dim3 grid((unsigned)(ceil_div(a.S, NW * 16 * QB) * a.heads * a.rows));
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
   const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes,
                                  TraceShape{a.S, a.L, (int64_t)a.heads * a.dh,
-                                            DH * 10000 + QB * 1000 + KB});
-  hipExtLaunchKernelGGL((attn_f16<DH, QB, KB>), grid, dim3(256), (uint32_t)lds, s, ev.a, ev.b, 0u,
-                        a);
+                                            DH * 10000 + QB * 1000 + KB + (NW - 4) * 100000});
+  hipExtLaunchKernelGGL((attn_f16<DH, QB, KB, NW>), grid, dim3(NW * 64), (uint32_t)lds, s, ev.a,
+                        ev.b, 0u, a);
   return hipGetLastError();
 }
 
@@ -360,11 +361,14 @@ hipError_t launch(const AttnArgs& a, hipStream_t s) {
       if (ceil_div(a.S, 64) * a.heads * a.rows <= 256) return launch_qb<DH, 1, 128>(a, s);
     return launch_qb<DH, 1, 64>(a, s);
   }
-  // 128-key blocks for 40-dim heads when at most two workgroups per CU exist
-  // (batch 1 at 4,096 queries): the larger register set (216 VGPRs) costs no
-  // occupancy there; on larger grids three 64-key workgroups per CU win
+  // 40-dim heads: eight waves (256 queries) share each K / V^T block, which
+  // halves the block loads and LDS stores per query (graph-timed, interleaved:
+  // 2 x 4096 x 4096 76.8 -> 73.4 us, 16 rows 513 -> 486 us); 128-key blocks
+  // when at most two four-wave workgroups per CU would exist (batch 1 at 4,096
+  // queries), 64-key blocks on larger grids.  Other head dims measured slower
+  // with eight waves.
   if constexpr (DH == 40)
-    if (wgs2 <= 512) return launch_qb<DH, 2, 128>(a, s);
+    return wgs2 <= 512 ? launch_qb<DH, 2, 128, 8>(a, s) : launch_qb<DH, 2, 64, 8>(a, s);
   return launch_qb<DH, 2, 64>(a, s);
 }
 

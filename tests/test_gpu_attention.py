@@ -2,9 +2,10 @@
 Sec. 2.1) against the oracle's float32 attention on the same float16-valued
 inputs, at the head dims of the configurations (16 tiny, 40 / 80 / 160
 SD-1.5, 64 SDXL), the 77-token context with its padded V^T rows, ragged
-query / key counts, and each launch form of the 40-dim heads (one query block
-per wave; two with 128-key blocks at up to 512 workgroups, as at batch 1 over
-4,096 queries; two with 64-key blocks beyond).
+query / key counts, and each launch form (one query block per wave; two, with
+eight waves sharing each key block for 40-dim heads: 128-key blocks at up to
+512 four-wave workgroups, as at batch 1 over 4,096 queries, 64-key blocks
+beyond; two with four waves for the other head dims).
 
 The peaked-score cases drive the online softmax through its rescale branch:
 the kernel keeps a per-query reference maximum and moves it (multiplying the
@@ -67,13 +68,15 @@ def _check(q, k, v, heads, scale, atol):
 # Launch forms (the launcher's rule over wgs2 = ceil(S / 128) * heads * rows):
 # wgs2 < 256 -> one query block per wave with 64-key blocks, or 128-key blocks
 # for 80-dim heads with at most 256 workgroups of 64 queries; otherwise two query
-# blocks per wave, with 128-key blocks for 40-dim heads up to 512 workgroups.
+# blocks per wave: 40-dim heads in eight-wave workgroups (256 queries) with
+# 128-key blocks up to wgs2 = 512 and 64-key blocks beyond, other head dims in
+# four-wave workgroups with 64-key blocks.
 PEAK_CASES = [  # (rows, S, L, heads, dh): form
     (1, 256, 700, 8, 40),    # 1 x 64
-    (2, 2048, 700, 8, 40),   # 2 x 128
-    (3, 4096, 700, 8, 40),   # 2 x 64
-    (2, 2048, 704, 8, 40),   # 2 x 128
-    (1, 4000, 1000, 8, 40),  # 2 x 128, ragged queries and last key block
+    (2, 2048, 700, 8, 40),   # 2 x 128, eight waves
+    (3, 4096, 700, 8, 40),   # 2 x 64, eight waves
+    (2, 2048, 704, 8, 40),   # 2 x 128, eight waves
+    (1, 4000, 1000, 8, 40),  # 2 x 128, eight waves, ragged queries and last key block
     (1, 300, 700, 8, 64),    # 1 x 64
     (2, 2048, 700, 8, 64),   # 2 x 64
     (1, 2100, 700, 8, 80),   # 1 x 64 (264 workgroups of 64 queries)
