@@ -25,7 +25,8 @@ def _h(a):
                                    (513, 2560, 1280), (130, 96, 136), (2048, 1024, 8192),
                                    (8200, 700, 192), (4100, 4000, 512), (512, 1280, 1280),
                                    (500, 1000, 768), (100, 1000, 4096), (8192, 960, 320),
-                                   (8200, 1000, 320), (4096, 2560, 1280)])
+                                   (8200, 1000, 320), (4096, 2560, 1280), (128, 1280, 1280),
+                                   (154, 1000, 768), (250, 3840, 1280)])
 def test_linear(M, N, K):
     import paper_2312_04429_amd as P
     print(f"op linear M={M} N={N} K={K}", flush=True)
