@@ -138,6 +138,139 @@ __device__ inline void store_geglu4(const GemmArgs& g, int64_t m, int na, const 
   }
 }
 
+// Epilogue of a wave's FM x FN quads (row m = mb + i * 16 + li, columns n =
+// nb + j * 16 + kc * 4 ..+3), the same arithmetic as store_out4 /
+// store_geglu4.  The stores could alias the loaded operands as far as the
+// compiler knows, so quad by quad every load (bias, row vector, residual)
+// would cost a memory round trip; here each row block's loads are issued
+// together, unconditionally from clamped addresses, before its stores.
+template <int FM, int FN>
+__device__ inline void epilogue_tile(const GemmArgs& g, int64_t mb, int nb, int li, int kc,
+                                  floatx4 (&acc)[FM][FN]) {
+  const bool vec = g.vec_ok;
+  // bias per column quad, loaded once
+  float bq[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int n = nb + j * 16 + kc * 4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) bq[j][r] = 0.f;
+    if (g.bias) {
+      if (vec && n + 4 <= g.N) {
+        const float4 b = *(const float4*)(g.bias + n);
+        bq[j][0] = b.x; bq[j][1] = b.y; bq[j][2] = b.z; bq[j][3] = b.w;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bq[j][r] = g.bias[n + r < g.N ? n + r : 0];
+      }
+    }
+  }
+  if (g.geglu) {  // quad j = 2 jj holds "a" columns na.., j = 2 jj + 1 the gates na + 16..
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int64_t m = mb + i * 16 + li;
+      if (m >= g.M) continue;
+#pragma unroll
+      for (int jj = 0; jj < FN / 2; ++jj) {
+        const int na = nb + 2 * jj * 16 + kc * 4;
+        if (na + 16 >= g.N) continue;
+        float y[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float av = acc[i][2 * jj][r], gv = acc[i][2 * jj + 1][r];
+          if (g.bias) {
+            av += bq[2 * jj][r];
+            gv += bq[2 * jj + 1][r];
+          }
+          y[r] = av * gelu_erf(gv);
+        }
+        const int oc = (na >> 5) * 16 + (na & 15);
+        _Float16* o = (_Float16*)g.out + m * g.ldo + oc;
+        if (vec) {
+          half4 h;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) h[r] = (_Float16)y[r];
+          *(half4*)o = h;
+        } else {
+          for (int r = 0; r < 4; ++r) o[r] = (_Float16)y[r];
+        }
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int64_t m = mb + i * 16 + li;
+    const int64_t mc = m < g.M ? m : 0;  // a row every load may use
+    float rv[FN][4];
+    half4 res[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = nb + j * 16 + kc * 4;
+      const bool qv = vec && n + 4 <= g.N;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rv[j][r] = 0.f;
+      if (g.rowvec) {
+        const float* p = g.rowvec + (mc / g.rows_div) * (int64_t)g.ld_rowvec;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rv[j][r] = p[n + r < g.N ? n + r : 0];
+      }
+      res[j] = half4{};
+      if (g.residual && !(g.vt && n >= g.vt_col0)) {
+        const _Float16* p = g.residual + mc * g.ld_res;
+        if (qv) {
+          res[j] = *(const half4*)(p + n);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) res[j][r] = p[n + r < g.N ? n + r : 0];
+        }
+      }
+    }
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = nb + j * 16 + kc * 4;
+      if (n >= g.N) continue;
+      const bool qv = vec && n + 4 <= g.N;
+      const int nn = qv ? 4 : min(4, g.N - n);
+      float w[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        w[r] = acc[i][j][r];
+        if (g.bias) w[r] += bq[j][r];
+        if (g.rowvec) w[r] += rv[j][r];
+        if (g.silu) w[r] = silu(w[r]);
+      }
+      if (g.vt && n >= g.vt_col0) {  // transposed columns (no residual on these)
+        _Float16* o = g.vt + (int64_t)(n - g.vt_col0) * g.vt_ld + (m / g.vt_div) * g.vt_stride +
+                      m % g.vt_div;
+        for (int r = 0; r < nn; ++r) o[(int64_t)r * g.vt_ld] = (_Float16)w[r];
+        continue;
+      }
+      if (g.residual)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[r] += (float)res[j][r];
+      if (g.out_f32) {
+        float* o = (float*)g.out + m * g.ldo + n;
+        if (qv)
+          *(float4*)o = make_float4(w[0], w[1], w[2], w[3]);
+        else
+          for (int r = 0; r < nn; ++r) o[r] = w[r];
+      } else {
+        _Float16* o = (_Float16*)g.out + m * g.ldo + n;
+        if (qv) {
+          half4 h;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) h[r] = (_Float16)w[r];
+          *(half4*)o = h;
+        } else {
+          for (int r = 0; r < nn; ++r) o[r] = (_Float16)w[r];
+        }
+      }
+    }
+  }
+}
+
 template <int MODE, int BM, int BN, bool DUAL>
 __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -440,172 +573,7 @@ __global__ void __launch_bounds__(256) gemm_f16(GemmArgs g, int kt_per_split) {
     }
     return;
   }
-  const bool vec = g.vec_ok;
-  if (g.geglu) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int64_t m = m0 + wm * WM + i * 16 + li;
-      if (m >= g.M) continue;
-#pragma unroll
-      for (int jj = 0; jj < FN / 2; ++jj) {
-        const int na = n0 + wn * WN + 2 * jj * 16 + kc * 4;
-        if (na + 16 >= g.N) continue;
-        float a[4], gt[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          a[r] = acc[i][2 * jj][r];
-          gt[r] = acc[i][2 * jj + 1][r];
-        }
-        store_geglu4(g, m, na, a, gt, vec);
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int64_t m = m0 + wm * WM + i * 16 + li;
-    if (m >= g.M) continue;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + kc * 4;
-      if (n >= g.N) continue;
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      store_out4(g, m, n, v, vec && n + 4 <= g.N);
-    }
-  }
-}
-
-// Epilogue of a wave's FM x FN quads (row m = mb + i * 16 + li, columns n =
-// nb + j * 16 + kc * 4 ..+3), the same arithmetic as store_out4 /
-// store_geglu4.  The stores could alias the loaded operands as far as the
-// compiler knows, so quad by quad every load (bias, row vector, residual)
-// would cost a memory round trip; here each row block's loads are issued
-// together, unconditionally from clamped addresses, before its stores.
-template <int FM, int FN>
-__device__ inline void store_tile(const GemmArgs& g, int64_t mb, int nb, int li, int kc,
-                                  floatx4 (&acc)[FM][FN]) {
-  const bool vec = g.vec_ok;
-  // bias per column quad, loaded once
-  float bq[FN][4];
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = nb + j * 16 + kc * 4;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) bq[j][r] = 0.f;
-    if (g.bias) {
-      if (vec && n + 4 <= g.N) {
-        const float4 b = *(const float4*)(g.bias + n);
-        bq[j][0] = b.x; bq[j][1] = b.y; bq[j][2] = b.z; bq[j][3] = b.w;
-      } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bq[j][r] = g.bias[n + r < g.N ? n + r : 0];
-      }
-    }
-  }
-  if (g.geglu) {  // quad j = 2 jj holds "a" columns na.., j = 2 jj + 1 the gates na + 16..
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int64_t m = mb + i * 16 + li;
-      if (m >= g.M) continue;
-#pragma unroll
-      for (int jj = 0; jj < FN / 2; ++jj) {
-        const int na = nb + 2 * jj * 16 + kc * 4;
-        if (na + 16 >= g.N) continue;
-        float y[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float av = acc[i][2 * jj][r], gv = acc[i][2 * jj + 1][r];
-          if (g.bias) {
-            av += bq[2 * jj][r];
-            gv += bq[2 * jj + 1][r];
-          }
-          y[r] = av * gelu_erf(gv);
-        }
-        const int oc = (na >> 5) * 16 + (na & 15);
-        _Float16* o = (_Float16*)g.out + m * g.ldo + oc;
-        if (vec) {
-          half4 h;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) h[r] = (_Float16)y[r];
-          *(half4*)o = h;
-        } else {
-          for (int r = 0; r < 4; ++r) o[r] = (_Float16)y[r];
-        }
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int64_t m = mb + i * 16 + li;
-    const int64_t mc = m < g.M ? m : 0;  // a row every load may use
-    float rv[FN][4];
-    half4 res[FN];
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = nb + j * 16 + kc * 4;
-      const bool qv = vec && n + 4 <= g.N;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) rv[j][r] = 0.f;
-      if (g.rowvec) {
-        const float* p = g.rowvec + (mc / g.rows_div) * (int64_t)g.ld_rowvec;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) rv[j][r] = p[n + r < g.N ? n + r : 0];
-      }
-      res[j] = half4{};
-      if (g.residual && !(g.vt && n >= g.vt_col0)) {
-        const _Float16* p = g.residual + mc * g.ld_res;
-        if (qv) {
-          res[j] = *(const half4*)(p + n);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) res[j][r] = p[n + r < g.N ? n + r : 0];
-        }
-      }
-    }
-    if (m >= g.M) continue;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = nb + j * 16 + kc * 4;
-      if (n >= g.N) continue;
-      const bool qv = vec && n + 4 <= g.N;
-      const int nn = qv ? 4 : min(4, g.N - n);
-      float w[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        w[r] = acc[i][j][r];
-        if (g.bias) w[r] += bq[j][r];
-        if (g.rowvec) w[r] += rv[j][r];
-        if (g.silu) w[r] = silu(w[r]);
-      }
-      if (g.vt && n >= g.vt_col0) {  // transposed columns (no residual on these)
-        _Float16* o = g.vt + (int64_t)(n - g.vt_col0) * g.vt_ld + (m / g.vt_div) * g.vt_stride +
-                      m % g.vt_div;
-        for (int r = 0; r < nn; ++r) o[(int64_t)r * g.vt_ld] = (_Float16)w[r];
-        continue;
-      }
-      if (g.residual)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) w[r] += (float)res[j][r];
-      if (g.out_f32) {
-        float* o = (float*)g.out + m * g.ldo + n;
-        if (qv)
-          *(float4*)o = make_float4(w[0], w[1], w[2], w[3]);
-        else
-          for (int r = 0; r < nn; ++r) o[r] = w[r];
-      } else {
-        _Float16* o = (_Float16*)g.out + m * g.ldo + n;
-        if (qv) {
-          half4 h;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) h[r] = (_Float16)w[r];
-          *(half4*)o = h;
-        } else {
-          for (int r = 0; r < nn; ++r) o[r] = (_Float16)w[r];
-        }
-      }
-    }
-  }
+  epilogue_tile<FM, FN>(g, m0 + wm * WM, n0 + wn * WN, li, kc, acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -908,7 +876,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_s(GemmArgs g, int kt_per_split) 
     }
     return;
   }
-  store_tile<FM, FN>(g, m0 + wm * WM, n0 + wn * WN, li, kc, acc);
+  epilogue_tile<FM, FN>(g, m0 + wm * WM, n0 + wn * WN, li, kc, acc);
 }
 
 // Sum split-K partials in split order and apply the epilogue, four
@@ -957,9 +925,65 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
     } else {
       const int64_t m = e / nq;
       const int n = (int)(e - m * nq) * 4;
+      // the epilogue's operands first: their loads overlap those of the partials
+      float b[4] = {0.f, 0.f, 0.f, 0.f}, rv[4] = {0.f, 0.f, 0.f, 0.f};
+      half4 res = {};
+      if (g.bias) {
+        const float4 q = *(const float4*)(g.bias + n);
+        b[0] = q.x; b[1] = q.y; b[2] = q.z; b[3] = q.w;
+      }
+      if (g.rowvec) {
+        const float* p = g.rowvec + (m / g.rows_div) * (int64_t)g.ld_rowvec + n;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rv[r] = p[r];
+      }
+      const bool vtc = g.vt && n >= g.vt_col0;
+      if (g.residual && !vtc) {
+        const _Float16* p = g.residual + m * g.ld_res + n;
+        if (g.vec_ok) {
+          res = *(const half4*)p;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) res[r] = p[r];
+        }
+      }
       float v[1][4] = {{0.f, 0.f, 0.f, 0.f}};
       sum_splits<1>(g.partial + m * g.N + n, 0, MN, splits, v);
-      store_out4(g, m, n, v[0], g.vec_ok);
+      float w[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        w[r] = v[0][r];
+        if (g.bias) w[r] += b[r];
+        if (g.rowvec) w[r] += rv[r];
+        if (g.silu) w[r] = silu(w[r]);
+      }
+      if (vtc) {  // transposed columns (no residual on these)
+        _Float16* o = g.vt + (int64_t)(n - g.vt_col0) * g.vt_ld + (m / g.vt_div) * g.vt_stride +
+                      m % g.vt_div;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(int64_t)r * g.vt_ld] = (_Float16)w[r];
+        continue;
+      }
+      if (g.residual)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[r] += (float)res[r];
+      if (g.out_f32) {
+        float* o = (float*)g.out + m * g.ldo + n;
+        if (g.vec_ok)
+          *(float4*)o = make_float4(w[0], w[1], w[2], w[3]);
+        else
+          for (int r = 0; r < 4; ++r) o[r] = w[r];
+      } else {
+        _Float16* o = (_Float16*)g.out + m * g.ldo + n;
+        if (g.vec_ok) {
+          half4 h;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) h[r] = (_Float16)w[r];
+          *(half4*)o = h;
+        } else {
+          for (int r = 0; r < 4; ++r) o[r] = (_Float16)w[r];
+        }
+      }
     }
   }
 }
