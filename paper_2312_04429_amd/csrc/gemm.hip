@@ -796,6 +796,16 @@ __global__ void __launch_bounds__(NW * 64) gemm_s(GemmArgs g, int kt_per_split) 
   half2v st_shift = {(_Float16)0.f, (_Float16)0.f};
   const half2v st_one = {(_Float16)1.f, (_Float16)1.f};
   float st_s1 = 0.f, st_s2 = 0.f;
+  // the folded LayerNorm's column sums c1 of this wave's columns, requested
+  // now so that the epilogue does not wait for them
+  float c1v[LN ? FN : 1][4];
+  if (LN)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + kc * 4;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) c1v[j][r] = n + r < g.N ? g.ln_c1[n + r] : 0.f;
+    }
   for (int kt = kt0; kt < kt1; kt += U) {
     wait_vmcnt<(STAGES - 2 * U) * OPS>();  // this wave's loads of tiles kt .. kt+U-1 have landed
     ring_barrier();                        // everyone's have; the previous U buffers are free
@@ -842,14 +852,9 @@ __global__ void __launch_bounds__(NW * 64) gemm_s(GemmArgs g, int kt_per_split) 
     for (int i = 0; i < FM; ++i) {
       const float2 st = lnst[wm * WM + i * 16 + li];
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int n = n0 + wn * WN + j * 16 + kc * 4;
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float c1 = n + r < g.N ? g.ln_c1[n + r] : 0.f;
-          acc[i][j][r] = st.y * (acc[i][j][r] - st.x * c1);
-        }
-      }
+        for (int r = 0; r < 4; ++r) acc[i][j][r] = st.y * (acc[i][j][r] - st.x * c1v[j][r]);
     }
   }
 

@@ -572,16 +572,30 @@ __device__ inline void gn_load(const GnLane<2 * W>& L, int hi, uint32_t (&x)[NV]
   }
 }
 
+// this lane's affine parameters, requested with its values (before the
+// reductions, so their latency is hidden)
+template <int W>
+__device__ inline void gn_affine(const GnArgs& a, const GnLane<2 * W>& L, float (&gam)[2 * W],
+                                 float (&bet)[2 * W]) {
+  const int c = L.on ? L.c : 0;
+#pragma unroll
+  for (int e = 0; e < 2 * W; ++e) {
+    gam[e] = a.gamma[c + e];
+    bet[e] = a.beta[c + e];
+  }
+}
+
 // normalise, affine, optional SiLU and store rounds j < NV of pixels below hi
 template <int NV, int W>
 __device__ inline void gn_store(const GnArgs& a, const GnLane<2 * W>& L, int row, int hi,
-                                float mean, float rstd, const uint32_t (&x)[NV][W]) {
+                                float mean, float rstd, const float (&gam)[2 * W],
+                                const float (&bet)[2 * W], const uint32_t (&x)[NV][W]) {
   const int C = a.C1 + a.C2;
   float k[2 * W], f[2 * W];
 #pragma unroll
   for (int e = 0; e < 2 * W; ++e) {
-    k[e] = rstd * a.gamma[L.c + e];
-    f[e] = a.beta[L.c + e] - mean * k[e];
+    k[e] = rstd * gam[e];
+    f[e] = bet[e] - mean * k[e];
   }
   _Float16* dst = a.out + (int64_t)row * a.HW * C + L.c;
 #pragma unroll
@@ -638,11 +652,13 @@ __global__ void __launch_bounds__(GN1_T) gn_group_k(GnArgs a) {
   const GnLane<2 * W> L(a, row, g, 0);
   uint32_t x[NV][W];
   gn_load<NV, W>(L, a.HW, x);
+  float gam[2 * W], bet[2 * W];
+  gn_affine<W>(a, L, gam, bet);
   const float n = (float)a.HW * (float)cg;
   const float mean = block_sum_1024(gn_sum<NV, W>(x), red) / n;
   const float rstd = rsqrtf(block_sum_1024(gn_sqdev<NV, W>(L, a.HW, mean, x), red) / n + a.eps);
   if (!L.on) return;
-  gn_store<NV, W>(a, L, row, a.HW, mean, rstd, x);
+  gn_store<NV, W>(a, L, row, a.HW, mean, rstd, gam, bet, x);
 }
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)ceil_div(n, 256); }
@@ -694,6 +710,8 @@ __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
   L.on = L.on && lo < hi;
   uint32_t x[NV][W];  // issued first: their latency overlaps the merge below
   gn_load<NV, W>(L, hi, x);
+  float gam[2 * W], bet[2 * W];
+  gn_affine<W>(a, L, gam, bet);
   if (threadIdx.x == 0) {
     double n = 0.0, mean = 0.0, m2 = 0.0;
     for (int q = 0; q < S; ++q) {
@@ -706,7 +724,7 @@ __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
   }
   __syncthreads();
   if (!L.on) return;
-  gn_store<NV, W>(a, L, row, hi, st[0], st[1], x);
+  gn_store<NV, W>(a, L, row, hi, st[0], st[1], gam, bet, x);
 }
 
 constexpr int GN_SPLIT_MAX = 8;
