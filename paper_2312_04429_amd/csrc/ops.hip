@@ -181,10 +181,24 @@ __global__ void __launch_bounds__(256) gn_apply_k(GnArgs a, int nchunks, int Q) 
   const int TPG = 256 / a.G;  // G is a power of two in [4, 256]
   const int g = t / TPG, s = t % TPG;
   double n = 0.0, mean = 0.0, m2 = 0.0;
-  for (int c = s; c < nchunks; c += TPG) {
-    const float* pp = a.part + ((int64_t)(row * nchunks + c) * a.G + g) * 2;
-    chan_merge(n, mean, m2, (double)(min(sh.P, a.HW - c * sh.P) * cg), (double)pp[0],
-               (double)pp[1]);
+  // eight chunks' partials requested together, then merged in chunk order
+  constexpr int PF = 8;
+  for (int c0 = s; c0 < nchunks; c0 += PF * TPG) {
+    float pm[PF], pv[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int c = c0 + u * TPG;
+      const float* pp = a.part + ((int64_t)(row * nchunks + (c < nchunks ? c : 0)) * a.G + g) * 2;
+      pm[u] = pp[0];
+      pv[u] = pp[1];
+    }
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int c = c0 + u * TPG;
+      if (c < nchunks)
+        chan_merge(n, mean, m2, (double)(min(sh.P, a.HW - c * sh.P) * cg), (double)pm[u],
+                   (double)pv[u]);
+    }
   }
   for (int o = 1; o < TPG; o <<= 1) {
     const double nb = __shfl_xor(n, o, 64), mb = __shfl_xor(mean, o, 64),
@@ -713,11 +727,20 @@ __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
   float gam[2 * W], bet[2 * W];
   gn_affine<W>(a, L, gam, bet);
   if (threadIdx.x == 0) {
+    // every range's partials requested together (S <= 8), then merged in order
+    float pm[8], pv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float* pp = a.part + ((int64_t)pair * S + (q < S ? q : 0)) * 2;
+      pm[q] = pp[0];
+      pv[q] = pp[1];
+    }
     double n = 0.0, mean = 0.0, m2 = 0.0;
-    for (int q = 0; q < S; ++q) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (q >= S) break;
       const int qlo = q * HWs, qhi = min(a.HW, qlo + HWs);
-      const float* pp = a.part + ((int64_t)pair * S + q) * 2;
-      chan_merge(n, mean, m2, (double)(max(0, qhi - qlo) * cg), (double)pp[0], (double)pp[1]);
+      chan_merge(n, mean, m2, (double)(max(0, qhi - qlo) * cg), (double)pm[q], (double)pv[q]);
     }
     st[0] = (float)mean;
     st[1] = rsqrtf((float)(m2 / n) + a.eps);
@@ -728,6 +751,7 @@ __global__ void __launch_bounds__(GN1_T) gn_split_apply_k(GnArgs a, int S) {
 }
 
 constexpr int GN_SPLIT_MAX = 8;
+static_assert(GN_SPLIT_MAX <= 8, "gn_split_apply_k requests at most eight ranges' partials");
 constexpr int GN_SPLIT_TARGET = 256;  // pairs below which the split form is considered
 
 // Launch the one-workgroup kernels with W packed pairs per access and the
