@@ -3,10 +3,12 @@
 // latent tokens and cross-attention to the text context (Sec. 2.1: text
 // conditioning enters the UNet through cross-attention).
 //
-// Work split: one workgroup of four waves = 64 or 128 queries of one (row,
-// head); each wave owns one or two 16-query column blocks (QB).  Keys stream
-// in blocks of 64 or 128 (KB) through two register sets (fetched two blocks
-// ahead) and a double-buffered LDS, one barrier per block.  The kernel computes the
+// Work split: one workgroup of 4, 8 or 16 waves = 32 to 256 queries of one
+// (row, head); each query wave owns one or two 16-query column blocks (QB),
+// and where the grid is small two sets of query waves split every key block
+// between them (key sets, merged at the end).  Keys stream in blocks through
+// two register sets (fetched two blocks ahead) and a double-buffered LDS, one
+// barrier per block.  The kernel computes the
 // transposed score block S^T = K Q^T so that every accumulator entry of a
 // lane belongs to one query (column l % 16): the running max / sum and the
 // output rescale are per-lane scalars, and the probabilities P^T are already
@@ -38,30 +40,41 @@ constexpr int krow(int dh) { return (dh / 8) % 2 ? dh : dh + 8; }
 // leave compute units idle, e.g. 1024 or 256 queries per head at batch 1).
 // KB: keys per block (64, or 128, which halves the barriers and max
 // reductions per key at the price of registers).
-template <int DH, int QB, int KB, int NW = 4>
+// KS: key splits.  With KS > 1 the NW waves form KS sets of NW / KS query
+// waves; every staged block holds KS * KB keys and set k multiplies its k-th
+// KB-key slice, so each query's keys are shared out over KS waves (more waves
+// per SIMD where the grid has few workgroups).  The sets' running maxima,
+// sums and output accumulators merge through LDS at the end (each rescaled by
+// 2^(its max - the largest)).
+template <int DH, int QB, int KB, int NW = 4, int KS = 1>
 __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
   constexpr int NT = NW * 64;  // threads; NW waves of QB query blocks share each K / V^T block
-  constexpr int VROW = KB + 8;                 // halfs per LDS V^T row
-  constexpr int NH = KB / 16, NS = KB / 32;    // 16-key quarters, 32-key PV steps
+  constexpr int NQ = NW / KS;                  // query waves per key set
+  constexpr int KBS = KS * KB;                 // keys per staged block
+  constexpr int VROW = KBS + 8;                // halfs per LDS V^T row
+  constexpr int NH = KB / 16, NS = KB / 32;    // 16-key quarters, 32-key PV steps of a slice
   constexpr int N32 = (DH + 31) / 32;          // 32-wide head-dim steps, dims past DH zero
   constexpr int DV = (DH + 15) / 16 * 16;      // output rows of O^T (padded)
   constexpr int KCH = DH / 8;                  // 16-byte chunks of a key row
   constexpr int KROW = krow(DH);               // halfs per LDS key row
-  constexpr int KCN = KB * KCH, VCN = DH * (KB / 8);  // chunks per K / V^T block
+  constexpr int KCN = KBS * KCH, VCN = DH * (KBS / 8);  // chunks per K / V^T block
   constexpr int KPT = (KCN + NT - 1) / NT, VPT = (VCN + NT - 1) / NT;
   static_assert(DH % 8 == 0, "head dim");
+  static_assert(NW % KS == 0 && KB % 32 == 0, "key sets");
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16 (*sK)[KB * KROW] = (_Float16 (*)[KB * KROW])smem;                       // [2]
-  _Float16 (*sVt)[DV * VROW] = (_Float16 (*)[DV * VROW])(smem + 2 * KB * KROW * 2);  // [2]
+  _Float16 (*sK)[KBS * KROW] = (_Float16 (*)[KBS * KROW])smem;                       // [2]
+  _Float16 (*sVt)[DV * VROW] = (_Float16 (*)[DV * VROW])(smem + 2 * KBS * KROW * 2);  // [2]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qw = wave % NQ, kset = wave / NQ;  // query wave, key set
   const int li = lane & 15, kc = lane >> 4;
   // 1-D grid; an XCD owns a contiguous range of (row, head, query block) ids so
   // the query blocks of one head share its K / V through that XCD's L2
-  const int nqb = (a.S + NW * 16 * QB - 1) / (NW * 16 * QB);
+  const int nqb = (a.S + NQ * 16 * QB - 1) / (NQ * 16 * QB);
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int qblk = id % nqb, head = (id / nqb) % a.heads, row = id / (nqb * a.heads);
-  const int q0 = qblk * (NW * 16 * QB) + wave * (16 * QB);
+  const int q0 = qblk * (NQ * 16 * QB) + qw * (16 * QB);
 
   // Q^T fragments (B operand): query q0 + qb*16 + li, dims ks*32 + kc*8 .. +8,
   // zero past DH, scaled by scale * log2(e) so the scores come out of the
@@ -97,7 +110,7 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
   // the same multiply then accumulates the softmax denominator in O^T row DH.
   constexpr bool ONES = DV > DH;
 
-  const int nkb = (a.L + KB - 1) / KB;
+  const int nkb = (a.L + KBS - 1) / KBS;
 
   // K and V^T tiles through buffer descriptors over the whole tensors (the
   // launcher checks both stay under 2 GiB): each thread's byte offsets of
@@ -121,11 +134,11 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
     const int c = tid + i * NT;
-    voff[i] = c < VCN ? (uint32_t)((((int64_t)head * DH + c / (KB / 8)) * a.vt_ld +
-                                    (int64_t)row * a.vt_row + (c % (KB / 8)) * 8) * 2)
+    voff[i] = c < VCN ? (uint32_t)((((int64_t)head * DH + c / (KBS / 8)) * a.vt_ld +
+                                    (int64_t)row * a.vt_row + (c % (KBS / 8)) * 8) * 2)
                       : OOB;
   }
-  const uint32_t kstep = (uint32_t)KB * a.ldk * 2, vstep = KB * 2;
+  const uint32_t kstep = (uint32_t)KBS * a.ldk * 2, vstep = KBS * 2;
 
   // Two register sets: block kb + 2 is requested while block kb is multiplied
   // and block kb + 1 waits in the other set (two blocks of latency hiding).
@@ -146,14 +159,14 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
-      if (KCN % 256 == 0 || c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
+      if (KCN % NT == 0 || c < KCN) *(uint4*)&sK[buf][(c / KCH) * KROW + (c % KCH) * 8] = rk[i];
     }
-    if ((kb + 1) * KB <= a.L) {  // uniform: every key of the block is real
+    if ((kb + 1) * KBS <= a.L) {  // uniform: every key of the block is real
 #pragma unroll
       for (int i = 0; i < VPT; ++i) {
         const int c = tid + i * NT;
-        if (VCN % 256 == 0 || c < VCN)
-          *(uint4*)&sVt[buf][(c / (KB / 8)) * VROW + (c % (KB / 8)) * 8] = rv[i];
+        if (VCN % NT == 0 || c < VCN)
+          *(uint4*)&sVt[buf][(c / (KBS / 8)) * VROW + (c % (KBS / 8)) * 8] = rv[i];
       }
       return;
     }
@@ -161,9 +174,9 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + i * NT;
       if (c < VCN) {
-        const int d = c / (KB / 8), k8 = (c % (KB / 8)) * 8;
+        const int d = c / (KBS / 8), k8 = (c % (KBS / 8)) * 8;
         half8 v = *(const half8*)&rv[i];
-        const int past = kb * KB + k8 + 8 - a.L;  // keys of this chunk at or past L
+        const int past = kb * KBS + k8 + 8 - a.L;  // keys of this chunk at or past L
         if (past > 0)
 #pragma unroll
           for (int e = 0; e < 8; ++e)
@@ -179,112 +192,118 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
                   const uint4(&Sv)[VPT]) {
     const int cur = kb & 1;
     if (kb + 2 < nkb) fetch(kb + 2, Fk, Fv);
-    const _Float16* K_ = sK[cur];
-    const _Float16* V_ = sVt[cur];
-    // Scores relative to the reference max come straight out of the multiply:
-    // the accumulators start at -base (base = the query's reference max, 0
-    // before the first block).
-    float base[QB];
+    const int key0 = kb * KBS + kset * KB;  // first key of this wave's slice
+    // a slice wholly past L (last block only) adds nothing; uniform per wave
+    if (KS == 1 || key0 < a.L) {
+      const _Float16* K_ = sK[cur] + kset * KB * KROW;
+      const _Float16* V_ = sVt[cur] + kset * KB;
+      // Scores relative to the reference max come straight out of the multiply:
+      // the accumulators start at -base (base = the query's reference max, 0
+      // before the first block).
+      float base[QB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) base[qb] = mrun[qb] == -INFINITY ? 0.f : mrun[qb];
-    // S^T - base for NH key quarters x QB query blocks; lane holds keys
-    // h*16 + 4*kc + r.
-    floatx4 s[QB][NH];
+      for (int qb = 0; qb < QB; ++qb) base[qb] = mrun[qb] == -INFINITY ? 0.f : mrun[qb];
+      // S^T - base for NH key quarters x QB query blocks; lane holds keys
+      // h*16 + 4*kc + r.
+      floatx4 s[QB][NH];
 #pragma unroll
-    for (int h = 0; h < NH; ++h) {
-      const _Float16* kr = &K_[(h * 16 + li) * KROW];
-      half8 fk[N32];
-#pragma unroll
-      for (int ks = 0; ks < N32; ++ks)
-        fk[ks] = *(const half8*)(kr + (ks * 32 + kc * 8 < DH ? ks * 32 + kc * 8 : ks * 32));
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        s[qb][h] = floatx4{-base[qb], -base[qb], -base[qb], -base[qb]};
+      for (int h = 0; h < NH; ++h) {
+        const _Float16* kr = &K_[(h * 16 + li) * KROW];
+        half8 fk[N32];
 #pragma unroll
         for (int ks = 0; ks < N32; ++ks)
-          s[qb][h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
-      }
-    }
-    // Keys past L (last block only) score -inf.
-    if ((kb + 1) * KB > a.L) {
+          fk[ks] = *(const half8*)(kr + (ks * 32 + kc * 8 < DH ? ks * 32 + kc * 8 : ks * 32));
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+        for (int qb = 0; qb < QB; ++qb) {
+          s[qb][h] = floatx4{-base[qb], -base[qb], -base[qb], -base[qb]};
+#pragma unroll
+          for (int ks = 0; ks < N32; ++ks)
+            s[qb][h] =
+                __builtin_amdgcn_mfma_f32_16x16x32_f16(fk[ks], fq[qb][ks], s[qb][h], 0, 0, 0);
+        }
+      }
+      // Keys past L (last block only) score -inf.
+      if (key0 + KB > a.L) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int h = 0; h < NH; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (key0 + h * 16 + kc * 4 + r >= a.L) s[qb][h][r] = -INFINITY;
+      }
+      // Online softmax with a lazily moved reference: while no score of the wave
+      // exceeds its query's reference max by more than 2^RESCALE_LOG2 (p stays
+      // <= 256, exact enough in float16), the reference stays and nothing is
+      // rescaled; otherwise every lane moves to its new max, rescales, and
+      // shifts this block's relative scores by the move.
+      constexpr float RESCALE_LOG2 = 8.0f;
+      float mloc[QB];
+      bool grow = false;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float m = -INFINITY;
 #pragma unroll
         for (int h = 0; h < NH; ++h)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (kb * KB + h * 16 + kc * 4 + r >= a.L) s[qb][h][r] = -INFINITY;
-    }
-    // Online softmax with a lazily moved reference: while no score of the wave
-    // exceeds its query's reference max by more than 2^RESCALE_LOG2 (p stays
-    // <= 256, exact enough in float16), the reference stays and nothing is
-    // rescaled; otherwise every lane moves to its new max, rescales, and
-    // shifts this block's relative scores by the move.
-    constexpr float RESCALE_LOG2 = 8.0f;
-    float mloc[QB];
-    bool grow = false;
+          for (int r = 0; r < 4; ++r) m = fmaxf(m, s[qb][h][r]);
+        m = rows_max(m);
+        mloc[qb] = m;  // relative to base
+        grow |= !(m <= RESCALE_LOG2) || mrun[qb] == -INFINITY;
+      }
+      if (__ballot(grow)) {  // uniform: the whole wave moves its references
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float m = -INFINITY;
+        for (int qb = 0; qb < QB; ++qb) {
+          // new reference base + delta = max(reference, block max)
+          const float delta = mrun[qb] == -INFINITY ? mloc[qb] : fmaxf(mloc[qb], 0.f);
+          const float mnew = base[qb] + delta;
+          const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
+          mrun[qb] = mnew;
+          lrun[qb] *= alpha;
 #pragma unroll
-      for (int h = 0; h < NH; ++h)
+          for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) m = fmaxf(m, s[qb][h][r]);
-      m = rows_max(m);
-      mloc[qb] = m;  // relative to base
-      grow |= !(m <= RESCALE_LOG2) || mrun[qb] == -INFINITY;
-    }
-    if (__ballot(grow)) {  // uniform: the whole wave moves its references
+          for (int h = 0; h < NH; ++h) s[qb][h] -= delta;
+        }
+      }
+      half8 fp[QB][NS];
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        // new reference base + delta = max(reference, block max)
-        const float delta = mrun[qb] == -INFINITY ? mloc[qb] : fmaxf(mloc[qb], 0.f);
-        const float mnew = base[qb] + delta;
-        const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
-        mrun[qb] = mnew;
-        lrun[qb] *= alpha;
+        float psum = 0.f;
 #pragma unroll
-        for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= alpha;
+        for (int h = 0; h < NH; ++h)
 #pragma unroll
-        for (int h = 0; h < NH; ++h) s[qb][h] -= delta;
+          for (int r = 0; r < 4; ++r) {
+            const float p = __builtin_amdgcn_exp2f(s[qb][h][r]);
+            if (!ONES) psum += p;
+            fp[qb][h >> 1][(h & 1) * 4 + r] = (_Float16)p;
+          }
+        if (!ONES) lrun[qb] += psum;
       }
-    }
-    half8 fp[QB][NS];
+      // O^T += V^T P^T over two 32-key steps (rows d >= DH of the tile are never
+      // written; they only feed output rows that are not stored)
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float psum = 0.f;
+      for (int j = 0; j < DV / 16; ++j) {
 #pragma unroll
-      for (int h = 0; h < NH; ++h)
+        for (int st = 0; st < NS; ++st) {
+          const _Float16* vr = &V_[(j * 16 + li) * VROW + st * 32];
+          const half4 lo = *(const half4*)(vr + kc * 4);
+          const half4 hi = *(const half4*)(vr + 16 + kc * 4);
+          half8 fv;
+          fv[0] = lo[0]; fv[1] = lo[1]; fv[2] = lo[2]; fv[3] = lo[3];
+          fv[4] = hi[0]; fv[5] = hi[1]; fv[6] = hi[2]; fv[7] = hi[3];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[qb][h][r]);
-          if (!ONES) psum += p;
-          fp[qb][h >> 1][(h & 1) * 4 + r] = (_Float16)p;
+          for (int qb = 0; qb < QB; ++qb)
+            acc[qb][j] =
+                __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp[qb][st], acc[qb][j], 0, 0, 0);
         }
-      if (!ONES) lrun[qb] += psum;
-    }
-    // O^T += V^T P^T over two 32-key steps (rows d >= DH of the tile are never
-    // written; they only feed output rows that are not stored)
-#pragma unroll
-    for (int j = 0; j < DV / 16; ++j) {
-#pragma unroll
-      for (int st = 0; st < NS; ++st) {
-        const _Float16* vr = &V_[(j * 16 + li) * VROW + st * 32];
-        const half4 lo = *(const half4*)(vr + kc * 4);
-        const half4 hi = *(const half4*)(vr + 16 + kc * 4);
-        half8 fv;
-        fv[0] = lo[0]; fv[1] = lo[1]; fv[2] = lo[2]; fv[3] = lo[3];
-        fv[4] = hi[0]; fv[5] = hi[1]; fv[6] = hi[2]; fv[7] = hi[3];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          acc[qb][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fv, fp[qb][st], acc[qb][j], 0, 0, 0);
       }
-    }
+    }  // slice holds keys
     if (kb + 1 < nkb) stash(cur ^ 1, kb + 1, Sk, Sv);
     __syncthreads();
   };
   if (ONES)
-    for (int i = tid; i < 2 * KB; i += NT) sVt[i / KB][DH * VROW + i % KB] = (_Float16)1.0f;
+    for (int i = tid; i < 2 * KBS; i += NT) sVt[i / KBS][DH * VROW + i % KBS] = (_Float16)1.0f;
   fetch(0, rkA, rvA);
   if (1 < nkb) fetch(1, rkB, rvB);
   stash(0, 0, rkA, rvA);
@@ -292,6 +311,54 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
   for (int kb = 0; kb < nkb; kb += 2) {  // unrolled by two: the register sets stay static
     body(kb, rkA, rvA, rkB, rvB);
     if (kb + 1 < nkb) body(kb + 1, rkB, rvB, rkA, rvA);
+  }
+  if constexpr (KS > 1) {
+    // Key sets 1.. hand their reference maxima, partial sums and accumulators
+    // to set 0 through LDS (free again after the loop's last barrier), field
+    // by field with consecutive lanes at consecutive words.  A set whose
+    // slices were all past L holds max -inf and contributes 2^-inf = 0; set 0
+    // always holds key 0.
+    constexpr int NF = 2 + 4 * (DV / 16);
+    float* xch = (float*)smem;
+    if (kset > 0) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float* slot = xch + ((((kset - 1) * NQ + qw) * QB + qb) * NF) * 64 + lane;
+        slot[0] = mrun[qb];
+        slot[64] = lrun[qb];
+#pragma unroll
+        for (int j = 0; j < DV / 16; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) slot[(2 + 4 * j + r) * 64] = acc[qb][j][r];
+      }
+    }
+    __syncthreads();
+    if (kset > 0) return;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mk[KS];
+      mk[0] = mrun[qb];
+      float mx = mk[0];
+#pragma unroll
+      for (int k = 1; k < KS; ++k) {
+        mk[k] = xch[((((k - 1) * NQ + qw) * QB + qb) * NF) * 64 + lane];
+        mx = fmaxf(mx, mk[k]);
+      }
+      const float f0 = __builtin_amdgcn_exp2f(mk[0] - mx);
+      lrun[qb] *= f0;
+#pragma unroll
+      for (int j = 0; j < DV / 16; ++j) acc[qb][j] *= f0;
+#pragma unroll
+      for (int k = 1; k < KS; ++k) {
+        const float* slot = xch + ((((k - 1) * NQ + qw) * QB + qb) * NF) * 64 + lane;
+        const float f = __builtin_amdgcn_exp2f(mk[k] - mx);
+        lrun[qb] += f * slot[64];
+#pragma unroll
+        for (int j = 0; j < DV / 16; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[qb][j][r] += f * slot[(2 + 4 * j + r) * 64];
+      }
+    }
   }
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -320,13 +387,17 @@ __global__ void __launch_bounds__(NW * 64) attn_f16(AttnArgs a) {
   }
 }
 
-template <int DH, int QB, int KB, int NW = 4>
+template <int DH, int QB, int KB, int NW = 4, int KS = 1>
 hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
-  constexpr int DV = (DH + 15) / 16 * 16, VROW = KB + 8;
-  const size_t lds = (size_t)2 * (KB * krow(DH) + DV * VROW) * 2;
+  constexpr int DV = (DH + 15) / 16 * 16, KBS = KS * KB, VROW = KBS + 8;
+  // the ring, or the key sets' exchange after the loop if that is larger
+  constexpr size_t ring = (size_t)2 * (KBS * krow(DH) + DV * VROW) * 2;
+  constexpr size_t xch = (size_t)(KS - 1) * (NW / KS) * QB * (2 + 4 * (DV / 16)) * 64 * 4;
+  constexpr size_t lds = ring > xch ? ring : xch;
+  static_assert(lds <= 160 * 1024, "LDS per workgroup");
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB, NW>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_f16<DH, QB, KB, NW, KS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -338,13 +409,14 @@ hipError_t launch_qb(const AttnArgs& a, hipStream_t s) {
   if ((int64_t)a.rows * a.L * a.ldk * 2 >= 0x80000000ll ||
       (int64_t)a.heads * DH * a.vt_ld * 2 >= 0x80000000ll)
     return hipErrorInvalidValue;
-  dim3 grid((unsigned)(ceil_div(a.S, NW * 16 * QB) * a.heads * a.rows));
+  dim3 grid((unsigned)(ceil_div(a.S, NW / KS * 16 * QB) * a.heads * a.rows));
   const double flops = 4.0 * a.S * (double)a.L * a.dh * a.heads * a.rows;
   const double bytes = 2.0 * a.rows * a.heads * a.dh * (2.0 * a.S + 2.0 * a.L);
   const TraceEv ev = trace_begin(NV_FAM_ATTN, flops, bytes,
                                  TraceShape{a.S, a.L, (int64_t)a.heads * a.dh,
-                                            DH * 10000 + QB * 1000 + KB + (NW - 4) * 100000});
-  hipExtLaunchKernelGGL((attn_f16<DH, QB, KB, NW>), grid, dim3(NW * 64), (uint32_t)lds, s, ev.a,
+                                            DH * 10000 + QB * 1000 + KB + (NW - 4) * 100000 +
+                                                (KS - 1) * 1000000});
+  hipExtLaunchKernelGGL((attn_f16<DH, QB, KB, NW, KS>), grid, dim3(NW * 64), (uint32_t)lds, s, ev.a,
                         ev.b, 0u, a);
   return hipGetLastError();
 }
@@ -355,20 +427,31 @@ template <int DH>
 hipError_t launch(const AttnArgs& a, hipStream_t s) {
   const int64_t wgs2 = ceil_div(a.S, 128) * a.heads * a.rows;
   if (wgs2 < 256) {
-    // 80-dim heads over at most one workgroup per CU (batch 1 at 1,024
-    // queries): 128-key blocks; the kernel holds one wave per SIMD either way
+    // Grids of at most one four-wave workgroup per CU leave one wave per SIMD;
+    // two key sets double the waves.  80-dim heads over at most 256 workgroups
+    // of 64 queries (batch 1 at 1,024 queries): two sets of four waves on
+    // 64-key slices (graph-timed 18.7 -> 17.0 us self-attention, 6.7 -> 6.5 us
+    // over the 77-token context); 160-dim heads (batch 1 at 256 and 64
+    // queries): workgroups of 32 queries, two sets of two waves on 32-key
+    // slices (256 x 256: 10.9 -> 8.8 us, 256 x 77: 8.4 -> 7.1 us, 64 x 77:
+    // 8.3 -> 7.0 us).
     if constexpr (DH == 80)
-      if (ceil_div(a.S, 64) * a.heads * a.rows <= 256) return launch_qb<DH, 1, 128>(a, s);
+      if (ceil_div(a.S, 64) * a.heads * a.rows <= 256) return launch_qb<DH, 1, 64, 8, 2>(a, s);
+    if constexpr (DH == 160) return launch_qb<DH, 1, 32, 4, 2>(a, s);
     return launch_qb<DH, 1, 64>(a, s);
   }
-  // 40-dim heads: eight waves (256 queries) share each K / V^T block, which
-  // halves the block loads and LDS stores per query (graph-timed, interleaved:
-  // 2 x 4096 x 4096 76.8 -> 73.4 us, 16 rows 513 -> 486 us); 128-key blocks
-  // when at most two four-wave workgroups per CU would exist (batch 1 at 4,096
-  // queries), 64-key blocks on larger grids.  Other head dims measured slower
-  // with eight waves.
-  if constexpr (DH == 40)
-    return wgs2 <= 512 ? launch_qb<DH, 2, 128, 8>(a, s) : launch_qb<DH, 2, 64, 8>(a, s);
+  // 40-dim heads: eight query waves (256 queries) share each K / V^T block,
+  // which halves the block loads and LDS stores per query (graph-timed,
+  // interleaved: 2 x 4096 x 4096 76.8 -> 73.4 us, 16 rows 513 -> 486 us).  At
+  // most two four-wave workgroups per CU (batch 1 at 4,096 queries): over more
+  // than one 128-key block, two key sets of eight waves on 64-key slices
+  // (sixteen waves, 71.9 -> 66.7 us at 2 x 4096 x 4096), else 128-key blocks;
+  // 64-key blocks on larger grids.  Other head dims measured slower with eight
+  // query waves.
+  if constexpr (DH == 40) {
+    if (wgs2 > 512) return launch_qb<DH, 2, 64, 8>(a, s);
+    return a.L > 128 ? launch_qb<DH, 2, 64, 16, 2>(a, s) : launch_qb<DH, 2, 128, 8>(a, s);
+  }
   return launch_qb<DH, 2, 64>(a, s);
 }
 

@@ -2,10 +2,14 @@
 Sec. 2.1) against the oracle's float32 attention on the same float16-valued
 inputs, at the head dims of the configurations (16 tiny, 40 / 80 / 160
 SD-1.5, 64 SDXL), the 77-token context with its padded V^T rows, ragged
-query / key counts, and each launch form (one query block per wave; two, with
-eight waves sharing each key block for 40-dim heads: 128-key blocks at up to
-512 four-wave workgroups, as at batch 1 over 4,096 queries, 64-key blocks
-beyond; two with four waves for the other head dims).
+query / key counts, and each launch form (one query block per wave, with two
+key sets splitting every key block for 80-dim heads over at most 256
+workgroups of 64 queries and for 160-dim heads on small grids; two query
+blocks per wave, with eight query waves sharing each key block for 40-dim
+heads: two key sets of eight waves at up to 512 four-wave workgroups over more
+than 128 keys, as at batch 1 over 4,096 queries, 128-key blocks at that grid
+size otherwise, 64-key blocks beyond; two with four waves for the other head
+dims).  The key-set cases include slices that hold a single key or none.
 
 The peaked-score cases drive the online softmax through its rescale branch:
 the kernel keeps a per-query reference maximum and moves it (multiplying the
@@ -32,7 +36,11 @@ pytestmark = pytest.mark.gpu
                                                (2, 2048, 333, 8, 40), (3, 4096, 200, 8, 40),
                                                (16, 256, 256, 8, 160), (16, 256, 77, 8, 160),
                                                (16, 1024, 77, 8, 80), (2, 4096, 4096, 8, 40),
-                                               (1, 2000, 1000, 16, 40), (2, 2048, 128, 8, 40)])
+                                               (1, 2000, 1000, 16, 40), (2, 2048, 128, 8, 40),
+                                               (1, 128, 20, 4, 80), (2, 1000, 999, 8, 80),
+                                               (1, 100, 33, 2, 160), (1, 64, 20, 2, 160),
+                                               (2, 256, 256, 8, 160), (1, 4096, 130, 8, 40),
+                                               (2, 1024, 1024, 8, 80)])
 def test_attention(rows, S, L, heads, dh):
     print(f"op attention rows={rows} S={S} L={L} heads={heads} dh={dh}", flush=True)
     C = heads * dh
@@ -66,23 +74,26 @@ def _check(q, k, v, heads, scale, atol):
 
 
 # Launch forms (the launcher's rule over wgs2 = ceil(S / 128) * heads * rows):
-# wgs2 < 256 -> one query block per wave with 64-key blocks, or 128-key blocks
-# for 80-dim heads with at most 256 workgroups of 64 queries; otherwise two query
-# blocks per wave: 40-dim heads in eight-wave workgroups (256 queries) with
-# 128-key blocks up to wgs2 = 512 and 64-key blocks beyond, other head dims in
-# four-wave workgroups with 64-key blocks.
+# wgs2 < 256 -> one query block per wave: 80-dim heads with at most 256
+# workgroups of 64 queries in two key sets of four waves on 64-key slices,
+# 160-dim heads in workgroups of 32 queries with two key sets of two waves on
+# 32-key slices, otherwise four waves with 64-key blocks; wgs2 >= 256 -> two
+# query blocks per wave: 40-dim heads with eight query waves (256 queries),
+# up to wgs2 = 512 in two key sets on 64-key slices when L > 128 (128-key
+# blocks otherwise) and with 64-key blocks beyond, other head dims in four-wave
+# workgroups with 64-key blocks.
 PEAK_CASES = [  # (rows, S, L, heads, dh): form
     (1, 256, 700, 8, 40),    # 1 x 64
-    (2, 2048, 700, 8, 40),   # 2 x 128, eight waves
+    (2, 2048, 700, 8, 40),   # 2 x 64 x 2 key sets, sixteen waves
     (3, 4096, 700, 8, 40),   # 2 x 64, eight waves
-    (2, 2048, 704, 8, 40),   # 2 x 128, eight waves
-    (1, 4000, 1000, 8, 40),  # 2 x 128, eight waves, ragged queries and last key block
+    (2, 2048, 704, 8, 40),   # 2 x 64 x 2 key sets, sixteen waves
+    (1, 4000, 1000, 8, 40),  # 2 x 64 x 2 key sets, ragged queries and last key block
     (1, 300, 700, 8, 64),    # 1 x 64
     (2, 2048, 700, 8, 64),   # 2 x 64
     (1, 2100, 700, 8, 80),   # 1 x 64 (264 workgroups of 64 queries)
-    (1, 2048, 700, 8, 80),   # 1 x 128
+    (1, 2048, 700, 8, 80),   # 1 x 64 x 2 key sets
     (16, 1024, 700, 8, 80),  # 2 x 64
-    (2, 200, 700, 8, 160),   # 1 x 64
+    (2, 200, 700, 8, 160),   # 1 x 32 x 2 key sets
     (16, 256, 700, 8, 160),  # 2 x 64
     (1, 250, 700, 4, 16),    # 1 x 64
     (8, 1024, 700, 4, 16),   # 2 x 64
