@@ -1149,7 +1149,11 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   // wide products just under the large-grid bound (batch-1 level-1 q|k|v,
   // 2048 x 1920 x 640: 15.2 -> 12.2 us graph-timed) take 64 x 128 tiles
   if (!split && t64 >= 768 && g.N >= 1920) return launch_s<MODE, 64, 128, 2>(g, 1, s);
-  return launch_s<MODE, 64, 64, GEMM_S64>(g, split ? split_to(t64, 700) : 1, s);
+  // convolutions aim at fewer workgroups in total: fewer float32 partials to
+  // write and sum (b1 guided step: the batch-1 8 x 8 convolutions at 12 splits
+  // instead of 17, 5.365 -> 5.318 ms; 15 splits 5.360, 10 splits 5.346)
+  return launch_s<MODE, 64, 64, GEMM_S64>(
+      g, split ? split_to(t64, MODE == 1 ? 480 : 700) : 1, s);
 }
 
 template <int MODE>
