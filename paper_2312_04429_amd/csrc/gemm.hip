@@ -891,12 +891,13 @@ __global__ void __launch_bounds__(NW * 64) gemm_s(GemmArgs g, int kt_per_split) 
 // still run in split order, so the sum does not change.
 constexpr int RED_CHUNK = 8;
 
-// NQ quads at p + k * off (k < NQ), each summed over the splits into v[k].
+// NQ quads at p + k * off (k < NQ), each summed over splits s_lo .. splits - 1
+// into v[k].
 template <int NQ>
 __device__ inline void sum_splits(const float* __restrict__ p, int off, int64_t MN, int splits,
-                                  float (&v)[NQ][4]) {
+                                  float (&v)[NQ][4], int s_lo = 0) {
   constexpr int CH = RED_CHUNK / NQ;
-  for (int s0 = 0; s0 < splits; s0 += CH) {
+  for (int s0 = s_lo; s0 < splits; s0 += CH) {
     float4 q[CH][NQ];
 #pragma unroll
     for (int u = 0; u < CH; ++u)
@@ -913,12 +914,19 @@ __device__ inline void sum_splits(const float* __restrict__ p, int off, int64_t 
   }
 }
 
+// P threads (adjacent lanes) per output quad where more than RED_CHUNK splits
+// would take a second round of loads: lane j of the P sums its share of the
+// splits in one round, and the shares are added in a fixed tree (lane pairs,
+// then pairs of pairs), so the result stays the same from call to call.
+template <int P>
 __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
+  static_assert(P == 1 || P == 2 || P == 4, "threads per quad");
   const int64_t MN = g.M * (int64_t)g.N;
   const int nq = g.N / 4;
   const int64_t total = g.geglu ? g.M * (int64_t)(g.N / 32) * 4 : g.M * (int64_t)nq;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * 256) {
+  const int sub = threadIdx.x % P, per = (splits + P - 1) / P;
+  for (int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) / P; e < total;
+       e += (int64_t)gridDim.x * (256 / P)) {
     if (g.geglu) {  // e -> (row, 32-column group, quad of the 16 "a" columns)
       const int per_row = (g.N / 32) * 4;
       const int64_t m = e / per_row;
@@ -953,7 +961,16 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
         }
       }
       float v[1][4] = {{0.f, 0.f, 0.f, 0.f}};
-      sum_splits<1>(g.partial + m * g.N + n, 0, MN, splits, v);
+      if (P == 1) {
+        sum_splits<1>(g.partial + m * g.N + n, 0, MN, splits, v);
+      } else {
+        sum_splits<1>(g.partial + m * g.N + n, 0, MN, min(splits, (sub + 1) * per), v, sub * per);
+#pragma unroll
+        for (int o = 1; o < P; o <<= 1)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[0][r] += __shfl_xor(v[0][r], o, 64);
+        if (sub != 0) continue;
+      }
       float w[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -993,6 +1010,21 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
   }
 }
 
+// Split-K reduction: one thread per output quad up to RED_CHUNK splits, two
+// or four beyond (each then loads its share in one round).
+hipError_t reduce_launch(const GemmArgs& g, int splits, hipStream_t s) {
+  const int P = g.geglu || splits <= RED_CHUNK ? 1 : splits <= 2 * RED_CHUNK ? 2 : 4;
+  const int64_t total = g.M * (int64_t)(g.N / 4) * P;
+  const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+  if (P == 1)
+    hipLaunchKernelGGL(splitk_reduce<1>, dim3(blocks), dim3(256), 0, s, g, splits);
+  else if (P == 2)
+    hipLaunchKernelGGL(splitk_reduce<2>, dim3(blocks), dim3(256), 0, s, g, splits);
+  else
+    hipLaunchKernelGGL(splitk_reduce<4>, dim3(blocks), dim3(256), 0, s, g, splits);
+  return hipGetLastError();
+}
+
 template <int MODE, int BM, int BN, bool DUAL>
 hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
   if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
@@ -1020,11 +1052,7 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
       trace_begin(fam, flops, bytes, TraceShape{g.M, g.N, g.K, BM * 10000 + BN * 10 + splits});
   hipExtLaunchKernelGGL((gemm_f16<MODE, BM, BN, DUAL>), grid, dim3(256), (uint32_t)lds, s, ev.a,
                         ev.b, 0u, g, kps);
-  if (splits > 1) {
-    const int64_t total = g.M * (int64_t)(g.N / 4);
-    const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
-    hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
-  }
+  if (splits > 1) return reduce_launch(g, splits, s);
   return hipGetLastError();
 }
 
@@ -1055,11 +1083,7 @@ hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
       trace_begin(fam, flops, bytes, TraceShape{g.M, g.N, g.K, BM * 10000 + BN * 10 + splits});
   hipExtLaunchKernelGGL((gemm_s<MODE, BM, BN, STAGES, LN, U, NW>), grid, dim3(NW * 64),
                         (uint32_t)lds, s, ev.a, ev.b, 0u, g, kps);
-  if (splits > 1) {
-    const int64_t total = g.M * (int64_t)(g.N / 4);
-    const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
-    hipLaunchKernelGGL(splitk_reduce, dim3(blocks), dim3(256), 0, s, g, splits);
-  }
+  if (splits > 1) return reduce_launch(g, splits, s);
   return hipGetLastError();
 }
 
