@@ -1163,9 +1163,10 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
     return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 512), s);
   // deep convolutions over mid-sized grids (batch 1 at 32 x 32 and 16 x 16):
   // 128 x 128 tiles halve the bytes per flop, split K refills the chip
-  // (graph-timed 47 against 64 us at 32 x 32 with 1280 input channels)
+  // (graph-timed 47 against 64 us at 32 x 32 with 1280 input channels); eight
+  // waves (b1 guided step 5.296 -> 5.279 ms against four)
   if (MODE == 1 && t128 >= 32 && t128 <= 128 && nk >= 80)
-    return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 700), s);
+    return launch_s<MODE, 128, 128, GEMM_S128, 1, 8>(g, split_to(t128, 700), s);
   // split K past 40 k tiles, or below about 100 tiles (graph-timed alone:
   // 2048 x 640 x 2560 22.2 -> 19.6 us and 512 x 1280 x 2560 17.9 -> 15.9 us
   // unsplit, 128 x 3840 x 1280 10.8 -> 9.5 us)

@@ -4,8 +4,8 @@ inputs.  Shapes cover every tile configuration of both kernels (register
 staged for K or channel counts off the 64 grid; streamed 64x64 with and
 without split-K (including one workgroup per CU over a long K, and at most
 128 rows with ragged N over a long K), 64x128, 128x128 with eight waves for
-large grids (dense and convolution, ragged rows and columns) and with four for
-long K with split),
+large grids (dense and convolution, ragged rows and columns) and for deep
+convolutions over mid-sized grids with split, with four for long K with split),
 ragged M / N / K edges, stride 2 and the fused nearest x2 upsample."""
 import numpy as np
 import pytest
@@ -71,7 +71,8 @@ def test_split_k_repeatable():
     (2, 32, 32, 640, 640, 2, 0), (2, 8, 8, 1280, 1280, 1, 0), (2, 16, 16, 96, 32, 1, 1),
     (3, 8, 8, 640, 640, 1, 1), (2, 8, 6, 64, 40, 2, 0), (2, 64, 64, 64, 1024, 1, 0),
     (2, 32, 32, 1024, 1024, 1, 0), (2, 64, 64, 64, 640, 1, 0), (2, 32, 32, 128, 256, 1, 0),
-    (1, 8, 8, 640, 1000, 1, 0), (4, 64, 64, 64, 320, 1, 0), (4, 32, 32, 64, 320, 1, 1)])
+    (1, 8, 8, 640, 1000, 1, 0), (4, 64, 64, 64, 320, 1, 0), (4, 32, 32, 64, 320, 1, 1),
+    (2, 16, 16, 1280, 1280, 1, 0), (2, 32, 32, 640, 640, 1, 0)])
 def test_conv3x3(B, H, W, Cin, Cout, stride, up):
     import paper_2312_04429_amd as P
     print(f"op conv B={B} {H}x{W} {Cin}->{Cout} s{stride} up{up}", flush=True)
