@@ -1151,13 +1151,16 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
     // 16384 x 5120 x 640 182 -> 168 us, 65536 x 2560 x 320 258 -> 226 us, the
     // 320-channel convolution over 65536 pixels 161 -> 148 us); dense products
     // over at least 8192 rows and 960 columns take them too (8192 x 960 x 320
-    // 17.0 -> 14.3 us, 8192 x 2560 x 320 32.7 -> 30.2 us against 64 x 128)
+    // 17.0 -> 14.3 us, 8192 x 2560 x 320 32.7 -> 30.2 us against 64 x 128).
+    // 64 x 128 tiles run eight waves as well (2 x 4 wave tiles of 32 x 32; guided
+    // steps, same box: b1 5.257 -> 5.232 ms, b8 2.982 -> 2.965 ms, SDXL 22.27 ->
+    // 22.09 ms, with the wide products below)
     const bool big = (g.N >= 2560 && t128 >= 1536) || g.K >= 8192 || g.N <= 320 ||
                      (g.M >= 4096 && g.N >= 2560 && g.K >= 1280) ||
                      (g.M >= 4096 && g.N >= 1280 && g.K >= 4096) ||
                      (MODE == 0 && g.M >= 8192 && g.N >= 960);
     return big ? launch_s<MODE, 128, 128, GEMM_S128, 1, 8>(g, 1, s)
-               : launch_s<MODE, 64, 128, 2>(g, 1, s);
+               : launch_s<MODE, 64, 128, 2, 1, 8>(g, 1, s);
   }
   if (t128 >= 128 && nk >= 128)
     return launch_s<MODE, 128, 128, GEMM_S128>(g, split_to(t128, 512), s);
@@ -1173,7 +1176,7 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   const bool split = nk > 40 || t64 < 100;
   // wide products just under the large-grid bound (batch-1 level-1 q|k|v,
   // 2048 x 1920 x 640: 15.2 -> 12.2 us graph-timed) take 64 x 128 tiles
-  if (!split && t64 >= 768 && g.N >= 1920) return launch_s<MODE, 64, 128, 2>(g, 1, s);
+  if (!split && t64 >= 768 && g.N >= 1920) return launch_s<MODE, 64, 128, 2, 1, 8>(g, 1, s);
   // convolutions aim at fewer workgroups in total: fewer float32 partials to
   // write and sum (b1 guided step: the batch-1 8 x 8 convolutions at 12 splits
   // instead of 17, 5.365 -> 5.318 ms; 15 splits 5.360, 10 splits 5.346)
