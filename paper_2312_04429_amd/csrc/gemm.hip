@@ -1058,6 +1058,8 @@ hipError_t launch_t(const GemmArgs& g, int splits, hipStream_t s) {
 
 template <int MODE, int BM, int BN, int STAGES, bool LN, int U = 1, int NW = 4>
 hipError_t launch_s_t(const GemmArgs& g, int splits, hipStream_t s) {
+  // the GEGLU epilogue pairs a wave's 16-column quads: at least 32 columns per wave
+  if (g.geglu && splits <= 1 && BN / (NW / 2) < 32) return hipErrorInvalidValue;
   if (g.bytes1 >= 0x80000000u || g.bytes2 >= 0x80000000u ||
       (int64_t)g.N * g.ldw * 2 >= 0x80000000ll)
     return hipErrorInvalidValue;  // descriptors address less than 2 GiB (gemm_launch chunks)
@@ -1180,8 +1182,13 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   // convolutions aim at fewer workgroups in total: fewer float32 partials to
   // write and sum (b1 guided step: the batch-1 8 x 8 convolutions at 12 splits
   // instead of 17, 5.365 -> 5.318 ms; 15 splits 5.360, 10 splits 5.346)
-  return launch_s<MODE, 64, 64, GEMM_S64>(
-      g, split ? split_to(t64, MODE == 1 ? 480 : 700) : 1, s);
+  const int spl = split ? split_to(t64, MODE == 1 ? 480 : 700) : 1;
+  // up to about two workgroups per CU: eight waves in 2 x 4 wave tiles of
+  // 32 x 16 (b1 guided step 5.208 -> 5.131 ms; swept: 5.255 -> 5.198, 5.213
+  // with every 64 x 64 grid, 5.225 up to one workgroup per CU).  The GEGLU
+  // epilogue pairs 16-column quads inside a wave and keeps four.
+  if (!g.geglu && t64 * spl <= 512) return launch_s<MODE, 64, 64, GEMM_S64, 1, 8>(g, spl, s);
+  return launch_s<MODE, 64, 64, GEMM_S64>(g, spl, s);
 }
 
 template <int MODE>

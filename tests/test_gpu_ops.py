@@ -3,7 +3,8 @@ kernel) against the oracle's float32 layers on the same float16-valued
 inputs.  Shapes cover every tile configuration of both kernels (register
 staged for K or channel counts off the 64 grid; streamed 64x64 with and
 without split-K (including one workgroup per CU over a long K, and at most
-128 rows with ragged N over a long K), 64x128, 128x128 with eight waves for
+128 rows with ragged N over a long K; eight waves at up to two workgroups per
+CU), 64x128, 128x128 with eight waves for
 large grids (dense and convolution, ragged rows and columns) and for deep
 convolutions over mid-sized grids with split, with four for long K with split),
 ragged M / N / K edges, stride 2 and the fused nearest x2 upsample."""
