@@ -1185,9 +1185,10 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
   const int spl = split ? split_to(t64, MODE == 1 ? 480 : 700) : 1;
   // up to about two workgroups per CU: eight waves in 2 x 4 wave tiles of
   // 32 x 16 (b1 guided step 5.208 -> 5.131 ms; swept: 5.255 -> 5.198, 5.213
-  // with every 64 x 64 grid, 5.225 up to one workgroup per CU).  The GEGLU
-  // epilogue pairs 16-column quads inside a wave and keeps four.
-  if (!g.geglu && t64 * spl <= 512) return launch_s<MODE, 64, 64, GEMM_S64, 1, 8>(g, spl, s);
+  // with every 64 x 64 grid, 5.225 up to one workgroup per CU) and a four-tile
+  // ring, 64 KB, two workgroups per CU (5.131 -> 5.117 ms; two tiles 5.478).
+  // The GEGLU epilogue pairs 16-column quads inside a wave and keeps four.
+  if (!g.geglu && t64 * spl <= 512) return launch_s<MODE, 64, 64, 4, 1, 8>(g, spl, s);
   return launch_s<MODE, 64, 64, GEMM_S64>(g, spl, s);
 }
 
