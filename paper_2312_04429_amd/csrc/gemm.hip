@@ -1155,7 +1155,7 @@ hipError_t dispatch_streamed(const GemmArgs& g, hipStream_t s) {
     // over at least 8192 rows and 960 columns take them too (8192 x 960 x 320
     // 17.0 -> 14.3 us, 8192 x 2560 x 320 32.7 -> 30.2 us against 64 x 128).
     // 64 x 128 tiles run eight waves as well (2 x 4 wave tiles of 32 x 32; guided
-    // steps, same box: b1 5.257 -> 5.232 ms, b8 2.982 -> 2.965 ms, SDXL 22.27 ->
+    // steps measured together: b1 5.257 -> 5.232 ms, b8 2.982 -> 2.965 ms, SDXL 22.27 ->
     // 22.09 ms, with the wide products below)
     const bool big = (g.N >= 2560 && t128 >= 1536) || g.K >= 8192 || g.N <= 320 ||
                      (g.M >= 4096 && g.N >= 2560 && g.K >= 1280) ||
